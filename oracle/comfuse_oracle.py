@@ -1,0 +1,275 @@
+"""fp64 CPU oracle for the fused GEMM + row-subgraph operators.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the package's smoke check and
+the benchmark's CPU-baseline leg may import this module.  The HIP library
+never calls it, and this module imports nothing from the HIP path.
+
+What it computes
+----------------
+The paper's fusion (joint compute-memory operator fusion, Introduction and
+Sec. III) changes *where* intermediate values live: a dependency edge
+becomes a register channel instead of a buffer in global memory (Sec. III-A).
+It does not change *what* is computed.  The same holds for the B2BGEMM
+paradigm: S_tile = F(P_tile) and the cluster partial sums add up to S.W2 by
+linearity (Sec. IV-A, Eq. 2 and the partial-sum identity).  So the oracle is
+the plain, unfused definition: a matrix product in fp64, then each subgraph
+operator in order, with every intermediate kept in fp64 and never rounded.
+
+Inputs are taken as given (bf16 or fp32 values, upcast exactly to fp64).
+The matrix product is numpy's fp64 ``@`` (a library primitive).  Every other
+step is written out from its definition.  Row statistics are computed
+two-pass (mean first, then the mean of squared deviations), which is the
+textbook definition, not a streaming or merged form.
+
+Readings of points the paper leaves open are listed in the repository's
+design notes; the ones that change numbers are repeated at each function.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+from scipy.special import erf as _erf
+
+F64 = np.float64
+
+
+def _f64(a):
+    return None if a is None else np.asarray(a, dtype=F64)
+
+
+# --------------------------------------------------------------------------
+# The compute-intensive operator (MatMul; Sec. III "MainLoop", Eq. 2 P = X.W1)
+# --------------------------------------------------------------------------
+def matmul(A, B):
+    """C = A . B in fp64.  A is M x K, B is K x N (mathematical orientation).
+
+    The contraction of Sec. III (MatMul producing the accumulator tile) and of
+    Eq. 2 (P = X W1, O = S W2).  numpy's fp64 matrix product is the step.
+    """
+    return _f64(A) @ _f64(B)
+
+
+# --------------------------------------------------------------------------
+# Stage 1 of the post-norm subgraph: x = alpha * Acc + Bias (+ residual)
+# (Sec. III-B, bypass example; the residual is an elementwise add node)
+# --------------------------------------------------------------------------
+def bias_residual(P, bias=None, R=None, alpha=1.0):
+    """x_ij = alpha * p_ij + b_j + r_ij (the terms that are given)."""
+    x = F64(alpha) * _f64(P)
+    if bias is not None:
+        x = x + _f64(bias)[None, :]
+    if R is not None:
+        x = x + _f64(R)
+    return x
+
+
+# --------------------------------------------------------------------------
+# Reduction stages (Sec. III-A compute/reduce; Sec. III-B chaining)
+# --------------------------------------------------------------------------
+def row_mean(x):
+    """mu_i = (1/N) sum_j x_ij."""
+    x = _f64(x)
+    return x.sum(axis=1) / F64(x.shape[1])
+
+
+def row_var(x, mu):
+    """sigma^2_i = (1/N) sum_j (x_ij - mu_i)^2 (biased, two-pass)."""
+    x = _f64(x)
+    d = x - mu[:, None]
+    return (d * d).sum(axis=1) / F64(x.shape[1])
+
+
+def layernorm(x, gamma=None, beta=None, eps=1e-5):
+    """y_ij = (x_ij - mu_i) / sqrt(sigma^2_i + eps) * gamma_j + beta_j.
+
+    LayerNorm over each row (the reduction dimension of Sec. III, Eq. 1).
+    Reading: biased variance (divide by N), eps inside the square root;
+    gamma = 1 and beta = 0 when not given.
+    """
+    x = _f64(x)
+    mu = row_mean(x)
+    var = row_var(x, mu)
+    y = (x - mu[:, None]) / np.sqrt(var + F64(eps))[:, None]
+    if gamma is not None:
+        y = y * _f64(gamma)[None, :]
+    if beta is not None:
+        y = y + _f64(beta)[None, :]
+    return y
+
+
+def rmsnorm(x, gamma=None, eps=1e-5):
+    """y_ij = x_ij / sqrt((1/N) sum_j x_ij^2 + eps) * gamma_j (MBR, Sec. VI)."""
+    x = _f64(x)
+    ms = (x * x).sum(axis=1) / F64(x.shape[1])
+    y = x / np.sqrt(ms + F64(eps))[:, None]
+    if gamma is not None:
+        y = y * _f64(gamma)[None, :]
+    return y
+
+
+def softmax_rows(s):
+    """Plain two-pass softmax over each row: m = max, e = exp(s - m), e / sum e.
+
+    The softmax ReduceMode of the StreamReduction node (Sec. V).
+    """
+    s = _f64(s)
+    m = s.max(axis=1, keepdims=True)
+    e = np.exp(s - m)
+    return e / e.sum(axis=1, keepdims=True)
+
+
+# --------------------------------------------------------------------------
+# Elementwise nodes
+# --------------------------------------------------------------------------
+SQRT1_2 = 1.0 / math.sqrt(2.0)
+
+
+def gelu_erf(x):
+    """GELU(x) = x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)).
+
+    Reading: the paper does not define GELU; the exact (erf) form is used.
+    """
+    x = _f64(x)
+    return 0.5 * x * (1.0 + _erf(x * SQRT1_2))
+
+
+def gelu_tanh(x):
+    """tanh approximation 0.5 x (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))."""
+    x = _f64(x)
+    c = math.sqrt(2.0 / math.pi)
+    return 0.5 * x * (1.0 + np.tanh(c * (x + 0.044715 * x * x * x)))
+
+
+def relu(x):
+    x = _f64(x)
+    return np.where(x > 0.0, x, 0.0)
+
+
+def tanh_softcap(x, cap):
+    """cap * tanh(x / cap) (MSTS, Sec. VI; the softcap formula is a reading)."""
+    x = _f64(x)
+    return F64(cap) * np.tanh(x / F64(cap))
+
+
+# --------------------------------------------------------------------------
+# OCP 8-bit floating point, E4M3FN (target of the row-amax scale chain)
+# --------------------------------------------------------------------------
+E4M3_MAX = 448.0
+
+
+def e4m3_decode(code):
+    """Value of an OCP E4M3FN code (1 sign, 4 exponent bits with bias 7,
+    3 mantissa bits; exponent 0 is subnormal m/8 * 2^-6; S.1111.111 is NaN;
+    there is no infinity)."""
+    c = np.asarray(code, dtype=np.int64) & 0xFF
+    s = (c >> 7) & 1
+    e = (c >> 3) & 0xF
+    m = c & 7
+    mag = np.where(e == 0, (m / 8.0) * 2.0 ** -6,
+                   (1.0 + m / 8.0) * np.exp2(e.astype(F64) - 7.0))
+    val = np.where(s == 1, -mag, mag)
+    return np.where((e == 15) & (m == 7), np.nan, val)
+
+
+_E4M3_POS_CODES = np.arange(0x00, 0x7F)            # 0 .. 448, monotone
+_E4M3_POS_VALUES = e4m3_decode(_E4M3_POS_CODES)
+
+
+def e4m3_encode(x):
+    """Encode to E4M3FN: nearest representable value, ties to the code with the
+    even mantissa bit; magnitudes beyond 448 saturate to +-448; NaN -> 0x7F.
+
+    Written as a literal nearest-neighbour search over the 127 non-negative
+    finite values, so that it follows the definition rather than bit tricks.
+    """
+    x = _f64(x)
+    a = np.abs(x)
+    sign = np.signbit(x)
+    a_c = np.minimum(a, E4M3_MAX)
+    hi = np.searchsorted(_E4M3_POS_VALUES, a_c, side="left")
+    hi = np.clip(hi, 0, len(_E4M3_POS_VALUES) - 1)
+    lo = np.clip(hi - 1, 0, len(_E4M3_POS_VALUES) - 1)
+    d_lo = np.abs(a_c - _E4M3_POS_VALUES[lo])
+    d_hi = np.abs(_E4M3_POS_VALUES[hi] - a_c)
+    pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (_E4M3_POS_CODES[hi] % 2 == 0))
+    code = np.where(pick_hi, _E4M3_POS_CODES[hi], _E4M3_POS_CODES[lo]).astype(np.int64)
+    code = np.where(sign & (code != 0), code | 0x80, code)
+    code = np.where(sign & (code == 0), 0x80, code)   # keep the sign of -0
+    code = np.where(np.isnan(x), 0x7F, code)
+    return code.astype(np.uint8)
+
+
+def rowamax_quant(z, qmax=E4M3_MAX):
+    """Row-amax quantisation scale chain (a second reduction stage, Sec. III-B):
+    a_i = max_j |z_ij|, s_i = a_i / qmax, q_ij = e4m3(z_ij / s_i).
+
+    Reading: a row whose amax is 0 gets s_i = 0 and all-zero codes.
+    """
+    z = _f64(z)
+    a = np.abs(z).max(axis=1)
+    s = a / F64(qmax)
+    safe = np.where(s > 0.0, s, 1.0)
+    q = e4m3_encode(z / safe[:, None])
+    q = np.where((s > 0.0)[:, None], q, np.uint8(0)).astype(np.uint8)
+    return s, q
+
+
+# --------------------------------------------------------------------------
+# Composite operators (what the fused kernels compute end to end)
+# --------------------------------------------------------------------------
+def postnorm(X, W_kn, bias=None, R=None, gamma=None, beta=None, alpha=1.0,
+             eps=1e-5):
+    """Post-norm: Y = LN(alpha * X.W + bias + R) * gamma + beta.
+
+    The MatMul + LayerNorm case of the Stage-Stream model (Sec. III, the
+    MatMul + LayerNorm illustration; Sec. III-B x = alpha*Acc + Bias).
+    ``W_kn`` is K x N in mathematical orientation.
+    """
+    x = bias_residual(matmul(X, W_kn), bias, R, alpha)
+    return layernorm(x, gamma, beta, eps)
+
+
+def ln_gelu_amax(X, W_kn, bias=None, R=None, gamma=None, beta=None, eps=1e-5,
+                 gelu="erf", qmax=E4M3_MAX):
+    """Three-stage chain with two reductions (Sec. III-B chaining):
+    x = X.W + b + R ; y = LN(x) ; z = GELU(y) ; s = rowmax|z| / qmax ;
+    q = e4m3(z / s).  Returns (z, s, q); z is not rounded.
+    """
+    y = postnorm(X, W_kn, bias, R, gamma, beta, 1.0, eps)
+    z = gelu_erf(y) if gelu == "erf" else gelu_tanh(y)
+    s, q = rowamax_quant(z, qmax)
+    return z, s, q
+
+
+def ffn_b2b(X, W1_kn, b1, W2_kn, b2, gamma=None, beta=None, eps=1e-5):
+    """B2BGEMM FFN (Sec. IV, Eq. 2 with F = GELU(. + b1)), followed by a
+    residual + LayerNorm epilogue on the second product:
+    P = X.W1 ; S = GELU(P + b1) ; O = S.W2 ; Y = LN(O + b2 + X).
+    S is kept in fp64 (not rounded).
+    """
+    P = matmul(X, W1_kn)
+    S = gelu_erf(bias_residual(P, b1))
+    O = matmul(S, W2_kn)
+    return layernorm(bias_residual(O, b2, X), gamma, beta, eps)
+
+
+def attention(Q, K, V, scale=None):
+    """Attention-style B2BGEMM (Sec. IV with F = softmax(scale * .)) per
+    (batch, head): O = softmax(scale * Q.K^T) . V, plain two-pass softmax.
+
+    Q is [..., Lq, d], K and V are [..., Lk, d]; leading dims are batch/head.
+    """
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    d = Q.shape[-1]
+    if scale is None:
+        scale = 1.0 / math.sqrt(d)
+    lead = Q.shape[:-2]
+    Qf = Q.reshape((-1,) + Q.shape[-2:])
+    Kf = K.reshape((-1,) + K.shape[-2:])
+    Vf = V.reshape((-1,) + V.shape[-2:])
+    out = np.empty((Qf.shape[0], Qf.shape[1], V.shape[-1]), dtype=F64)
+    for i in range(Qf.shape[0]):
+        s = matmul(Qf[i], Kf[i].T) * F64(scale)
+        out[i] = matmul(softmax_rows(s), Vf[i])
+    return out.reshape(lead + out.shape[-2:])

@@ -1,0 +1,318 @@
+"""Pins for the fp64 oracle: each check compares it against something other
+than itself — exact rational arithmetic, mpmath at 40 digits, closed forms,
+textbook tables, invariants the mathematics fixes, or a library routine that
+is not the one the oracle calls.  Chosen so that a dropped term, a sign or
+index slip, or a transposed operand in the oracle fails at least one of them.
+"""
+import math
+import os
+from fractions import Fraction
+
+import mpmath
+import numpy as np
+import pytest
+import torch
+
+from oracle import comfuse_oracle as O
+from paper_2608_03537_amd import inputs as I
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+mpmath.mp.dps = 40
+
+
+def _fr(a):
+    return [[Fraction(float(v)) for v in row] for row in np.asarray(a, np.float64)]
+
+
+def _mm_exact(A, B):
+    A, B = _fr(A), _fr(B)
+    M, K, N = len(A), len(B), len(B[0])
+    return [[sum(A[i][k] * B[k][j] for k in range(K)) for j in range(N)] for i in range(M)]
+
+
+def _small(shape, seed, tid, std=1.0):
+    rng = np.random.default_rng([seed, 7777, tid])
+    return I.round_to_bf16((rng.standard_normal(shape) * std).astype(np.float32))
+
+
+# ---------------------------------------------------------------- matmul
+@pytest.mark.parametrize("M,K,N", [(4, 4, 4), (4, 8, 4), (3, 5, 7)])
+def test_matmul_exact_rational(M, K, N):
+    A, B = _small((M, K), 1, 0), _small((K, N), 1, 1)
+    ref = _mm_exact(A, B)
+    got = O.matmul(A, B)
+    for i in range(M):
+        for j in range(N):
+            # bf16 x bf16 products are exact in fp64; only the K-term sum rounds.
+            assert abs(Fraction(float(got[i, j])) - ref[i][j]) <= Fraction(K) * Fraction(2) ** -52 * (
+                abs(ref[i][j]) + 1)
+
+
+def test_matmul_orientation():
+    # A 2x3 times 3x2 with a hand-computed result: catches a transposed operand.
+    A = np.array([[1.0, 2.0, 3.0], [4.0, 5.0, 6.0]])
+    B = np.array([[7.0, 8.0], [9.0, 10.0], [11.0, 12.0]])
+    assert np.array_equal(O.matmul(A, B), np.array([[58.0, 64.0], [139.0, 154.0]]))
+
+
+# ---------------------------------------------------------------- bias / residual
+def test_bias_residual_exact():
+    P, R = _small((4, 4), 2, 0), _small((4, 4), 2, 1)
+    b = _small((4,), 2, 2)
+    got = O.bias_residual(P, b, R, alpha=0.5)
+    for i in range(4):
+        for j in range(4):
+            ref = Fraction(1, 2) * Fraction(float(P[i, j])) + Fraction(float(b[j])) + Fraction(float(R[i, j]))
+            assert Fraction(float(got[i, j])) == ref  # small bf16 sums are exact in fp64
+
+
+# ---------------------------------------------------------------- LayerNorm
+def _ln_mp(row, gamma, beta, eps):
+    fr = [v if isinstance(v, Fraction) else Fraction(float(v)) for v in row]
+    n = len(fr)
+    mu = sum(fr) / n
+    var = sum((v - mu) ** 2 for v in fr) / n
+    rstd = 1 / mpmath.sqrt(mpmath.mpf(var.numerator) / var.denominator + mpmath.mpf(eps))
+    out = []
+    for j, v in enumerate(fr):
+        d = mpmath.mpf((v - mu).numerator) / (v - mu).denominator
+        out.append(d * rstd * mpmath.mpf(float(gamma[j])) + mpmath.mpf(float(beta[j])))
+    return mu, var, out
+
+
+def test_layernorm_exact_stats_4x4():
+    x = _small((4, 4), 3, 0, std=3.0)
+    g = 1.0 + _small((4,), 3, 1, std=0.3)
+    b = _small((4,), 3, 2, std=0.3)
+    y = O.layernorm(x, g, b, 1e-5)
+    mu = O.row_mean(x)
+    var = O.row_var(x, mu)
+    for i in range(4):
+        mu_r, var_r, y_r = _ln_mp(x[i], g, b, 1e-5)
+        assert abs(Fraction(float(mu[i])) - mu_r) <= abs(mu_r) * Fraction(1, 10 ** 15) + Fraction(1, 10 ** 300)
+        assert abs(Fraction(float(var[i])) - var_r) <= var_r * Fraction(1, 10 ** 14)
+        for j in range(4):
+            assert abs(float(y[i, j]) - float(y_r[j])) <= 1e-14 * (1 + abs(float(y_r[j])))
+
+
+def test_layernorm_constant_row_gives_beta():
+    x = np.full((3, 64), 1.75)
+    beta = _small((64,), 4, 0)
+    gamma = 1.0 + _small((64,), 4, 1)
+    y = O.layernorm(x, gamma, beta, 1e-5)
+    assert np.array_equal(y, np.broadcast_to(beta.astype(np.float64), y.shape))
+
+
+@pytest.mark.parametrize("a,b,eps", [(3.0, -1.0, 1e-5), (0.125, 0.5, 1e-5), (2.0, 7.0, 0.0)])
+def test_layernorm_two_element_closed_form(a, b, eps):
+    h = (a - b) / 2.0
+    expect = h / math.sqrt(h * h + eps)
+    y = O.layernorm(np.array([[a, b]]), np.array([2.0, 2.0]), np.array([3.0, -3.0]), eps)
+    assert y[0, 0] == pytest.approx(2.0 * expect + 3.0, rel=1e-15, abs=1e-15)
+    assert y[0, 1] == pytest.approx(-2.0 * expect - 3.0, rel=1e-15, abs=1e-15)
+
+
+def test_layernorm_invariants_identity_affine():
+    x = np.random.default_rng(5).standard_normal((64, 768)) * 2.5 + 0.7
+    eps = 1e-5
+    y = O.layernorm(x, None, None, eps)
+    var = x.var(axis=1)  # numpy's own variance routine, not the oracle's
+    assert np.max(np.abs(y.mean(axis=1))) <= 1e-12 * np.max(np.abs(y))
+    np.testing.assert_allclose((y * y).mean(axis=1), var / (var + eps), rtol=1e-12)
+    y0 = O.layernorm(x, None, None, 0.0)
+    np.testing.assert_allclose((y0 * y0).mean(axis=1), 1.0, rtol=1e-12)
+
+
+def test_rmsnorm_closed_form():
+    y = O.rmsnorm(np.array([[3.0, 4.0]]), None, 0.0)  # rms = 5/sqrt(2)
+    np.testing.assert_allclose(y, [[3.0 * math.sqrt(2) / 5.0, 4.0 * math.sqrt(2) / 5.0]], rtol=1e-15)
+
+
+# ---------------------------------------------------------------- GELU
+def _golden_cdf():
+    rows = []
+    with open(os.path.join(GOLDEN, "normal_cdf.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                x, p = line.split()[:2]
+                rows.append((float(x), float(p)))
+    return rows
+
+
+def test_gelu_textbook_values():
+    for x, phi in _golden_cdf():
+        assert O.gelu_erf(np.array([x]))[0] == pytest.approx(x * phi, rel=1e-15, abs=1e-17)
+
+
+def test_gelu_identities_and_library():
+    from scipy.special import ndtr
+    x = np.linspace(-8, 8, 4001)
+    g = O.gelu_erf(x)
+    np.testing.assert_allclose(g - O.gelu_erf(-x), x, rtol=0, atol=1e-14)
+    np.testing.assert_allclose(g, x * ndtr(x), rtol=1e-15, atol=1e-15)
+    assert O.gelu_erf(np.array([0.0]))[0] == 0.0
+
+
+def test_gelu_tanh_variant():
+    x = np.linspace(-6, 6, 2001)
+    gt = O.gelu_tanh(x)
+    np.testing.assert_allclose(gt - O.gelu_tanh(-x), x, atol=1e-14)
+    c = mpmath.sqrt(2 / mpmath.pi)
+    ref = float(mpmath.mpf(0.5) * (1 + mpmath.tanh(c * (1 + mpmath.mpf("0.044715")))))
+    assert O.gelu_tanh(np.array([1.0]))[0] == pytest.approx(ref, rel=1e-15)
+    diff = np.max(np.abs(gt - O.gelu_erf(x)))
+    assert 1e-4 < diff < 1e-3  # the two variants differ by ~5e-4: a swap is visible
+
+
+# ---------------------------------------------------------------- e4m3
+def _golden_e4m3():
+    rows = []
+    with open(os.path.join(GOLDEN, "e4m3_spec_points.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                c, v = line.split()[:2]
+                rows.append((int(c, 16), float(v)))
+    return rows
+
+
+def test_e4m3_decode_spec_points():
+    for code, val in _golden_e4m3():
+        got = O.e4m3_decode(code)
+        if math.isnan(val):
+            assert np.isnan(got)
+        else:
+            assert float(got) == val and math.copysign(1, float(got)) == math.copysign(1, val)
+
+
+def test_e4m3_decode_exhaustive_vs_torch():
+    codes = np.arange(256, dtype=np.uint8)
+    ours = O.e4m3_decode(codes)
+    theirs = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    nan = np.isnan(theirs)
+    assert np.array_equal(np.isnan(ours), nan)
+    assert np.array_equal(ours[~nan], theirs[~nan])
+
+
+def test_e4m3_roundtrip_midpoints_saturation():
+    codes = np.array([c for c in range(256) if c not in (0x7F, 0xFF)], dtype=np.uint8)
+    assert np.array_equal(O.e4m3_encode(O.e4m3_decode(codes)), codes)
+    pos = O.e4m3_decode(np.arange(0x00, 0x7F))
+    mids = (pos[:-1] + pos[1:]) / 2
+    enc = O.e4m3_encode(mids).astype(int)
+    lo = np.arange(0x00, 0x7E)
+    assert np.all(enc == np.where(lo % 2 == 0, lo, lo + 1))   # ties to even mantissa
+    assert np.all(O.e4m3_encode(np.array([448.0, 449.0, 464.0, 1e6])) == 0x7E)
+    assert np.all(O.e4m3_encode(np.array([-448.0, -1e6])) == 0xFE)
+    assert O.e4m3_encode(np.array([np.nan]))[0] == 0x7F
+
+
+def test_e4m3_encode_vs_torch_in_range():
+    x = (np.random.default_rng(9).standard_normal(200000) * 60).astype(np.float32)
+    x = np.clip(x, -448, 448)
+    x[:1000] *= 1e-3  # subnormal range
+    theirs = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(O.e4m3_encode(x), theirs)
+
+
+# ---------------------------------------------------------------- amax / quant
+def test_rowamax_quant_properties():
+    z = np.random.default_rng(11).standard_normal((32, 300)) * np.linspace(0.1, 9, 32)[:, None]
+    z[5] = 0.0
+    s, q = O.rowamax_quant(z)
+    dq = O.e4m3_decode(q)
+    nz = np.arange(32) != 5
+    assert np.all(np.max(np.abs(dq[nz]), axis=1) == 448.0)
+    assert s[5] == 0.0 and np.all(q[5] == 0)
+    np.testing.assert_allclose(s[nz], np.max(np.abs(z[nz]), axis=1) / 448.0, rtol=0)
+    s2, q2 = O.rowamax_quant(-z)
+    assert np.array_equal(s2, s)
+    assert np.array_equal(q2[nz], q[nz] ^ 0x80)             # sign bit flips, magnitude kept
+    s4, q4 = O.rowamax_quant(z * 4.0)          # power-of-two scale: codes unchanged
+    assert np.array_equal(q4, q) and np.array_equal(s4, s * 4.0)
+
+
+# ---------------------------------------------------------------- softmax / attention
+def test_softmax_rows_sum_and_shift():
+    s = np.random.default_rng(12).standard_normal((16, 333)) * 4
+    p = O.softmax_rows(s)
+    np.testing.assert_allclose(p.sum(axis=1), 1.0, atol=1e-14)
+    np.testing.assert_allclose(O.softmax_rows(s + 123.25), p, rtol=1e-12, atol=1e-300)
+
+
+def _attn_mp(Q, K, V, scale):
+    Lq, Lk, dv = Q.shape[0], K.shape[0], V.shape[1]
+    out = np.zeros((Lq, dv))
+    for i in range(Lq):
+        sc = [mpmath.fsum(mpmath.mpf(float(Q[i, k])) * mpmath.mpf(float(K[j, k])) for k in range(Q.shape[1]))
+              * mpmath.mpf(scale) for j in range(Lk)]
+        m = max(sc)
+        e = [mpmath.exp(v - m) for v in sc]
+        l = mpmath.fsum(e)
+        for d in range(dv):
+            out[i, d] = float(mpmath.fsum(e[j] * mpmath.mpf(float(V[j, d])) for j in range(Lk)) / l)
+    return out
+
+
+def test_attention_brute_force_asymmetric():
+    Q, K, V = _small((4, 3), 13, 0), _small((5, 3), 13, 1), _small((5, 2), 13, 2)
+    ref = _attn_mp(Q, K, V, 0.7)
+    got = O.attention(Q[None], K[None], V[None], 0.7)[0]
+    np.testing.assert_allclose(got, ref, rtol=1e-14, atol=1e-15)
+
+
+def test_attention_special_cases():
+    rng = np.random.default_rng(14)
+    Q, K, V = rng.standard_normal((2, 8, 16)), rng.standard_normal((2, 12, 16)), rng.standard_normal((2, 12, 16))
+    ones = O.attention(Q, K, np.ones_like(V))
+    np.testing.assert_allclose(ones, 1.0, rtol=1e-14)
+    zq = O.attention(np.zeros_like(Q), K, V)
+    np.testing.assert_allclose(zq, np.broadcast_to(V.mean(axis=1, keepdims=True), zq.shape), rtol=1e-13, atol=1e-15)
+    one = O.attention(Q, K[:, :1], V[:, :1])
+    np.testing.assert_allclose(one, np.broadcast_to(V[:, :1], one.shape), rtol=1e-15)
+
+
+# ---------------------------------------------------------------- composites
+def test_postnorm_end_to_end_brute_force():
+    X, W, R = _small((4, 6), 15, 0), _small((6, 4), 15, 1), _small((4, 4), 15, 2)
+    b, g, be = _small((4,), 15, 3), 1 + _small((4,), 15, 4, 0.2), _small((4,), 15, 5, 0.2)
+    Pm = _mm_exact(X, W)
+    got = O.postnorm(X, W, b, R, g, be, 1.0, 1e-5)
+    for i in range(4):
+        x = [Pm[i][j] + Fraction(float(b[j])) + Fraction(float(R[i, j])) for j in range(4)]
+        _, _, y = _ln_mp(x, g, be, 1e-5)
+        np.testing.assert_allclose(got[i], [float(v) for v in y], rtol=1e-13, atol=1e-14)
+
+
+def test_ln_gelu_amax_brute_force():
+    X, W, R = _small((3, 8), 16, 0), _small((8, 5), 16, 1), _small((3, 5), 16, 2)
+    b = _small((5,), 16, 3, 0.1)
+    z, s, q = O.ln_gelu_amax(X, W, b, R, None, None, 1e-5)
+    Pm = _mm_exact(X, W)
+    for i in range(3):
+        x = [Pm[i][j] + Fraction(float(b[j])) + Fraction(float(R[i, j])) for j in range(5)]
+        _, _, y = _ln_mp(x, np.ones(5), np.zeros(5), 1e-5)
+        zr = [v * mpmath.ncdf(v) for v in y]
+        np.testing.assert_allclose(z[i], [float(v) for v in zr], rtol=1e-13, atol=1e-14)
+        a = max(abs(v) for v in zr)
+        assert s[i] == pytest.approx(float(a / 448), rel=1e-14)
+        enc = [int(O.e4m3_encode(np.array([float(v / (a / 448))]))[0]) for v in zr]
+        assert list(q[i]) == enc
+
+
+def test_ffn_special_case_and_brute_force():
+    X = _small((6, 8), 17, 0)
+    W1, b1 = _small((8, 16), 17, 1, 0.3), _small((16,), 17, 2, 0.05)
+    Y = O.ffn_b2b(X, W1, b1, np.zeros((16, 8)), np.zeros(8))
+    np.testing.assert_allclose(Y, O.layernorm(X), rtol=1e-15, atol=1e-15)
+    W2, b2 = _small((16, 8), 17, 3, 0.3), _small((8,), 17, 4, 0.05)
+    Y = O.ffn_b2b(X, W1, b1, W2, b2)
+    P = _mm_exact(X, W1)
+    for i in range(6):
+        h = [mpmath.mpf(P[i][j].numerator) / P[i][j].denominator + mpmath.mpf(float(b1[j])) for j in range(16)]
+        h = [v * mpmath.ncdf(v) for v in h]
+        u = [mpmath.fsum(h[j] * mpmath.mpf(float(W2[j, c])) for j in range(16)) + mpmath.mpf(float(b2[c]))
+             + mpmath.mpf(float(X[i, c])) for c in range(8)]
+        mu = mpmath.fsum(u) / 8
+        var = mpmath.fsum((v - mu) ** 2 for v in u) / 8
+        yr = [(v - mu) / mpmath.sqrt(var + mpmath.mpf(1e-5)) for v in u]
+        np.testing.assert_allclose(Y[i], [float(v) for v in yr], rtol=1e-12, atol=1e-13)
