@@ -1,0 +1,250 @@
+/*
+ * libcomfuse — fused GEMM + row-subgraph operators for AMD Instinct MI355X
+ * (gfx950), after "ComFuse: Fusing Complex Memory-Intensive Subgraphs with
+ * Compute-Intensive Kernels" (arXiv 2608.03537).
+ *
+ * A GEMM keeps its output tile on chip while a dependent elementwise /
+ * reduction subgraph consumes it (the paper's joint compute-memory operator
+ * fusion, Sec. I and Sec. III); two GEMMs joined by such a subgraph keep the
+ * intermediate on chip as well (B2BGEMM, Sec. IV, Eq. 2).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Ownership   Every data pointer is a DEVICE pointer owned by the caller.
+ *             The library never allocates or frees device memory, never
+ *             synchronises, and enqueues work only on the given HIP stream
+ *             (NULL = the null stream).  Host descriptors and node arrays are
+ *             read during the call only.  Buffers must stay alive until the
+ *             enqueued work completes.
+ * Layout      Matrices are row-major with an explicit leading dimension (in
+ *             elements).  A weight that plays the mathematical role W (K x N)
+ *             may be stored K x N (CF_LAYOUT_KN) or N x K (CF_LAYOUT_NK, the
+ *             torch.nn.Linear layout; the fast path).  Per-column vectors
+ *             (bias, gamma, beta) are fp32.
+ * Errors      All validation happens before the first launch; on failure
+ *             nothing is enqueued and a non-zero cf_status is returned, with a
+ *             detail string from cf_last_error().  A launch failure returns
+ *             CF_ERR_HIP.  Faults inside a kernel surface at the caller's next
+ *             synchronisation.  No C++ exception crosses this interface.
+ * Domain      Shapes or node lists outside the compiled vocabulary return
+ *             CF_ERR_UNSUPPORTED (never a silent slow path), mirroring the
+ *             restricted domain of the paper's frontend (Sec. V, frontend
+ *             mapping).  M = 0 (or batch = 0) is a no-op returning CF_OK.
+ * Alignment   Base pointers of matrices must be 16-byte aligned and leading
+ *             dimensions multiples of 16 bytes (CF_ERR_ALIGN otherwise).
+ * Aliasing    An output equal to an input pointer returns CF_ERR_ALIAS;
+ *             partial overlap is undefined.
+ * Determinism Results are bitwise reproducible run to run: no floating-point
+ *             atomics, fixed merge orders.
+ * Threads     The library is stateless apart from an immutable device-info
+ *             cache filled once; calls from several host threads are safe.
+ *             Two calls that share one workspace must not overlap in time.
+ */
+#ifndef COMFUSE_H
+#define COMFUSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define CF_VERSION 1
+#define CF_WS_HEADER_BYTES 33024  /* 256 + 8 * 4096 */
+
+typedef enum {
+  CF_F32 = 0,       /* IEEE binary32 */
+  CF_BF16 = 1,      /* bfloat16 */
+  CF_FP8_E4M3 = 2   /* OCP E4M3FN: bias 7, max 448, no infinities */
+} cf_dtype;
+
+typedef enum {
+  CF_LAYOUT_KN = 0, /* weight stored K x N row-major (ld >= N) */
+  CF_LAYOUT_NK = 1  /* weight stored N x K row-major (ld >= K) */
+} cf_layout;
+
+typedef enum {
+  CF_OK = 0,
+  CF_ERR_NULL = 1,        /* a required pointer is NULL */
+  CF_ERR_SHAPE = 2,       /* a size is negative or violates the shape rules */
+  CF_ERR_LD = 3,          /* a leading dimension is smaller than the row */
+  CF_ERR_ALIGN = 4,       /* pointer or leading dimension misaligned */
+  CF_ERR_DTYPE = 5,       /* unsupported dtype combination */
+  CF_ERR_WORKSPACE = 6,   /* workspace missing or smaller than required */
+  CF_ERR_UNSUPPORTED = 7, /* outside the compiled vocabulary */
+  CF_ERR_ALIAS = 8,       /* an output aliases an input */
+  CF_ERR_HIP = 9,         /* the HIP runtime reported an error */
+  CF_ERR_STRUCT = 10      /* struct_size does not match this library */
+} cf_status;
+
+/* ------------------------------------------------------------------------
+ * cf_gemm_postnorm — post-norm GEMM epilogue (Sec. III; the MatMul +
+ * LayerNorm illustration and the bypass example x = alpha*Acc + Bias of
+ * Sec. III-B):
+ *
+ *     x = alpha * (X . W) + bias + R
+ *     Y = (x - mean_row(x)) / sqrt(var_row(x) + eps) * gamma + beta
+ *
+ * mean/var over each row of N, biased variance.  X is M x K (in_dtype), W
+ * plays K x N (in_dtype, layout w_layout), R is M x N (in_dtype) or NULL,
+ * bias/gamma/beta are fp32 [N] or NULL (= 0 / 1 / 0), Y is M x N (out_dtype).
+ * dtypes: in {F32, BF16} with out == in, or in = BF16 with out = F32.
+ * Shape rules: N % 32 == 0, K % 16 == 0, 32 <= N <= 8192.
+ * Workspace: cf_gemm_postnorm_workspace() bytes (0 on the whole-row path),
+ * 16-byte aligned.  Every non-empty workspace begins with CF_WS_HEADER_BYTES
+ * of library state (an error word and the arrival counters of the row-cluster
+ * path): zero-fill that header once before first use and do not modify it
+ * afterwards; every call leaves it valid for any later call, whatever its
+ * shape or path.  A non-zero first 32-bit word means a wait for peer
+ * workgroups exceeded its bound (results of that call are invalid).
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  size_t struct_size;            /* = sizeof(cf_postnorm_args) */
+  int64_t M, N, K;
+  cf_dtype in_dtype, out_dtype;
+  const void* X; int64_t ldx;
+  const void* W; int64_t ldw; cf_layout w_layout;
+  const float* bias;
+  const void* R; int64_t ldr;
+  const float* gamma;
+  const float* beta;
+  float alpha, eps;
+  void* Y; int64_t ldy;
+  int path;                      /* 0 = auto, 1 = whole-row, 2 = row cluster
+                                    (on-chip statistics exchange), 3 = split-N
+                                    through the workspace */
+} cf_postnorm_args;
+
+size_t    cf_gemm_postnorm_workspace(const cf_postnorm_args* a);
+cf_status cf_gemm_postnorm(const cf_postnorm_args* a, void* workspace,
+                           size_t ws_bytes, void* hip_stream);
+
+/* ------------------------------------------------------------------------
+ * cf_gemm_subgraph — GEMM followed by an elementwise/reduction node list
+ * executed on the on-chip tile (the Stage-Stream execution model, Sec. III;
+ * reductions are stage boundaries, Sec. III-B).  The list is read in order
+ * and must match this grammar (anything else is CF_ERR_UNSUPPORTED):
+ *
+ *     [SCALE] [BIAS] [RESIDUAL] [LAYERNORM | RMSNORM]
+ *     [GELU | GELU_TANH | RELU] STORE [ROWAMAX_QUANT]
+ *
+ * SCALE       x *= f0                    (alpha)
+ * BIAS        x += v0[n]                 (fp32 [N])
+ * RESIDUAL    x += in[m, n]   (dtype: the GEMM input dtype here; F32 or
+ *             BF16 in cf_rowop; ld)
+ * LAYERNORM   x = (x-mean)/sqrt(var+f0) * v0 + v1   (v0/v1 may be NULL)
+ * RMSNORM     x = x/sqrt(mean(x^2)+f0) * v0         (v0 may be NULL)
+ * GELU        x = x * Phi(x) (erf form); GELU_TANH the tanh approximation
+ * STORE       out[m, n] = x  (dtype: F32 or BF16; ld)
+ * ROWAMAX_QUANT  s[m] = max_n |x| / f0 (f0 = qmax, 448 for E4M3) into out
+ *             (fp32 [M]); out2[m, n] = e4m3(x / s[m]) (ld, may be NULL).
+ *             A row with amax 0 gets s = 0 and zero codes.  The amax is
+ *             taken over the fp32 value before the STORE rounding.
+ * ------------------------------------------------------------------------ */
+typedef enum {
+  CF_N_SCALE = 0, CF_N_BIAS = 1, CF_N_RESIDUAL = 2, CF_N_LAYERNORM = 3,
+  CF_N_RMSNORM = 4, CF_N_GELU = 5, CF_N_GELU_TANH = 6, CF_N_RELU = 7,
+  CF_N_STORE = 8, CF_N_ROWAMAX_QUANT = 9, CF_N_SOFTMAX = 10
+} cf_node_kind;
+
+typedef struct {
+  cf_node_kind kind;
+  const void* in;     /* RESIDUAL: matrix */
+  void* out;          /* STORE: matrix; ROWAMAX_QUANT: s (fp32 [M]) */
+  void* out2;         /* ROWAMAX_QUANT: codes (uint8 M x N) or NULL */
+  int64_t ld;         /* leading dimension of in / out (STORE) / out2 */
+  cf_dtype dtype;     /* STORE output dtype */
+  const float* v0;    /* BIAS: bias; LAYERNORM/RMSNORM: gamma */
+  const float* v1;    /* LAYERNORM: beta */
+  float f0;           /* SCALE: alpha; *NORM: eps; ROWAMAX_QUANT: qmax */
+} cf_node;
+
+typedef struct {
+  size_t struct_size;            /* = sizeof(cf_subgraph_args) */
+  int64_t M, N, K;
+  cf_dtype in_dtype;
+  const void* X; int64_t ldx;
+  const void* W; int64_t ldw; cf_layout w_layout;
+  const cf_node* nodes; int n_nodes;
+  int path;                      /* as cf_postnorm_args.path */
+} cf_subgraph_args;
+
+size_t    cf_gemm_subgraph_workspace(const cf_subgraph_args* a);
+cf_status cf_gemm_subgraph(const cf_subgraph_args* a, void* workspace,
+                           size_t ws_bytes, void* hip_stream);
+
+/* ------------------------------------------------------------------------
+ * cf_b2bgemm — back-to-back GEMM with the intermediate kept on chip
+ * (Sec. IV, Eq. 2: P = X W1, S = F(P), O = S W2), batched over `batch`
+ * independent problems (strides sx, sw1, ... in elements).
+ *
+ *   mid = CF_MID_GELU_BIAS : S = GELU(P + b1)                       (FFN)
+ *   mid = CF_MID_SOFTMAX   : S = softmax_row(mid_scale * P), computed
+ *                            online over blocks of N1 (running row max and
+ *                            sum in fp32), so O = S W2 is exact softmax   (attention)
+ *   out = CF_OUT_STORE     : Y = O (+ b2 if given)
+ *   out = CF_OUT_BIAS_RESIDUAL_LN : Y = LN(O + b2 + R) * gamma + beta
+ *
+ * FFN: batch = 1, K = N2 = d.  Attention: batch = B*H, M = Lq, K = d,
+ * N1 = Lk, N2 = d, W1 = keys stored Lk x d (CF_LAYOUT_NK, i.e. Q.K^T),
+ * W2 = values stored Lk x d (CF_LAYOUT_KN).  dtype: CF_BF16.
+ * Shape rules: K % 32 == 0, N2 % 32 == 0; FFN: N1 % 32 == 0, N1 <= 1024,
+ * N2 <= 512; attention: K == N2 in {64, 128}, N1 >= 1.
+ * Workspace: none (cf_b2bgemm_workspace returns 0).
+ * ------------------------------------------------------------------------ */
+typedef enum { CF_MID_GELU_BIAS = 0, CF_MID_SOFTMAX = 1 } cf_mid_op;
+typedef enum { CF_OUT_STORE = 0, CF_OUT_BIAS_RESIDUAL_LN = 1 } cf_out_op;
+
+typedef struct {
+  size_t struct_size;            /* = sizeof(cf_b2b_args) */
+  int64_t batch, M, K, N1, N2;
+  cf_dtype dtype;
+  const void* X;  int64_t ldx, sx;
+  const void* W1; int64_t ldw1, sw1; cf_layout w1_layout; const float* b1;
+  cf_mid_op mid; float mid_scale;
+  const void* W2; int64_t ldw2, sw2; cf_layout w2_layout;
+  cf_out_op out; const float* b2;
+  const void* R; int64_t ldr, sr;
+  const float* gamma; const float* beta; float eps;
+  void* O; int64_t ldo, so;
+} cf_b2b_args;
+
+size_t    cf_b2bgemm_workspace(const cf_b2b_args* a);
+cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes,
+                     void* hip_stream);
+
+/* ------------------------------------------------------------------------
+ * Unfused comparator (the materialising baseline the paper's introduction
+ * describes): a plain GEMM whose result goes to global memory, then a
+ * row-operator kernel that reloads it.
+ *
+ * cf_gemm:  C[b] = alpha * A[b] . B[b] (+ bias), A M x K, B K x N (layout),
+ *           C M x N in out dtype (F32 or BF16).  in: F32 or BF16.
+ *           Shape rules: N % 32 == 0, K % 16 == 0.
+ * cf_rowop: runs a node list (same grammar as cf_gemm_subgraph, or a single
+ *           SOFTMAX node, f0 = scale, writing out) over each row of the
+ *           materialised P (M x N, dtype in).
+ * ------------------------------------------------------------------------ */
+cf_status cf_gemm(int64_t batch, int64_t M, int64_t N, int64_t K,
+                  cf_dtype in, cf_dtype out,
+                  const void* A, int64_t lda, int64_t sa,
+                  const void* B, int64_t ldb, int64_t sb, cf_layout b_layout,
+                  const float* bias, float alpha,
+                  void* C, int64_t ldc, int64_t sc, void* hip_stream);
+
+cf_status cf_rowop(int64_t M, int64_t N, cf_dtype in, const void* P,
+                   int64_t ldp, const cf_node* nodes, int n_nodes,
+                   void* hip_stream);
+
+/* ------------------------------------------------------------------------
+ * Diagnostics
+ * ------------------------------------------------------------------------ */
+const char* cf_status_string(cf_status s);
+const char* cf_last_error(void);   /* thread-local detail of the last error */
+int         cf_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* COMFUSE_H */

@@ -215,6 +215,24 @@ def rowamax_quant(z, qmax=E4M3_MAX):
     return s, q
 
 
+def rowamax_quant_f32(z, qmax=E4M3_MAX):
+    """The same scale chain with every rounding decision taken in fp32:
+    s_i = fl32(a_i / qmax), q_ij = e4m3(fl32(z_ij / s_i)).
+
+    Where floating point decides an integer code, comparing codes exactly
+    needs both sides to decide in the same precision; an fp32 kernel is
+    checked against this form (inputs must be fp32 values).
+    """
+    z = np.asarray(z, dtype=np.float32)
+    a = np.abs(z).max(axis=1)
+    s = (a / np.float32(qmax)).astype(np.float32)
+    safe = np.where(s > 0.0, s, np.float32(1.0)).astype(np.float32)
+    ratio = (z / safe[:, None]).astype(np.float32)
+    q = e4m3_encode(ratio.astype(np.float64))
+    q = np.where((s > 0.0)[:, None], q, np.uint8(0)).astype(np.uint8)
+    return s, q
+
+
 # --------------------------------------------------------------------------
 # Composite operators (what the fused kernels compute end to end)
 # --------------------------------------------------------------------------

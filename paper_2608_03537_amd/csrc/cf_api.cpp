@@ -1,0 +1,547 @@
+// C ABI of libcomfuse: argument validation, path planning, workspace sizing
+// and kernel dispatch.  Every check runs before the first launch, so an
+// invalid call enqueues nothing; no exception leaves this file.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "../../include/comfuse.h"
+#include "cf_internal.h"
+
+using namespace cf;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+cf_status fail(cf_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+cf_status fail(cf_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+size_t dsize(cf_dtype t) { return t == CF_F32 ? 4 : t == CF_BF16 ? 2 : 1; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+cf_status check_matrix(const char* name, const void* p, int64_t rows, int64_t cols, int64_t ld,
+                       cf_dtype t, bool required) {
+  if (!p) {
+    // An empty matrix (rows == 0) may come with a NULL pointer.
+    if (required && rows > 0) return fail(CF_ERR_NULL, "%s is NULL", name);
+    return CF_OK;
+  }
+  if (rows > 0 && ld < cols) return fail(CF_ERR_LD, "%s: leading dimension %lld < %lld", name, (long long)ld,
+                                         (long long)cols);
+  if (!aligned16(p)) return fail(CF_ERR_ALIGN, "%s is not 16-byte aligned", name);
+  if ((ld * (int64_t)dsize(t)) % 16 != 0)
+    return fail(CF_ERR_ALIGN, "%s: leading dimension %lld is not a multiple of 16 bytes", name, (long long)ld);
+  return CF_OK;
+}
+
+cf_status check_vec(const char* name, const float* p) {
+  if (p && !aligned16(p)) return fail(CF_ERR_ALIGN, "%s is not 16-byte aligned", name);
+  return CF_OK;
+}
+
+cf_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return CF_OK;
+  return fail(CF_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---------------------------------------------------------------------------
+// Planning of the GEMM + row-subgraph launch.
+// ---------------------------------------------------------------------------
+enum Path { PATH_AUTO = 0, PATH_WHOLE_ROW = 1, PATH_CLUSTER = 2, PATH_SPLIT = 3 };
+
+constexpr int kWholeRowMaxN = 768;
+constexpr int kClusterMaxPeers = 16;
+
+struct Plan {
+  int cfg = -1, mode = ROWS_LOCAL, cn = 1, num_rb = 0, slots = 0, tm = 0, tn = 0;
+  size_t ws = 0;
+  size_t off_part = 0, off_x = 0;
+};
+
+int find_cfg(int in_f32, int tm, int tn) {
+  for (int i = 0; i < tile_cfg_count(); ++i) {
+    const TileCfg& t = tile_cfg(i);
+    if (t.in_f32 == in_f32 && t.tm == tm && t.tn == tn) return i;
+  }
+  return -1;
+}
+
+// Every non-empty workspace starts with the fixed header (error word and
+// arrival counters; only the cluster path writes it).  Then the cluster path
+// keeps part[2][M][cn] float2, the split path part[M][cn] float2 and x[M][N].
+void size_workspace(Plan& pl, int64_t M, int64_t N) {
+  if (pl.mode == ROWS_CLUSTER) {
+    pl.off_part = kWsHeaderBytes;
+    pl.ws = pl.off_part + round_up((size_t)2 * M * pl.cn * 8, 256);
+  } else if (pl.mode == ROWS_SPLIT) {
+    pl.off_part = kWsHeaderBytes;
+    pl.off_x = pl.off_part + round_up((size_t)M * pl.cn * 8, 256);
+    pl.ws = pl.off_x + round_up((size_t)M * N * 4, 256);
+  } else {
+    pl.ws = 0;
+  }
+}
+
+// Chooses the tiling for a row-subgraph GEMM.  `need_rows` is false when the
+// epilogue has no row reduction (then any tiling is valid).
+cf_status plan_rows(int64_t M, int64_t N, int in_f32, int path, bool need_rows, bool probe_device,
+                    Plan& pl) {
+  pl = Plan();
+  if (!need_rows) {
+    const int tn = (N >= 256) ? 256 : 128;
+    pl.cfg = find_cfg(in_f32, 128, tn);
+    pl.mode = ROWS_LOCAL;
+  } else {
+    if (path == PATH_AUTO) path = (N <= kWholeRowMaxN) ? PATH_WHOLE_ROW : PATH_SPLIT;
+    if (path == PATH_WHOLE_ROW) {
+      if (N > kWholeRowMaxN)
+        return fail(CF_ERR_UNSUPPORTED, "whole-row path needs N <= %d (N = %lld)", kWholeRowMaxN, (long long)N);
+      static const int tns[] = {128, 256, 384, 512, 768};
+      for (int tn : tns)
+        if (tn >= N) { pl.cfg = find_cfg(in_f32, 32, tn); break; }
+      pl.mode = ROWS_LOCAL;
+    } else if (path == PATH_CLUSTER) {
+      static const int tns[] = {256, 192, 128};
+      for (int tn : tns) {
+        const int c = find_cfg(in_f32, 128, tn);
+        if (c >= 0 && N % tn == 0 && N / tn <= kClusterMaxPeers) { pl.cfg = c; break; }
+      }
+      if (pl.cfg < 0)
+        return fail(CF_ERR_UNSUPPORTED, "cluster path: no tile width divides N = %lld into <= %d peers",
+                    (long long)N, kClusterMaxPeers);
+      pl.mode = ROWS_CLUSTER;
+    } else if (path == PATH_SPLIT) {
+      pl.cfg = find_cfg(in_f32, 128, 256);
+      pl.mode = ROWS_SPLIT;
+    } else {
+      return fail(CF_ERR_UNSUPPORTED, "unknown path %d", path);
+    }
+  }
+  if (pl.cfg < 0) return fail(CF_ERR_UNSUPPORTED, "no compiled tile for this shape");
+  const TileCfg& t = tile_cfg(pl.cfg);
+  pl.tm = t.tm;
+  pl.tn = t.tn;
+  pl.cn = (int)((N + t.tn - 1) / t.tn);
+  pl.num_rb = (int)((M + t.tm - 1) / t.tm);
+  pl.slots = (pl.num_rb + 7) / 8;
+  if (pl.mode == ROWS_CLUSTER && probe_device) {
+    // Every peer group must be resident at once: cap the persistent grid.
+    const int cap = resident_wgs(pl.cfg);
+    const int slots = cap / (8 * pl.cn);
+    if (slots < 1) return fail(CF_ERR_UNSUPPORTED, "cluster path: %d peers do not fit the device", pl.cn);
+    pl.slots = std::min(pl.slots, std::min(slots, kMaxSlots / 8));
+  }
+  size_workspace(pl, M, N);
+  return CF_OK;
+}
+
+void bind_workspace(const Plan& pl, void* ws, GemmRowsParams& p) {
+  char* b = reinterpret_cast<char*>(ws);
+  if (pl.mode == ROWS_CLUSTER) {
+    p.ws_err = reinterpret_cast<unsigned*>(b);
+    p.ws_arrive = reinterpret_cast<unsigned long long*>(b + 256);
+    p.ws_part = reinterpret_cast<float*>(b + pl.off_part);
+  } else if (pl.mode == ROWS_SPLIT) {
+    p.ws_part = reinterpret_cast<float*>(b + pl.off_part);
+    p.ws_x = reinterpret_cast<float*>(b + pl.off_x);
+  }
+}
+
+// Runs a planned GEMM + row subgraph (and the finish pass of the split path).
+cf_status run_rows(const Plan& pl, GemmRowsParams p, void* ws, hipStream_t st) {
+  p.mode = pl.mode;
+  p.cn = pl.cn;
+  p.num_rb = pl.num_rb;
+  p.slots = pl.slots;
+  bind_workspace(pl, ws, p);
+  if (pl.mode == ROWS_SPLIT) {
+    RowEpi full = p.epi;
+    // The GEMM runs stage 1 only and publishes x and partial statistics.
+    p.epi.norm = NORM_NONE;
+    p.epi.act = ACT_NONE;
+    p.epi.Y = nullptr;
+    p.epi.quant = 0;
+    cf_status s = hip_status(launch_gemm_rows(p, tile_cfg(pl.cfg).in_f32, pl.cfg, st), "GEMM launch");
+    if (s != CF_OK) return s;
+    RowKernelParams f{};
+    f.M = p.M;
+    f.N = p.N;
+    f.P = p.ws_x;
+    f.ldp = p.N;
+    f.p_f32 = 1;
+    f.finish = 1;
+    f.cn = pl.cn;
+    f.tn = pl.tn;
+    f.part = p.ws_part;
+    f.epi = full;
+    f.epi.alpha = 1.0f;
+    f.epi.bias = nullptr;
+    f.epi.R = nullptr;
+    return hip_status(launch_row_kernel(f, st), "finish launch");
+  }
+  return hip_status(launch_gemm_rows(p, tile_cfg(pl.cfg).in_f32, pl.cfg, st), "GEMM launch");
+}
+
+// ---------------------------------------------------------------------------
+// Node lists -> RowEpi (the fixed stage grammar).
+// ---------------------------------------------------------------------------
+cf_status parse_nodes(const cf_node* nodes, int n, int64_t M, int64_t N, cf_dtype in, RowEpi& e,
+                      bool allow_softmax, int* softmax, float* softmax_scale) {
+  e = RowEpi{};
+  e.alpha = 1.0f;
+  e.qmax = 448.0f;
+  if (softmax) *softmax = 0;
+  if (!nodes || n <= 0) return fail(CF_ERR_NULL, "empty node list");
+  if (n == 1 && nodes[0].kind == CF_N_SOFTMAX) {
+    if (!allow_softmax) return fail(CF_ERR_UNSUPPORTED, "SOFTMAX is available in cf_rowop only");
+    const cf_node& d = nodes[0];
+    if (d.dtype != CF_F32 && d.dtype != CF_BF16) return fail(CF_ERR_DTYPE, "SOFTMAX output dtype");
+    cf_status s = check_matrix("SOFTMAX out", d.out, M, N, d.ld, d.dtype, true);
+    if (s != CF_OK) return s;
+    e.Y = d.out;
+    e.ldy = d.ld;
+    e.y_f32 = d.dtype == CF_F32;
+    *softmax = 1;
+    *softmax_scale = d.f0;
+    return CF_OK;
+  }
+  // Grammar position of each kind; positions must strictly increase.
+  auto rank = [](cf_node_kind k) -> int {
+    switch (k) {
+      case CF_N_SCALE: return 0;
+      case CF_N_BIAS: return 1;
+      case CF_N_RESIDUAL: return 2;
+      case CF_N_LAYERNORM: case CF_N_RMSNORM: return 3;
+      case CF_N_GELU: case CF_N_GELU_TANH: case CF_N_RELU: return 4;
+      case CF_N_STORE: return 5;
+      case CF_N_ROWAMAX_QUANT: return 6;
+      default: return -1;
+    }
+  };
+  int last = -1;
+  for (int i = 0; i < n; ++i) {
+    const cf_node& d = nodes[i];
+    const int r = rank(d.kind);
+    if (r < 0) return fail(CF_ERR_UNSUPPORTED, "node %d: kind %d is not in the fused vocabulary", i, (int)d.kind);
+    if (r <= last)
+      return fail(CF_ERR_UNSUPPORTED, "node %d: kind %d out of order (grammar: SCALE BIAS RESIDUAL NORM ACT STORE QUANT)",
+                  i, (int)d.kind);
+    last = r;
+    cf_status s = CF_OK;
+    switch (d.kind) {
+      case CF_N_SCALE: e.alpha = d.f0; break;
+      case CF_N_BIAS:
+        if (!d.v0) return fail(CF_ERR_NULL, "BIAS vector is NULL");
+        if ((s = check_vec("BIAS", d.v0)) != CF_OK) return s;
+        e.bias = d.v0;
+        break;
+      case CF_N_RESIDUAL:
+        if (d.dtype != CF_F32 && d.dtype != CF_BF16) return fail(CF_ERR_DTYPE, "RESIDUAL dtype must be F32 or BF16");
+        if (!allow_softmax && d.dtype != in)
+          return fail(CF_ERR_DTYPE, "RESIDUAL dtype must equal the GEMM input dtype");
+        if ((s = check_matrix("RESIDUAL", d.in, M, N, d.ld, d.dtype, true)) != CF_OK) return s;
+        e.R = d.in;
+        e.ldr = d.ld;
+        e.r_f32 = d.dtype == CF_F32;
+        break;
+      case CF_N_LAYERNORM: case CF_N_RMSNORM:
+        if ((s = check_vec("gamma", d.v0)) != CF_OK || (s = check_vec("beta", d.v1)) != CF_OK) return s;
+        if (!(d.f0 >= 0.0f)) return fail(CF_ERR_SHAPE, "eps must be >= 0");
+        e.norm = d.kind == CF_N_LAYERNORM ? NORM_LAYER : NORM_RMS;
+        e.gamma = d.v0;
+        e.beta = d.kind == CF_N_LAYERNORM ? d.v1 : nullptr;
+        e.eps = d.f0;
+        break;
+      case CF_N_GELU: e.act = ACT_GELU; break;
+      case CF_N_GELU_TANH: e.act = ACT_GELU_TANH; break;
+      case CF_N_RELU: e.act = ACT_RELU; break;
+      case CF_N_STORE:
+        if (d.dtype != CF_F32 && d.dtype != CF_BF16) return fail(CF_ERR_DTYPE, "STORE dtype must be F32 or BF16");
+        if ((s = check_matrix("STORE", d.out, M, N, d.ld, d.dtype, true)) != CF_OK) return s;
+        e.Y = d.out;
+        e.ldy = d.ld;
+        e.y_f32 = d.dtype == CF_F32;
+        break;
+      case CF_N_ROWAMAX_QUANT:
+        if (!d.out) return fail(CF_ERR_NULL, "ROWAMAX_QUANT scale output is NULL");
+        if (!(d.f0 > 0.0f)) return fail(CF_ERR_SHAPE, "ROWAMAX_QUANT qmax must be > 0");
+        if (d.out2) {
+          if (!aligned16(d.out2) || d.ld % 16 != 0)
+            return fail(CF_ERR_ALIGN, "ROWAMAX_QUANT codes: 16-byte alignment and ld %% 16 == 0 required");
+          if (M > 0 && d.ld < N) return fail(CF_ERR_LD, "ROWAMAX_QUANT codes: ld < N");
+        }
+        e.quant = 1;
+        e.qmax = d.f0;
+        e.s_out = reinterpret_cast<float*>(d.out);
+        e.q_out = reinterpret_cast<uint8_t*>(d.out2);
+        e.ldq = d.ld;
+        break;
+      default: break;
+    }
+  }
+  if (!e.Y && !e.quant) return fail(CF_ERR_UNSUPPORTED, "node list has no output (STORE or ROWAMAX_QUANT)");
+  return CF_OK;
+}
+
+cf_status check_gemm_shape(int64_t M, int64_t N, int64_t K) {
+  if (M < 0 || N <= 0 || K <= 0) return fail(CF_ERR_SHAPE, "need M >= 0, N > 0, K > 0");
+  if (N % 32 != 0) return fail(CF_ERR_SHAPE, "N = %lld must be a multiple of 32", (long long)N);
+  if (K % 16 != 0) return fail(CF_ERR_SHAPE, "K = %lld must be a multiple of 16", (long long)K);
+  if (N > 8192) return fail(CF_ERR_SHAPE, "N = %lld exceeds 8192", (long long)N);
+  if (M > (int64_t)1 << 30 || K > (int64_t)1 << 30) return fail(CF_ERR_SHAPE, "size exceeds 2^30");
+  return CF_OK;
+}
+
+bool outputs_alias(const void* out, std::initializer_list<const void*> ins) {
+  if (!out) return false;
+  for (const void* p : ins)
+    if (p && p == out) return true;
+  return false;
+}
+
+// Shared body of cf_gemm_postnorm / cf_gemm_subgraph.
+cf_status rows_common(int64_t M, int64_t N, int64_t K, cf_dtype in, const void* X, int64_t ldx,
+                      const void* W, int64_t ldw, cf_layout wl, const RowEpi& epi, int path,
+                      void* ws, size_t ws_bytes, void* stream, bool size_only, size_t* ws_out) {
+  cf_status s = check_gemm_shape(M, N, K);
+  if (s != CF_OK) return s;
+  if (in != CF_F32 && in != CF_BF16) return fail(CF_ERR_DTYPE, "input dtype must be F32 or BF16");
+  if (wl != CF_LAYOUT_KN && wl != CF_LAYOUT_NK) return fail(CF_ERR_UNSUPPORTED, "unknown weight layout");
+  if ((s = check_matrix("X", X, M, K, ldx, in, true)) != CF_OK) return s;
+  if ((s = check_matrix("W", W, 1, wl == CF_LAYOUT_NK ? K : N, ldw, in, true)) != CF_OK) return s;
+  const bool need_rows = epi.norm != NORM_NONE || epi.quant;
+  Plan pl;
+  if ((s = plan_rows(M, N, in == CF_F32, path, need_rows, !size_only && M > 0, pl)) != CF_OK) return s;
+  if (size_only) {
+    *ws_out = pl.ws;
+    return CF_OK;
+  }
+  for (const void* out : {(const void*)epi.Y, (const void*)epi.s_out, (const void*)epi.q_out})
+    if (outputs_alias(out, {X, W, epi.R, (const void*)epi.bias, (const void*)epi.gamma, (const void*)epi.beta}))
+      return fail(CF_ERR_ALIAS, "an output aliases an input");
+  if (pl.ws > 0) {
+    if (!ws) return fail(CF_ERR_WORKSPACE, "workspace of %zu bytes required", pl.ws);
+    if (ws_bytes < pl.ws) return fail(CF_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, pl.ws);
+    if (!aligned16(ws)) return fail(CF_ERR_ALIGN, "workspace is not 16-byte aligned");
+  }
+  if (M == 0) return CF_OK;
+  GemmRowsParams p{};
+  p.batch = 1;
+  p.M = (int)M;
+  p.N = (int)N;
+  p.K = (int)K;
+  p.X = X;
+  p.ldx = ldx;
+  p.W = W;
+  p.ldw = ldw;
+  p.w_nk = wl == CF_LAYOUT_NK;
+  p.epi = epi;
+  return run_rows(pl, p, ws, reinterpret_cast<hipStream_t>(stream));
+}
+
+cf_status postnorm_epi(const cf_postnorm_args* a, RowEpi& e) {
+  if (!a) return fail(CF_ERR_NULL, "args is NULL");
+  if (a->struct_size != sizeof(cf_postnorm_args))
+    return fail(CF_ERR_STRUCT, "struct_size %zu != %zu", a->struct_size, sizeof(cf_postnorm_args));
+  if (a->in_dtype != CF_F32 && a->in_dtype != CF_BF16) return fail(CF_ERR_DTYPE, "in_dtype must be F32 or BF16");
+  if (a->out_dtype != CF_F32 && a->out_dtype != CF_BF16) return fail(CF_ERR_DTYPE, "out_dtype must be F32 or BF16");
+  if (a->in_dtype == CF_F32 && a->out_dtype != CF_F32) return fail(CF_ERR_DTYPE, "F32 input needs F32 output");
+  if (!(a->eps >= 0.0f)) return fail(CF_ERR_SHAPE, "eps must be >= 0");
+  cf_status s;
+  if ((s = check_matrix("Y", a->Y, a->M, a->N, a->ldy, a->out_dtype, true)) != CF_OK) return s;
+  if ((s = check_matrix("R", a->R, a->M, a->N, a->ldr, a->in_dtype, false)) != CF_OK) return s;
+  if ((s = check_vec("bias", a->bias)) != CF_OK || (s = check_vec("gamma", a->gamma)) != CF_OK ||
+      (s = check_vec("beta", a->beta)) != CF_OK)
+    return s;
+  e = RowEpi{};
+  e.alpha = a->alpha;
+  e.bias = a->bias;
+  e.R = a->R;
+  e.ldr = a->ldr;
+  e.r_f32 = a->in_dtype == CF_F32;
+  e.norm = NORM_LAYER;
+  e.gamma = a->gamma;
+  e.beta = a->beta;
+  e.eps = a->eps;
+  e.Y = a->Y;
+  e.ldy = a->ldy;
+  e.y_f32 = a->out_dtype == CF_F32;
+  e.qmax = 448.0f;
+  return CF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int cf_version(void) { return CF_VERSION; }
+
+const char* cf_last_error(void) { return g_last_error.c_str(); }
+
+const char* cf_status_string(cf_status s) {
+  switch (s) {
+    case CF_OK: return "CF_OK";
+    case CF_ERR_NULL: return "CF_ERR_NULL: a required pointer is NULL";
+    case CF_ERR_SHAPE: return "CF_ERR_SHAPE: invalid size";
+    case CF_ERR_LD: return "CF_ERR_LD: leading dimension too small";
+    case CF_ERR_ALIGN: return "CF_ERR_ALIGN: misaligned pointer or leading dimension";
+    case CF_ERR_DTYPE: return "CF_ERR_DTYPE: unsupported dtype";
+    case CF_ERR_WORKSPACE: return "CF_ERR_WORKSPACE: workspace missing or too small";
+    case CF_ERR_UNSUPPORTED: return "CF_ERR_UNSUPPORTED: outside the compiled vocabulary";
+    case CF_ERR_ALIAS: return "CF_ERR_ALIAS: an output aliases an input";
+    case CF_ERR_HIP: return "CF_ERR_HIP: HIP runtime error";
+    case CF_ERR_STRUCT: return "CF_ERR_STRUCT: struct_size mismatch";
+  }
+  return "unknown cf_status";
+}
+
+size_t cf_gemm_postnorm_workspace(const cf_postnorm_args* a) {
+  try {
+    RowEpi e;
+    if (postnorm_epi(a, e) != CF_OK) return 0;
+    size_t ws = 0;
+    if (rows_common(a->M, a->N, a->K, a->in_dtype, a->X, a->ldx, a->W, a->ldw, a->w_layout, e, a->path,
+                    nullptr, 0, nullptr, true, &ws) != CF_OK)
+      return 0;
+    return ws;
+  } catch (...) {
+    return 0;
+  }
+}
+
+cf_status cf_gemm_postnorm(const cf_postnorm_args* a, void* workspace, size_t ws_bytes, void* hip_stream) {
+  try {
+    RowEpi e;
+    cf_status s = postnorm_epi(a, e);
+    if (s != CF_OK) return s;
+    return rows_common(a->M, a->N, a->K, a->in_dtype, a->X, a->ldx, a->W, a->ldw, a->w_layout, e, a->path,
+                       workspace, ws_bytes, hip_stream, false, nullptr);
+  } catch (...) {
+    return fail(CF_ERR_HIP, "internal error");
+  }
+}
+
+static cf_status subgraph_epi(const cf_subgraph_args* a, RowEpi& e) {
+  if (!a) return fail(CF_ERR_NULL, "args is NULL");
+  if (a->struct_size != sizeof(cf_subgraph_args))
+    return fail(CF_ERR_STRUCT, "struct_size %zu != %zu", a->struct_size, sizeof(cf_subgraph_args));
+  if (a->in_dtype != CF_F32 && a->in_dtype != CF_BF16) return fail(CF_ERR_DTYPE, "in_dtype must be F32 or BF16");
+  return parse_nodes(a->nodes, a->n_nodes, a->M, a->N, a->in_dtype, e, false, nullptr, nullptr);
+}
+
+size_t cf_gemm_subgraph_workspace(const cf_subgraph_args* a) {
+  try {
+    RowEpi e;
+    if (subgraph_epi(a, e) != CF_OK) return 0;
+    size_t ws = 0;
+    if (rows_common(a->M, a->N, a->K, a->in_dtype, a->X, a->ldx, a->W, a->ldw, a->w_layout, e, a->path,
+                    nullptr, 0, nullptr, true, &ws) != CF_OK)
+      return 0;
+    return ws;
+  } catch (...) {
+    return 0;
+  }
+}
+
+cf_status cf_gemm_subgraph(const cf_subgraph_args* a, void* workspace, size_t ws_bytes, void* hip_stream) {
+  try {
+    RowEpi e;
+    cf_status s = subgraph_epi(a, e);
+    if (s != CF_OK) return s;
+    return rows_common(a->M, a->N, a->K, a->in_dtype, a->X, a->ldx, a->W, a->ldw, a->w_layout, e, a->path,
+                       workspace, ws_bytes, hip_stream, false, nullptr);
+  } catch (...) {
+    return fail(CF_ERR_HIP, "internal error");
+  }
+}
+
+cf_status cf_gemm(int64_t batch, int64_t M, int64_t N, int64_t K, cf_dtype in, cf_dtype out, const void* A,
+                  int64_t lda, int64_t sa, const void* B, int64_t ldb, int64_t sb, cf_layout b_layout,
+                  const float* bias, float alpha, void* C, int64_t ldc, int64_t sc, void* hip_stream) {
+  try {
+    cf_status s = check_gemm_shape(M, N, K);
+    if (s != CF_OK) return s;
+    if (batch < 0 || batch > 65535) return fail(CF_ERR_SHAPE, "batch must be in [0, 65535]");
+    if (in != CF_F32 && in != CF_BF16) return fail(CF_ERR_DTYPE, "input dtype must be F32 or BF16");
+    if (out != CF_F32 && out != CF_BF16) return fail(CF_ERR_DTYPE, "output dtype must be F32 or BF16");
+    if (b_layout != CF_LAYOUT_KN && b_layout != CF_LAYOUT_NK) return fail(CF_ERR_UNSUPPORTED, "unknown layout");
+    if ((s = check_matrix("A", A, M, K, lda, in, true)) != CF_OK) return s;
+    if ((s = check_matrix("B", B, 1, b_layout == CF_LAYOUT_NK ? K : N, ldb, in, true)) != CF_OK) return s;
+    if ((s = check_matrix("C", C, M, N, ldc, out, true)) != CF_OK) return s;
+    if ((s = check_vec("bias", bias)) != CF_OK) return s;
+    if (batch > 1 && (sa % 8 != 0 || sb % 8 != 0 || sc % 8 != 0 || sa < 0 || sb < 0 || sc < 0))
+      return fail(CF_ERR_ALIGN, "batch strides must be non-negative multiples of 8 elements");
+    if (outputs_alias(C, {A, B, (const void*)bias})) return fail(CF_ERR_ALIAS, "C aliases an input");
+    if (M == 0 || batch == 0) return CF_OK;
+    Plan pl;
+    if ((s = plan_rows(M, N, in == CF_F32, PATH_AUTO, false, false, pl)) != CF_OK) return s;
+    GemmRowsParams p{};
+    p.batch = (int)batch;
+    p.M = (int)M;
+    p.N = (int)N;
+    p.K = (int)K;
+    p.X = A;
+    p.ldx = lda;
+    p.sx = sa;
+    p.W = B;
+    p.ldw = ldb;
+    p.sw = sb;
+    p.w_nk = b_layout == CF_LAYOUT_NK;
+    p.epi.alpha = alpha;
+    p.epi.bias = bias;
+    p.epi.Y = C;
+    p.epi.ldy = ldc;
+    p.epi.sy = sc;
+    p.epi.y_f32 = out == CF_F32;
+    p.epi.qmax = 448.0f;
+    return run_rows(pl, p, nullptr, reinterpret_cast<hipStream_t>(hip_stream));
+  } catch (...) {
+    return fail(CF_ERR_HIP, "internal error");
+  }
+}
+
+cf_status cf_rowop(int64_t M, int64_t N, cf_dtype in, const void* P, int64_t ldp, const cf_node* nodes,
+                   int n_nodes, void* hip_stream) {
+  try {
+    if (M < 0 || N <= 0 || N % 4 != 0 || N > 8192) return fail(CF_ERR_SHAPE, "need M >= 0, 0 < N <= 8192, N %% 4 == 0");
+    if (in != CF_F32 && in != CF_BF16) return fail(CF_ERR_DTYPE, "input dtype must be F32 or BF16");
+    cf_status s = check_matrix("P", P, M, N, ldp, in, true);
+    if (s != CF_OK) return s;
+    RowKernelParams r{};
+    if ((s = parse_nodes(nodes, n_nodes, M, N, in, r.epi, true, &r.softmax, &r.softmax_scale)) != CF_OK) return s;
+    for (const void* out : {(const void*)r.epi.Y, (const void*)r.epi.s_out, (const void*)r.epi.q_out})
+      if (outputs_alias(out, {P, r.epi.R, (const void*)r.epi.bias}))
+        return fail(CF_ERR_ALIAS, "an output aliases an input");
+    if (M == 0) return CF_OK;
+    r.M = (int)M;
+    r.N = (int)N;
+    r.P = P;
+    r.ldp = ldp;
+    r.p_f32 = in == CF_F32;
+    return hip_status(launch_row_kernel(r, reinterpret_cast<hipStream_t>(hip_stream)), "row kernel launch");
+  } catch (...) {
+    return fail(CF_ERR_HIP, "internal error");
+  }
+}
+
+size_t cf_b2bgemm_workspace(const cf_b2b_args* a) {
+  (void)a;
+  return 0;
+}
+
+}  // extern "C"

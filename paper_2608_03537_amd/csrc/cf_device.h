@@ -1,0 +1,177 @@
+// Device-side building blocks for the gfx950 kernels: MFMA atoms, type
+// conversions, the E4M3 encoder and GELU.  Everything here is __device__
+// inline; nothing allocates.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cf_internal.h"
+
+namespace cf {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4_t;
+typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2_t;
+
+typedef uint16_t bf16_t;  // storage type of bfloat16 values
+
+// ---------------------------------------------------------------------------
+// Conversions
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) {
+  return __uint_as_float(h << 16);
+}
+
+// fp32 -> bf16, round to nearest even (finite inputs; NaN stays NaN because
+// the quiet bit survives the rounding add for every NaN payload we produce).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+}
+
+// OCP E4M3FN encoder: nearest representable value, ties to even mantissa,
+// magnitudes beyond 448 saturate to 448, NaN -> 0x7F.  Integer-only so the
+// rounding is exact and independent of any hardware conversion mode.
+//   normal:    (-1)^s 2^(e-7) (1 + m/8), e in 1..15 (e=15,m=7 is NaN)
+//   subnormal: (-1)^s 2^-6 (m/8)
+__device__ __forceinline__ uint32_t f32_to_e4m3(float f) {
+  uint32_t u = __float_as_uint(f);
+  uint32_t sign = (u >> 24) & 0x80u;
+  uint32_t a = u & 0x7FFFFFFFu;
+  if (a > 0x7F800000u) return 0x7Fu;                 // NaN
+  if (a >= 0x43E00000u) return sign | 0x7Eu;          // |f| >= 448: saturate
+  uint32_t e32 = a >> 23;                             // biased fp32 exponent
+  uint32_t code;
+  if (e32 >= 121u) {                                  // |f| >= 2^-6: normal
+    // Keep 3 mantissa bits; round the 20 dropped bits to nearest even.
+    uint32_t mant = a & 0x7FFFFFu;
+    uint32_t keep = mant >> 20;
+    uint32_t rest = mant & 0xFFFFFu;
+    uint32_t e8 = e32 - 120u;                         // e4m3 exponent field
+    uint32_t v = (e8 << 3) | keep;
+    if (rest > 0x80000u || (rest == 0x80000u && (keep & 1u))) v += 1u;  // may carry into exponent
+    code = v;                                          // v <= 0x7E since |f| < 448
+  } else {
+    // Subnormal target: value = k * 2^-9, k = round_even(|f| * 2^9).
+    // |f| < 2^-6 so k <= 8 (8 = smallest normal, code 0x08: the carry is right).
+    if (e32 < 110u) return sign;                      // |f| < 2^-17: rounds to 0
+    uint32_t mant = (a & 0x7FFFFFu) | 0x800000u;      // 1.m * 2^(e32-127)
+    // |f| * 2^9 = mant * 2^(e32 - 127 - 23 + 9) = mant >> (141 - e32);
+    // e32 in [110, 120] gives a shift of 21..31.
+    uint32_t shift = 141u - e32;
+    uint32_t k = mant >> shift;
+    uint32_t rest = mant & ((1u << shift) - 1u);
+    uint32_t half = 1u << (shift - 1u);
+    if (rest > half || (rest == half && (k & 1u))) k += 1u;
+    code = k;
+  }
+  return sign | code;
+}
+
+// GELU, erf form: x * Phi(x).
+__device__ __forceinline__ float gelu_erf(float x) {
+  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+}
+// GELU, tanh approximation.
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float c = 0.79788456080286536f;  // sqrt(2/pi)
+  return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
+}
+
+// ---------------------------------------------------------------------------
+// MFMA atoms.  Both operate on 16-byte operand chunks read from LDS rows that
+// are contiguous along k; lane group g = lane/32 holds the g-th chunk of a
+// 2-chunk k step.  Because the instruction pairs A and B k-indices the same
+// way, any fixed k assignment inside a step gives the right dot product.
+//
+// Accumulator layout of a 32x32 block (D = A.B, A 32 x k, B k x 32):
+//   lane l holds column (l % 32) and rows 8*(i/4) + 4*(l/32) + (i%4),
+//   i = 0..15.
+// ---------------------------------------------------------------------------
+template <typename T> struct Mma;
+
+template <> struct Mma<bf16_t> {
+  static constexpr int kPerChunk = 8;   // bf16 values per 16-byte chunk
+  __device__ __forceinline__ static void run(f32x16_t& acc, u32x4_t a, u32x4_t b) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                  __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+  }
+};
+
+template <> struct Mma<float> {
+  static constexpr int kPerChunk = 4;   // fp32 values per 16-byte chunk
+  // Four k=2 MFMAs: step j pairs element j of lane group 0 with element j of
+  // lane group 1, so the four together cover the 8 k values of the chunk pair.
+  __device__ __forceinline__ static void run(f32x16_t& acc, u32x4_t a, u32x4_t b) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a[j]), __uint_as_float(b[j]),
+                                                 acc, 0, 0, 0);
+  }
+};
+
+// Row index (inside a 32x32 block) held by accumulator element i of lane l.
+__device__ __forceinline__ int acc_row(int i, int lane) {
+  return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+}
+
+// ---------------------------------------------------------------------------
+// LDS / global helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ u32x4_t lds_read16(const char* p) {
+  return *reinterpret_cast<const u32x4_t*>(p);
+}
+__device__ __forceinline__ void lds_write16(char* p, u32x4_t v) {
+  *reinterpret_cast<u32x4_t*>(p) = v;
+}
+__device__ __forceinline__ u32x4_t gload16(const void* p) {
+  return *reinterpret_cast<const u32x4_t*>(p);
+}
+
+// ---------------------------------------------------------------------------
+// Four consecutive row elements: load (bf16 or fp32), activation, store.
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ void load4(const T* p, float (&v)[4]);
+template <>
+__device__ __forceinline__ void load4<bf16_t>(const bf16_t* p, float (&v)[4]) {
+  const u32x2_t u = *reinterpret_cast<const u32x2_t*>(p);
+  v[0] = bf16_to_f32(u[0] & 0xFFFFu);
+  v[1] = bf16_to_f32(u[0] >> 16);
+  v[2] = bf16_to_f32(u[1] & 0xFFFFu);
+  v[3] = bf16_to_f32(u[1] >> 16);
+}
+template <>
+__device__ __forceinline__ void load4<float>(const float* p, float (&v)[4]) {
+  const f32x4_t u = *reinterpret_cast<const f32x4_t*>(p);
+  v[0] = u[0]; v[1] = u[1]; v[2] = u[2]; v[3] = u[3];
+}
+
+__device__ __forceinline__ float apply_act(int act, float x) {
+  switch (act) {
+    case ACT_GELU: return gelu_erf(x);
+    case ACT_GELU_TANH: return gelu_tanh(x);
+    case ACT_RELU: return x > 0.0f ? x : 0.0f;
+    default: return x;
+  }
+}
+
+__device__ __forceinline__ void store4(void* base, int64_t off, int f32, const float (&v)[4]) {
+  if (f32) {
+    f32x4_t o = {v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<f32x4_t*>(reinterpret_cast<float*>(base) + off) = o;
+  } else {
+    u32x2_t o = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+    *reinterpret_cast<u32x2_t*>(reinterpret_cast<bf16_t*>(base) + off) = o;
+  }
+}
+
+}  // namespace cf

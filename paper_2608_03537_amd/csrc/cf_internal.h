@@ -1,0 +1,95 @@
+// Internal host <-> kernel interface of libcomfuse (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cf {
+
+enum NormKind { NORM_NONE = 0, NORM_LAYER = 1, NORM_RMS = 2 };
+enum ActKind { ACT_NONE = 0, ACT_GELU = 1, ACT_GELU_TANH = 2, ACT_RELU = 3 };
+
+// Epilogue "program": the stage chain of the Stage-Stream model in a fixed
+// order.  Every field is uniform across the launch, so the kernel branches on
+// it with scalar branches.
+//   stage 1: x = alpha * acc + bias[n] + R[m, n]
+//   stage 2: optional row reduction (LayerNorm / RMSNorm) and its PostOp
+//   stage 3: optional activation
+//   store  : Y[m, n] = x (bf16 or fp32)
+//   stage 4: optional row amax -> s[m] = amax / qmax, Q[m, n] = e4m3(x / s)
+struct RowEpi {
+  float alpha;
+  const float* bias;
+  const void* R; int64_t ldr; int64_t sr;   // residual
+  int r_f32;                                // row kernel: residual is fp32
+  int norm;
+  const float* gamma; const float* beta; float eps;
+  int act;
+  void* Y; int64_t ldy; int64_t sy; int y_f32;
+  int quant; float qmax; float* s_out; uint8_t* q_out; int64_t ldq;
+};
+
+// Where the row statistics of one row block are finished.
+enum RowMode {
+  ROWS_LOCAL = 0,    // the workgroup holds whole rows (or no reduction)
+  ROWS_CLUSTER = 1,  // cn co-resident workgroups exchange partials on chip
+  ROWS_SPLIT = 2     // write fp32 x and partial (mean, M2) for a finish pass
+};
+
+struct GemmRowsParams {
+  int batch, M, N, K;
+  const void* X; int64_t ldx; int64_t sx;
+  const void* W; int64_t ldw; int64_t sw; int w_nk;   // w_nk: W stored N x K
+  RowEpi epi;
+  int mode;            // RowMode
+  int cn;              // workgroups along N per row block
+  int num_rb;          // row blocks = ceil(M / TM)
+  int slots;           // row-block slots per XCD processed concurrently
+  // Workspace views.  Every workspace starts with a fixed header that only
+  // the cluster path touches: an error word and one 64-bit arrival counter
+  // per concurrent peer group ("slot").  Counters only ever grow by whole
+  // multiples of kArriveUnit, so a zero-filled header stays valid across
+  // calls of any shape and path without a reset.
+  unsigned* ws_err;              // sticky flag: a peer wait exceeded its spin limit
+  unsigned long long* ws_arrive; // [kMaxSlots] arrival counters
+  float* ws_part;                // CLUSTER: [2][M][cn] float2; SPLIT: [M][cn] float2
+  float* ws_x;                   // SPLIT: [M][N] fp32 pre-norm x
+};
+
+// lcm(1..16): every peer of a group of cn <= 16 adds kArriveUnit / cn.
+constexpr unsigned long long kArriveUnit = 720720ull;
+constexpr int kMaxSlots = 4096;                      // concurrent peer groups
+constexpr size_t kWsHeaderBytes = 256 + 8 * kMaxSlots;   // err word, then the counters
+
+// Wave-per-row kernel: the finish pass of the split path (merge the partial
+// (mean, M2) of each row's tiles, then stages 2..4 on the fp32 x the GEMM
+// wrote) and the unfused row operator (stages 1..4, or softmax, on a
+// materialised matrix).
+struct RowKernelParams {
+  int M, N;
+  const void* P; int64_t ldp; int p_f32;  // input rows (finish: fp32 x)
+  int finish;                             // 1: statistics from partials
+  int cn, tn;                             // finish: tiles per row, tile width
+  const float* part;                      // finish: [M][cn] (mean, M2)
+  int softmax; float softmax_scale;       // softmax(scale * P) instead
+  RowEpi epi;
+};
+
+struct B2BParams;  // defined with the B2B kernels
+
+// Launchers (return hipSuccess or the launch error).
+hipError_t launch_gemm_rows(const GemmRowsParams& p, int in_f32, int cfg, hipStream_t st);
+hipError_t launch_row_kernel(const RowKernelParams& p, hipStream_t st);
+
+// Tile configurations known to the host planner.
+struct TileCfg {
+  int id;          // index passed to launch_gemm_rows
+  int tm, tn;      // workgroup tile
+  int in_f32;      // operand type
+  int threads;
+};
+int tile_cfg_count();
+const TileCfg& tile_cfg(int i);
+int resident_wgs(int cfg);   // co-resident workgroups of this config on the device
+
+}  // namespace cf

@@ -1,0 +1,154 @@
+"""C-ABI contract tests that need no GPU: the library loads, exports every
+symbol the header declares, and rejects invalid calls before any launch.
+Fake (never dereferenced) device addresses are used: validation returns
+before anything is enqueued, and M = 0 is a no-op."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2608_03537_amd import comfuse as cf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "comfuse.h")
+
+A = 0x7F0000000000          # 16-byte aligned fake device addresses
+B = 0x7F0000100000
+Y = 0x7F0000200000
+R = 0x7F0000300000
+V = 0x7F0000400000
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cf_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    lib = cf.lib()
+    names = header_functions()
+    assert len(names) >= 11
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in comfuse.h but not exported"
+
+
+def test_version_and_status_strings():
+    assert cf.cf_version() == 1
+    for s in range(11):
+        assert cf.cf_status_string(s).startswith(cf.STATUS[s])
+
+
+def _pn(**kw):
+    a = cf.PostnormArgs()
+    a.struct_size = C.sizeof(cf.PostnormArgs)
+    a.M, a.N, a.K = kw.get("M", 64), kw.get("N", 256), kw.get("K", 128)
+    a.in_dtype, a.out_dtype = kw.get("in_dtype", cf.CF_BF16), kw.get("out_dtype", cf.CF_BF16)
+    a.X, a.ldx = kw.get("X", A), kw.get("ldx", a.K)
+    a.W, a.ldw, a.w_layout = kw.get("W", B), kw.get("ldw", a.K), kw.get("w_layout", cf.CF_LAYOUT_NK)
+    a.bias, a.gamma, a.beta = kw.get("bias", V), kw.get("gamma", None), kw.get("beta", None)
+    a.R, a.ldr = kw.get("R", R), kw.get("ldr", a.N)
+    a.alpha, a.eps = 1.0, kw.get("eps", 1e-5)
+    a.Y, a.ldy = kw.get("Y", Y), kw.get("ldy", a.N)
+    a.path = kw.get("path", 0)
+    return a
+
+
+def _call(a, ws=None, nbytes=0):
+    return cf.cf_gemm_postnorm(a, ws, nbytes, None)
+
+
+def test_postnorm_m0_is_noop():
+    assert _call(_pn(M=0)) == 0          # also proves the ctypes layout matches
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(X=None), "CF_ERR_NULL"),
+    (dict(Y=None), "CF_ERR_NULL"),
+    (dict(W=None), "CF_ERR_NULL"),
+    (dict(N=48), "CF_ERR_SHAPE"),
+    (dict(K=40), "CF_ERR_SHAPE"),
+    (dict(M=-1), "CF_ERR_SHAPE"),
+    (dict(N=16384, ldy=16384, ldr=16384), "CF_ERR_SHAPE"),
+    (dict(ldx=64), "CF_ERR_LD"),
+    (dict(ldy=128), "CF_ERR_LD"),
+    (dict(X=A + 2), "CF_ERR_ALIGN"),
+    (dict(ldx=132), "CF_ERR_ALIGN"),
+    (dict(bias=V + 4), "CF_ERR_ALIGN"),
+    (dict(in_dtype=cf.CF_F32, out_dtype=cf.CF_BF16), "CF_ERR_DTYPE"),
+    (dict(in_dtype=cf.CF_FP8_E4M3), "CF_ERR_DTYPE"),
+    (dict(Y=A), "CF_ERR_ALIAS"),
+    (dict(Y=R), "CF_ERR_ALIAS"),
+    (dict(path=1, N=1024, ldy=1024, ldr=1024), "CF_ERR_UNSUPPORTED"),
+    (dict(path=7), "CF_ERR_UNSUPPORTED"),
+])
+def test_postnorm_rejects(kw, status):
+    s = _call(_pn(**kw))
+    assert cf.STATUS[s] == status, cf.cf_last_error()
+    assert cf.cf_last_error()
+
+
+def test_struct_size_checked():
+    a = _pn()
+    a.struct_size = 8
+    assert cf.STATUS[_call(a)] == "CF_ERR_STRUCT"
+
+
+def test_split_workspace_required():
+    a = _pn(path=3, N=1024, ldy=1024, ldr=1024)
+    need = cf.cf_gemm_postnorm_workspace(a)
+    # header + partials M x ceil(N/256) float2 + fp32 x, each rounded to 256 B
+    assert need == 33024 + 64 * 4 * 8 + 64 * 1024 * 4
+    assert cf.STATUS[_call(a)] == "CF_ERR_WORKSPACE"
+    assert cf.STATUS[_call(a, A, need - 1)] == "CF_ERR_WORKSPACE"
+
+
+def test_whole_row_needs_no_workspace():
+    assert cf.cf_gemm_postnorm_workspace(_pn(N=768, ldy=768, ldr=768)) == 0
+
+
+def _sg(nodes, **kw):
+    arr = cf.make_nodes(nodes)
+    a = cf.SubgraphArgs()
+    a.struct_size = C.sizeof(cf.SubgraphArgs)
+    a.M, a.N, a.K = kw.get("M", 64), 256, 128
+    a.in_dtype = cf.CF_BF16
+    a.X, a.ldx, a.W, a.ldw, a.w_layout = A, 128, B, 128, cf.CF_LAYOUT_NK
+    a.nodes, a.n_nodes, a.path = arr, len(nodes), 0
+    return a, arr
+
+
+def test_subgraph_grammar():
+    ok = [dict(kind=cf.CF_N_BIAS, v0=V), dict(kind=cf.CF_N_LAYERNORM, f0=1e-5), dict(kind=cf.CF_N_GELU),
+          dict(kind=cf.CF_N_STORE, out=Y, ld=256, dtype=cf.CF_BF16),
+          dict(kind=cf.CF_N_ROWAMAX_QUANT, out=R, out2=0x7F0000500000, ld=256, f0=448.0)]
+    a, keep = _sg(ok, M=0)
+    assert cf.cf_gemm_subgraph(a, None, 0, None) == 0
+    bad_order = [ok[2], ok[1], ok[3]]
+    a, keep = _sg(bad_order)
+    assert cf.STATUS[cf.cf_gemm_subgraph(a, None, 0, None)] == "CF_ERR_UNSUPPORTED"
+    no_out = ok[:3]
+    a, keep = _sg(no_out)
+    assert cf.STATUS[cf.cf_gemm_subgraph(a, None, 0, None)] == "CF_ERR_UNSUPPORTED"
+    softmax = [dict(kind=cf.CF_N_SOFTMAX, out=Y, ld=256, dtype=cf.CF_BF16, f0=1.0)]
+    a, keep = _sg(softmax)
+    assert cf.STATUS[cf.cf_gemm_subgraph(a, None, 0, None)] == "CF_ERR_UNSUPPORTED"
+    bad_q = ok[:4] + [dict(kind=cf.CF_N_ROWAMAX_QUANT, out=R, out2=0x7F0000500000, ld=250, f0=448.0)]
+    a, keep = _sg(bad_q)
+    assert cf.STATUS[cf.cf_gemm_subgraph(a, None, 0, None)] == "CF_ERR_ALIGN"
+
+
+def test_gemm_and_rowop_validation():
+    st = cf.STATUS
+    assert cf.cf_gemm(1, 0, 256, 128, cf.CF_BF16, cf.CF_BF16, A, 128, 0, B, 128, 0, cf.CF_LAYOUT_NK,
+                      None, 1.0, Y, 256, 0, None) == 0
+    assert st[cf.cf_gemm(1, 64, 250, 128, cf.CF_BF16, cf.CF_BF16, A, 128, 0, B, 128, 0, cf.CF_LAYOUT_NK,
+                         None, 1.0, Y, 256, 0, None)] == "CF_ERR_SHAPE"
+    assert st[cf.cf_gemm(1, 64, 256, 128, cf.CF_BF16, cf.CF_BF16, A, 128, 0, B, 128, 0, cf.CF_LAYOUT_NK,
+                         None, 1.0, A, 256, 0, None)] == "CF_ERR_ALIAS"
+    nodes = cf.make_nodes([dict(kind=cf.CF_N_SOFTMAX, out=Y, ld=256, dtype=cf.CF_BF16, f0=1.0)])
+    assert cf.cf_rowop(0, 256, cf.CF_BF16, A, 256, nodes, 1, None) == 0
+    assert st[cf.cf_rowop(4, 256, cf.CF_BF16, None, 256, nodes, 1, None)] == "CF_ERR_NULL"
+    nodes2 = cf.make_nodes([dict(kind=cf.CF_N_SOFTMAX, out=A, ld=256, dtype=cf.CF_BF16, f0=1.0)])
+    assert st[cf.cf_rowop(4, 256, cf.CF_BF16, A, 256, nodes2, 1, None)] == "CF_ERR_ALIAS"

@@ -316,3 +316,19 @@ def test_ffn_special_case_and_brute_force():
         var = mpmath.fsum((v - mu) ** 2 for v in u) / 8
         yr = [(v - mu) / mpmath.sqrt(var + mpmath.mpf(1e-5)) for v in u]
         np.testing.assert_allclose(Y[i], [float(v) for v in yr], rtol=1e-12, atol=1e-13)
+
+
+def test_rowamax_quant_f32_matches_f64_off_ties():
+    # Decided in fp32 or fp64, codes agree except at rounding ties; on random
+    # data almost every code must agree, and the scales agree to fp32 rounding.
+    z = (np.random.default_rng(21).standard_normal((64, 512)) * 3).astype(np.float32)
+    s64, q64 = O.rowamax_quant(z)
+    s32, q32 = O.rowamax_quant_f32(z)
+    np.testing.assert_allclose(s32, s64, rtol=2 ** -23)
+    diff = q32 != q64
+    assert diff.mean() < 1e-3
+    assert np.all(np.abs(O.e4m3_decode(q32[diff]) - O.e4m3_decode(q64[diff])) <=
+                  np.abs(O.e4m3_decode(q64[diff])) * 0.125 + 2 ** -9)
+    zero = np.zeros((2, 8), np.float32)
+    s, q = O.rowamax_quant_f32(zero)
+    assert np.all(s == 0) and np.all(q == 0)

@@ -1,0 +1,141 @@
+"""GPU parity of cf_gemm_postnorm against the fp64 oracle.
+
+Full-size workloads: fp32 post-norm 128x256x256 (max-abs 1e-4) and the
+BERT-base post-norm 8192x768x768 in bf16 (max-abs 2e-2, rel-RMS 5e-3),
+compared element by element over the whole output.  Small ragged shapes
+cover row tails (M not a multiple of the tile), K tails, masked columns,
+both weight layouts and all three row paths.
+"""
+import numpy as np
+import pytest
+
+from oracle import comfuse_oracle as O
+from paper_2608_03537_amd import inputs as I
+from tests.helpers import assert_close_bf16, assert_close_f32, dev, host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2608_03537_amd import comfuse as cf  # noqa: E402
+
+LAYOUT = {"nk": cf.CF_LAYOUT_NK, "kn": cf.CF_LAYOUT_KN}
+
+
+def run(inp, layout="nk", path=0, out_dtype=None, ws=None):
+    dt = inp.dtype
+    X = dev(inp.X, dt)
+    W = dev(I.lay_out_weight(inp.W, layout), dt)
+    R = dev(inp.R, dt) if inp.R is not None else None
+    vec = lambda v: None if v is None else dev(v, "f32")
+    od = {"bf16": torch.bfloat16, "f32": torch.float32}[out_dtype or dt]
+    Y = cf.gemm_postnorm(X, W, vec(inp.bias), R, vec(inp.gamma), vec(inp.beta), w_layout=LAYOUT[layout],
+                         alpha=inp.alpha, eps=inp.eps, out_dtype=od, path=path, ws=ws)
+    torch.cuda.synchronize()
+    return host(Y)
+
+
+def ref(inp):
+    return O.postnorm(inp.X, inp.W, inp.bias, inp.R, inp.gamma, inp.beta, inp.alpha, inp.eps)
+
+
+def test_tiny_fp32_full():
+    inp = I.postnorm_tiny_fp32()
+    assert_close_f32(run(inp), ref(inp), "fp32 128x256x256")
+
+
+@pytest.mark.parametrize("path", [0, 1, 2, 3])
+def test_bert_base_full(path):
+    inp = I.bert_base_postnorm()
+    got = run(inp, path=path)
+    assert_close_bf16(got, ref(inp), f"BERT-base path {path}")
+
+
+SMALL = [  # (M, K, N)
+    (100, 64, 128),
+    (77, 48, 256),
+    (129, 96, 352),
+    (33, 784, 768),
+    (1, 32, 64),
+    (257, 128, 384),
+]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("layout", ["nk", "kn"])
+@pytest.mark.parametrize("M,K,N", SMALL)
+def test_small_shapes_all_paths(M, K, N, layout, dtype):
+    inp = I.postnorm_inputs(M, K, N, dtype, seed=3, bias_std=0.5, gamma="uniform", beta_std=0.3)
+    r = ref(inp)
+    check = assert_close_f32 if dtype == "f32" else assert_close_bf16
+    for path in (1, 2, 3):
+        if path == 1 and N > 768:
+            continue
+        if path == 2 and not any(N % t == 0 for t in ((256, 128) if dtype == "f32" else (256, 192, 128))):
+            with pytest.raises(cf.CfError, match="UNSUPPORTED"):
+                run(inp, layout, path)
+            continue
+        check(run(inp, layout, path), r, f"{M}x{K}x{N} {layout} {dtype} path {path}")
+
+
+def test_bf16_in_f32_out():
+    inp = I.postnorm_inputs(200, 256, 512, "bf16", seed=5)
+    assert_close_f32(run(inp, out_dtype="f32"), ref(inp), "bf16 in / fp32 out")
+
+
+def test_alpha_and_no_optional_vectors():
+    inp = I.postnorm_inputs(96, 128, 256, "f32", seed=6, with_bias=False, with_residual=False,
+                            with_affine=False, alpha=0.37)
+    for path in (1, 2, 3):
+        assert_close_f32(run(inp, path=path), ref(inp), f"alpha path {path}")
+
+
+def test_constant_rows_give_beta():
+    inp = I.postnorm_inputs(64, 64, 256, "f32", seed=7)
+    inp.X[:] = 0.0
+    inp.bias = None
+    # Row constants k/8: every partial sum of a row is exact in fp32, so the
+    # mean is exact, x - mean is exactly 0 and y must equal beta bit for bit.
+    inp.R[:] = np.repeat(((np.arange(64) - 32) / 8.0).astype(np.float32)[:, None], 256, axis=1)
+    for path in (1, 2, 3):
+        got = run(inp, path=path)
+        assert np.array_equal(got, np.broadcast_to(inp.beta.astype(np.float64), got.shape)), path
+
+
+def test_layernorm_invariants_on_gpu():
+    inp = I.postnorm_inputs(512, 256, 768, "f32", seed=8, with_affine=False, r_std=3.0)
+    y = run(inp)
+    x = O.bias_residual(O.matmul(inp.X, inp.W), inp.bias, inp.R)
+    var = x.var(axis=1)
+    assert np.max(np.abs(y.mean(axis=1))) < 1e-5
+    np.testing.assert_allclose((y * y).mean(axis=1), var / (var + inp.eps), rtol=2e-5)
+
+
+@pytest.mark.parametrize("path", [1, 2, 3])
+def test_bitwise_deterministic(path):
+    inp = I.bert_base_postnorm(M=2048)
+    a, b = run(inp, path=path), run(inp, path=path)
+    assert np.array_equal(a, b)
+
+
+def test_cluster_flags_clean_and_reusable():
+    inp = I.postnorm_inputs(1000, 128, 768, "bf16", seed=9)
+    ws = torch.zeros(8 << 20, dtype=torch.uint8, device="cuda")
+    r = ref(inp)
+    for _ in range(3):
+        assert_close_bf16(run(inp, path=2, ws=ws), r, "cluster reuse")
+    # Header: [err word | 256 B][64-bit arrival counters x 4096][partials ...]
+    err = ws[:4].view(torch.int32).cpu().numpy()
+    ctr = ws[256:256 + 8 * 4096].view(torch.int64).cpu().numpy()
+    assert err[0] == 0                       # no peer wait timed out
+    assert np.any(ctr > 0)                   # the cluster path did run
+    assert np.all(ctr % 720720 == 0)         # every peer group completed
+
+
+def test_m0_noop():
+    X = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    W = torch.zeros((128, 64), dtype=torch.bfloat16, device="cuda")
+    Y = cf.gemm_postnorm(X, W)
+    assert Y.shape == (0, 128)

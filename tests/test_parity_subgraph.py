@@ -1,0 +1,159 @@
+"""GPU parity of cf_gemm_subgraph / cf_rowop (the Stage-Stream node lists)
+against the fp64 oracle.
+
+The LN -> GELU -> row-amax -> E4M3 chain: Z (bf16) within max-abs 2e-2 /
+rel-RMS 5e-3, s within relative 1e-3, codes equal to the oracle's for at least
+99.99 % of elements with every mismatch one code step away (Z differs from
+the exact value by bf16 GEMM rounding, so codes at rounding boundaries can
+move by one step).  With Z stored in fp32 the quantisation stage is checked
+bit-exactly against the kernel's own z, deciding in fp32 on both sides.
+"""
+import numpy as np
+import pytest
+
+from oracle import comfuse_oracle as O
+from paper_2608_03537_amd import inputs as I
+from tests.helpers import assert_close_bf16, assert_close_f32, dev, host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2608_03537_amd import comfuse as cf  # noqa: E402
+
+
+def signed_code_index(q):
+    q = np.asarray(q, np.int64)
+    return np.where(q & 0x80, -(q & 0x7F), q & 0x7F)
+
+
+def check_codes(q_gpu, q_ref, min_equal=0.9999):
+    eq = np.mean(q_gpu == q_ref)
+    step = np.abs(signed_code_index(q_gpu) - signed_code_index(q_ref))
+    assert eq >= min_equal, f"codes equal {eq:.6f}"
+    assert step.max() <= 1, f"max code step {step.max()}"
+    return eq
+
+
+def run_chain(inp, path=0, z_f32=False, layout="nk", gelu=cf.CF_N_GELU):
+    X = dev(inp.X, inp.dtype)
+    W = dev(I.lay_out_weight(inp.W, layout), inp.dtype)
+    R = dev(inp.R, inp.dtype) if inp.R is not None else None
+    b = dev(inp.bias, "f32") if inp.bias is not None else None
+    Z, s, Q = cf.ln_gelu_amax(X, W, b, R, eps=inp.eps, z_dtype=torch.float32 if z_f32 else None,
+                              w_layout=cf.CF_LAYOUT_NK if layout == "nk" else cf.CF_LAYOUT_KN, path=path,
+                              gelu=gelu)
+    torch.cuda.synchronize()
+    return host(Z), s.cpu().numpy(), Q.cpu().numpy()
+
+
+@pytest.mark.parametrize("path", [1, 2, 3])
+@pytest.mark.parametrize("N", [256, 768, 1024])
+def test_chain_small(N, path):
+    if path == 1 and N > 768:
+        pytest.skip("whole-row path covers N <= 768")
+    inp = I.postnorm_inputs(150, 128, N, "bf16", seed=11, with_affine=False)
+    z, s, q = O.ln_gelu_amax(inp.X, inp.W, inp.bias, inp.R, eps=inp.eps)
+    Zg, sg, Qg = run_chain(inp, path)
+    assert_close_bf16(Zg, z, f"Z N={N} path {path}")
+    np.testing.assert_allclose(sg, s, rtol=1e-3)
+    check_codes(Qg, q, min_equal=0.999)
+
+
+@pytest.mark.parametrize("path", [1, 2, 3])
+def test_chain_quant_exact_against_own_z(path):
+    inp = I.postnorm_inputs(97, 64, 512, "f32", seed=12, with_affine=False)
+    Zg, sg, Qg = run_chain(inp, path, z_f32=True)
+    s32, q32 = O.rowamax_quant_f32(Zg.astype(np.float32))
+    assert np.array_equal(sg, s32)
+    assert np.array_equal(Qg, q32)
+    z, _, _ = O.ln_gelu_amax(inp.X, inp.W, inp.bias, inp.R, eps=inp.eps)
+    assert_close_f32(Zg, z, "fp32 chain")
+
+
+def test_gelu_tanh_variant_is_the_tanh_one():
+    inp = I.postnorm_inputs(64, 64, 256, "f32", seed=13, with_affine=False)
+    Zg, _, _ = run_chain(inp, 1, z_f32=True, gelu=cf.CF_N_GELU_TANH)
+    y = O.postnorm(inp.X, inp.W, inp.bias, inp.R, eps=inp.eps)
+    assert_close_f32(Zg, O.gelu_tanh(y), "tanh GELU")
+    assert np.max(np.abs(Zg - O.gelu_erf(y))) > 2e-4
+
+
+@pytest.mark.parametrize("path", [0, 2])
+def test_chain_full_size_sampled_rows(path):
+    inp = I.ln_gelu_amax_inputs()
+    Zg, sg, Qg = run_chain(inp, path)
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, inp.M - 1],
+                                     np.random.default_rng(0).choice(inp.M, 59, replace=False)]))
+    z, s, q = O.ln_gelu_amax(inp.X[rows], inp.W, inp.bias, inp.R[rows], eps=inp.eps)
+    assert_close_bf16(Zg[rows], z, f"cfg3 Z path {path}")
+    np.testing.assert_allclose(sg[rows], s, rtol=1e-3)
+    check_codes(Qg[rows], q)
+    # Properties that hold at any size: every row's largest code is +-448.
+    assert np.all(np.max(np.abs(O.e4m3_decode(Qg[::97])), axis=1) == 448.0)
+
+
+@pytest.mark.parametrize("norm", ["rms", "ln_relu"])
+def test_other_stage_stream_patterns(norm):
+    # MatMul-BiasAdd-RMSNorm and MatMul-BiasAdd-LayerNorm-ReLU (Sec. VI).
+    inp = I.postnorm_inputs(130, 96, 512, "f32", seed=14, with_residual=False)
+    X, W = dev(inp.X, "f32"), dev(I.lay_out_weight(inp.W, "nk"), "f32")
+    b, g, be = dev(inp.bias, "f32"), dev(inp.gamma, "f32"), dev(inp.beta, "f32")
+    for path in (1, 2, 3):
+        Y = torch.empty((inp.M, inp.N), dtype=torch.float32, device="cuda")
+        if norm == "rms":
+            spec = [dict(kind=cf.CF_N_BIAS, v0=b), dict(kind=cf.CF_N_RMSNORM, v0=g, f0=1e-5),
+                    dict(kind=cf.CF_N_STORE, out=Y, ld=inp.N, dtype=cf.CF_F32)]
+            r = O.rmsnorm(O.bias_residual(O.matmul(inp.X, inp.W), inp.bias), inp.gamma, 1e-5)
+        else:
+            spec = [dict(kind=cf.CF_N_BIAS, v0=b), dict(kind=cf.CF_N_LAYERNORM, v0=g, v1=be, f0=1e-5),
+                    dict(kind=cf.CF_N_RELU), dict(kind=cf.CF_N_STORE, out=Y, ld=inp.N, dtype=cf.CF_F32)]
+            r = O.relu(O.postnorm(inp.X, inp.W, inp.bias, None, inp.gamma, inp.beta, 1.0, 1e-5))
+        cf.gemm_subgraph(X, W, spec, path=path)
+        torch.cuda.synchronize()
+        assert_close_f32(host(Y), r, f"{norm} path {path}")
+
+
+def test_rowop_quant_encoder_exact():
+    # Rows built so that z/s hits every E4M3 value, every midpoint between
+    # neighbours, and values just either side of each midpoint.
+    vals = O.e4m3_decode(np.arange(0, 0x7F)).astype(np.float64)
+    mids = (vals[:-1] + vals[1:]) / 2
+    pts = np.concatenate([vals, mids, np.nextafter(mids.astype(np.float32), np.float32(0)),
+                          np.nextafter(mids.astype(np.float32), np.float32(1e9))]).astype(np.float32)
+    pts = np.concatenate([pts, -pts])
+    n = ((len(pts) + 255) // 256) * 256
+    row = np.zeros(n, np.float32)
+    row[:len(pts)] = pts
+    P = np.stack([row, row * np.float32(0.5), row * np.float32(1e-3), np.zeros(n, np.float32)])
+    Pd = dev(P, "f32")
+    s = torch.empty(4, dtype=torch.float32, device="cuda")
+    Q = torch.empty((4, n), dtype=torch.uint8, device="cuda")
+    cf.rowop(Pd, [dict(kind=cf.CF_N_ROWAMAX_QUANT, out=s, out2=Q, ld=n, f0=448.0)])
+    torch.cuda.synchronize()
+    s32, q32 = O.rowamax_quant_f32(P)
+    assert np.array_equal(s.cpu().numpy(), s32)
+    qg = Q.cpu().numpy()
+    bad = np.argwhere(qg != q32)
+    assert len(bad) == 0, [(int(i), int(j), float(P[i, j]), hex(qg[i, j]), hex(q32[i, j])) for i, j in bad[:8]]
+
+
+def test_rowop_matches_fused_chain():
+    inp = I.postnorm_inputs(70, 64, 384, "bf16", seed=15, with_affine=False)
+    X, W = dev(inp.X), dev(I.lay_out_weight(inp.W, "nk"))
+    b, R = dev(inp.bias, "f32"), dev(inp.R)
+    P = cf.gemm(X, W, out_dtype=torch.float32)
+    Z = torch.empty((70, 384), dtype=torch.bfloat16, device="cuda")
+    s = torch.empty(70, dtype=torch.float32, device="cuda")
+    Q = torch.empty((70, 384), dtype=torch.uint8, device="cuda")
+    cf.rowop(P, [dict(kind=cf.CF_N_BIAS, v0=b), dict(kind=cf.CF_N_RESIDUAL, **{"in": R}, ld=384, dtype=cf.CF_BF16),
+                 dict(kind=cf.CF_N_LAYERNORM, f0=1e-5), dict(kind=cf.CF_N_GELU),
+                 dict(kind=cf.CF_N_STORE, out=Z, ld=384, dtype=cf.CF_BF16),
+                 dict(kind=cf.CF_N_ROWAMAX_QUANT, out=s, out2=Q, ld=384, f0=448.0)])
+    torch.cuda.synchronize()
+    z, sr, q = O.ln_gelu_amax(inp.X, inp.W, inp.bias, inp.R, eps=1e-5)
+    assert_close_bf16(host(Z), z, "unfused chain")
+    np.testing.assert_allclose(s.cpu().numpy(), sr, rtol=1e-3)
+    check_codes(Q.cpu().numpy(), q, min_equal=0.999)
