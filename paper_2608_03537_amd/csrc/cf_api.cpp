@@ -10,7 +10,7 @@
 #include <cstring>
 #include <string>
 
-#include "../../include/comfuse.h"
+#include "comfuse.h"
 #include "cf_internal.h"
 
 using namespace cf;
@@ -68,18 +68,12 @@ constexpr int kWholeRowMaxN = 768;
 constexpr int kClusterMaxPeers = 16;
 
 struct Plan {
-  int cfg = -1, mode = ROWS_LOCAL, cn = 1, num_rb = 0, slots = 0, tm = 0, tn = 0;
+  int kidx = -1, mode = ROWS_LOCAL, cn = 1, num_rb = 0, slots = 0, tm = 0, tn = 0;
   size_t ws = 0;
   size_t off_part = 0, off_x = 0;
 };
 
-int find_cfg(int in_f32, int tm, int tn) {
-  for (int i = 0; i < tile_cfg_count(); ++i) {
-    const TileCfg& t = tile_cfg(i);
-    if (t.in_f32 == in_f32 && t.tm == tm && t.tn == tn) return i;
-  }
-  return -1;
-}
+constexpr int kAssumedCUs = 256;   // MI355X; used only to rank tile widths
 
 // Every non-empty workspace starts with the fixed header (error word and
 // arrival counters; only the cluster path writes it).  Then the cluster path
@@ -97,43 +91,69 @@ void size_workspace(Plan& pl, int64_t M, int64_t N) {
   }
 }
 
-// Chooses the tiling for a row-subgraph GEMM.  `need_rows` is false when the
-// epilogue has no row reduction (then any tiling is valid).
-cf_status plan_rows(int64_t M, int64_t N, int in_f32, int path, bool need_rows, bool probe_device,
-                    Plan& pl) {
+// Picks the 128-row tile width: the one whose workgroups, laid out in waves
+// of one workgroup per CU, give the least work per CU (rounds x width).
+// `divides` restricts to widths that split N exactly into <= max_cn peers.
+int pick_tile(int64_t M, int64_t N, int in_f32, int loop, int epi, bool divides, int max_cn) {
+  int best = -1;
+  double best_cost = 1e300;
+  for (int tn : {256, 192, 128}) {
+    const int idx = find_gemm_kernel(in_f32, 128, tn, loop, epi);
+    if (idx < 0) continue;
+    const int64_t cn = (N + tn - 1) / tn;
+    if (divides && (N % tn != 0 || cn > max_cn)) continue;
+    const int64_t wgs = ((M + 127) / 128) * cn;
+    const double cost = (double)((wgs + kAssumedCUs - 1) / kAssumedCUs) * tn - 1e-3 * tn;
+    if (cost < best_cost) { best_cost = cost; best = idx; }
+  }
+  return best;
+}
+
+// Chooses kernel and row path for a GEMM (+ row subgraph).  `need_rows` is
+// false when the epilogue has no row reduction (then any tiling is valid).
+cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int path, bool need_rows,
+                    bool probe_device, Plan& pl) {
   pl = Plan();
+  const int tk = in_f32 ? 32 : 64;                     // k per 128-byte stage
+  const int loop = (w_nk && K % tk == 0) ? 1 : 0;
   if (!need_rows) {
-    const int tn = (N >= 256) ? 256 : 128;
-    pl.cfg = find_cfg(in_f32, 128, tn);
+    pl.kidx = pick_tile(M, N, in_f32, loop, 0, false, 0);
+    if (pl.kidx < 0) pl.kidx = pick_tile(M, N, in_f32, 0, 0, false, 0);
     pl.mode = ROWS_LOCAL;
   } else {
-    if (path == PATH_AUTO) path = (N <= kWholeRowMaxN) ? PATH_WHOLE_ROW : PATH_SPLIT;
+    if (path == PATH_AUTO) {
+      // Row clusters when N splits into <= kClusterMaxPeers tiles and the
+      // peers fit on the device; else whole rows for narrow N; else split-N.
+      path = PATH_SPLIT;
+      if (pick_tile(M, N, in_f32, loop, 1, true, kClusterMaxPeers) >= 0 ||
+          pick_tile(M, N, in_f32, 0, 1, true, kClusterMaxPeers) >= 0)
+        path = PATH_CLUSTER;
+      else if (N <= kWholeRowMaxN)
+        path = PATH_WHOLE_ROW;
+    }
     if (path == PATH_WHOLE_ROW) {
       if (N > kWholeRowMaxN)
         return fail(CF_ERR_UNSUPPORTED, "whole-row path needs N <= %d (N = %lld)", kWholeRowMaxN, (long long)N);
-      static const int tns[] = {128, 256, 384, 512, 768};
-      for (int tn : tns)
-        if (tn >= N) { pl.cfg = find_cfg(in_f32, 32, tn); break; }
+      for (int tn : {128, 256, 384, 512, 768})
+        if (tn >= N) { pl.kidx = find_gemm_kernel(in_f32, 32, tn, 0, 1); break; }
       pl.mode = ROWS_LOCAL;
     } else if (path == PATH_CLUSTER) {
-      static const int tns[] = {256, 192, 128};
-      for (int tn : tns) {
-        const int c = find_cfg(in_f32, 128, tn);
-        if (c >= 0 && N % tn == 0 && N / tn <= kClusterMaxPeers) { pl.cfg = c; break; }
-      }
-      if (pl.cfg < 0)
+      pl.kidx = pick_tile(M, N, in_f32, loop, 1, true, kClusterMaxPeers);
+      if (pl.kidx < 0) pl.kidx = pick_tile(M, N, in_f32, 0, 1, true, kClusterMaxPeers);
+      if (pl.kidx < 0)
         return fail(CF_ERR_UNSUPPORTED, "cluster path: no tile width divides N = %lld into <= %d peers",
                     (long long)N, kClusterMaxPeers);
       pl.mode = ROWS_CLUSTER;
     } else if (path == PATH_SPLIT) {
-      pl.cfg = find_cfg(in_f32, 128, 256);
+      pl.kidx = pick_tile(M, N, in_f32, loop, 1, false, 0);
+      if (pl.kidx < 0) pl.kidx = pick_tile(M, N, in_f32, 0, 1, false, 0);
       pl.mode = ROWS_SPLIT;
     } else {
       return fail(CF_ERR_UNSUPPORTED, "unknown path %d", path);
     }
   }
-  if (pl.cfg < 0) return fail(CF_ERR_UNSUPPORTED, "no compiled tile for this shape");
-  const TileCfg& t = tile_cfg(pl.cfg);
+  if (pl.kidx < 0) return fail(CF_ERR_UNSUPPORTED, "no compiled tile for this shape");
+  const GemmKernel& t = gemm_kernel(pl.kidx);
   pl.tm = t.tm;
   pl.tn = t.tn;
   pl.cn = (int)((N + t.tn - 1) / t.tn);
@@ -141,7 +161,7 @@ cf_status plan_rows(int64_t M, int64_t N, int in_f32, int path, bool need_rows, 
   pl.slots = (pl.num_rb + 7) / 8;
   if (pl.mode == ROWS_CLUSTER && probe_device) {
     // Every peer group must be resident at once: cap the persistent grid.
-    const int cap = resident_wgs(pl.cfg);
+    const int cap = resident_wgs(pl.kidx);
     const int slots = cap / (8 * pl.cn);
     if (slots < 1) return fail(CF_ERR_UNSUPPORTED, "cluster path: %d peers do not fit the device", pl.cn);
     pl.slots = std::min(pl.slots, std::min(slots, kMaxSlots / 8));
@@ -176,7 +196,7 @@ cf_status run_rows(const Plan& pl, GemmRowsParams p, void* ws, hipStream_t st) {
     p.epi.act = ACT_NONE;
     p.epi.Y = nullptr;
     p.epi.quant = 0;
-    cf_status s = hip_status(launch_gemm_rows(p, tile_cfg(pl.cfg).in_f32, pl.cfg, st), "GEMM launch");
+    cf_status s = hip_status(launch_gemm_rows(p, pl.kidx, st), "GEMM launch");
     if (s != CF_OK) return s;
     RowKernelParams f{};
     f.M = p.M;
@@ -194,7 +214,7 @@ cf_status run_rows(const Plan& pl, GemmRowsParams p, void* ws, hipStream_t st) {
     f.epi.R = nullptr;
     return hip_status(launch_row_kernel(f, st), "finish launch");
   }
-  return hip_status(launch_gemm_rows(p, tile_cfg(pl.cfg).in_f32, pl.cfg, st), "GEMM launch");
+  return hip_status(launch_gemm_rows(p, pl.kidx, st), "GEMM launch");
 }
 
 // ---------------------------------------------------------------------------
@@ -326,7 +346,9 @@ cf_status rows_common(int64_t M, int64_t N, int64_t K, cf_dtype in, const void* 
   if ((s = check_matrix("W", W, 1, wl == CF_LAYOUT_NK ? K : N, ldw, in, true)) != CF_OK) return s;
   const bool need_rows = epi.norm != NORM_NONE || epi.quant;
   Plan pl;
-  if ((s = plan_rows(M, N, in == CF_F32, path, need_rows, !size_only && M > 0, pl)) != CF_OK) return s;
+  // Validation and sizing never touch the device; residency is queried only
+  // right before a launch.
+  if ((s = plan_rows(M, N, K, in == CF_F32, wl == CF_LAYOUT_NK, path, need_rows, false, pl)) != CF_OK) return s;
   if (size_only) {
     *ws_out = pl.ws;
     return CF_OK;
@@ -334,12 +356,16 @@ cf_status rows_common(int64_t M, int64_t N, int64_t K, cf_dtype in, const void* 
   for (const void* out : {(const void*)epi.Y, (const void*)epi.s_out, (const void*)epi.q_out})
     if (outputs_alias(out, {X, W, epi.R, (const void*)epi.bias, (const void*)epi.gamma, (const void*)epi.beta}))
       return fail(CF_ERR_ALIAS, "an output aliases an input");
+  if (M == 0) return CF_OK;   // nothing to compute: no workspace needed
   if (pl.ws > 0) {
     if (!ws) return fail(CF_ERR_WORKSPACE, "workspace of %zu bytes required", pl.ws);
     if (ws_bytes < pl.ws) return fail(CF_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, pl.ws);
     if (!aligned16(ws)) return fail(CF_ERR_ALIGN, "workspace is not 16-byte aligned");
   }
   if (M == 0) return CF_OK;
+  if (pl.mode == ROWS_CLUSTER &&
+      (s = plan_rows(M, N, K, in == CF_F32, wl == CF_LAYOUT_NK, path, need_rows, true, pl)) != CF_OK)
+    return s;
   GemmRowsParams p{};
   p.batch = 1;
   p.M = (int)M;
@@ -489,7 +515,8 @@ cf_status cf_gemm(int64_t batch, int64_t M, int64_t N, int64_t K, cf_dtype in, c
     if (outputs_alias(C, {A, B, (const void*)bias})) return fail(CF_ERR_ALIAS, "C aliases an input");
     if (M == 0 || batch == 0) return CF_OK;
     Plan pl;
-    if ((s = plan_rows(M, N, in == CF_F32, PATH_AUTO, false, false, pl)) != CF_OK) return s;
+    if ((s = plan_rows(M, N, K, in == CF_F32, b_layout == CF_LAYOUT_NK, PATH_AUTO, false, false, pl)) != CF_OK)
+      return s;
     GemmRowsParams p{};
     p.batch = (int)batch;
     p.M = (int)M;

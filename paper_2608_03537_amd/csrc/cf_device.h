@@ -100,6 +100,7 @@ template <typename T> struct Mma;
 
 template <> struct Mma<bf16_t> {
   static constexpr int kPerChunk = 8;   // bf16 values per 16-byte chunk
+  static constexpr int kInstrs = 1;     // MFMA instructions per run()
   __device__ __forceinline__ static void run(f32x16_t& acc, u32x4_t a, u32x4_t b) {
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                   __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
@@ -108,6 +109,7 @@ template <> struct Mma<bf16_t> {
 
 template <> struct Mma<float> {
   static constexpr int kPerChunk = 4;   // fp32 values per 16-byte chunk
+  static constexpr int kInstrs = 4;     // MFMA instructions per run()
   // Four k=2 MFMAs: step j pairs element j of lane group 0 with element j of
   // lane group 1, so the four together cover the 8 k values of the chunk pair.
   __device__ __forceinline__ static void run(f32x16_t& acc, u32x4_t a, u32x4_t b) {

@@ -1,4 +1,4 @@
-// GEMM + row-subgraph kernels for gfx950.
+// GEMM + row-subgraph kernel template for gfx950 (instantiated in cf_gemm_inst_*.hip).
 //
 // One tiled MFMA GEMM template whose epilogue runs the Stage-Stream stage
 // chain (Sec. III) on the accumulator tile while it is still in registers:
@@ -25,6 +25,8 @@
 //   ROWS_SPLIT: each workgroup writes fp32 x and its partial (mean, M2); a
 //     light finish pass merges them (Chan et al.'s pairwise update) and runs
 //     stages 2..4.
+#pragma once
+
 #include "cf_device.h"
 #include "cf_internal.h"
 
@@ -32,9 +34,13 @@ namespace cf {
 
 constexpr int kSpinLimit = 1 << 22;   // bounded wait for peers (~1 s)
 
-template <typename TIn, int BM_, int BN_, int WM_, int WN_, int TKB_>
+template <typename TIn, int BM_, int BN_, int WM_, int WN_, int TKB_, int STAGES_ = 0>
 struct TileShape {
   using T = TIn;
+  // STAGES > 0 selects the direct-to-LDS pipeline (mainloop_v2) for weights
+  // stored N x K with K a multiple of the 128-byte stage; the register-staged
+  // loop (mainloop) remains for K x N weights and ragged K.
+  static constexpr int STAGES = STAGES_;
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr int NW = WM * WN, NT = 64 * NW;
   static constexpr int WTM = 32 * BM, WTN = 32 * BN;     // wave tile (m, n)
@@ -47,11 +53,22 @@ struct TileShape {
   static constexpr int ROWB = TKB + 16;                   // padded LDS row
   static constexpr int A_BYTES = TN * ROWB, B_BYTES = TM * ROWB;
   static constexpr int STAGE = A_BYTES + B_BYTES;
-  static constexpr int LDS = 2 * STAGE;
+  static constexpr int V2_ROWB = 128;                    // bytes of k per row per stage
+  static constexpr int V2_TK = V2_ROWB / (int)sizeof(T);
+  static constexpr int V2_STAGE = (TM + TN) * V2_ROWB;
+  static constexpr int V2_INSTR = (TM + TN) / 8;          // 8 rows per wave-wide load
+  static constexpr int V2_PER_WAVE = V2_INSTR / NW;
+  static constexpr int LDS_V1 = 2 * STAGE;
+  static constexpr int LDS_V2 = STAGES * V2_STAGE;
+  static_assert(STAGES == 0 || (V2_INSTR % NW == 0 && STAGES >= 2), "v2 pipeline shape");
+  static_assert(STAGES == 0 || V2_PER_WAVE * (STAGES - 2) < 64, "vmcnt range");
   static constexpr int A_CHUNKS = TN * CPR, B_CHUNKS = TM * CPR;
   static constexpr int A_PT = (A_CHUNKS + NT - 1) / NT;
   static constexpr int B_PT = (B_CHUNKS + NT - 1) / NT;
-  static_assert(LDS <= 160 * 1024, "LDS budget");
+  static constexpr int LDS_STORE = TM * (TN * 4 + 16);   // staged output tile (fp32 worst case)
+  static constexpr int SMEM_V1 = LDS_V1 > LDS_STORE ? LDS_V1 : LDS_STORE;
+  static constexpr int SMEM_V2 = LDS_V2 > LDS_STORE ? LDS_V2 : LDS_STORE;
+  static_assert(SMEM_V1 <= 160 * 1024 && SMEM_V2 <= 160 * 1024, "LDS budget");
   static_assert(TK % KSTEP == 0, "stage must hold whole MFMA steps");
 };
 
@@ -183,6 +200,141 @@ __device__ __forceinline__ void mainloop(f32x16_t (&acc)[S::BM][S::BN],
   }
 }
 
+// 16-byte global -> LDS copy for the whole wave: lane i's 16 bytes land at
+// LDS address lds + 16 * i (lds must be wave-uniform).
+__device__ __forceinline__ void dma16(const void* gptr, char* lds) {
+  __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+// Workgroup barrier without the implicit wait for outstanding memory
+// operations (callers wait explicitly); also a compiler reordering fence.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14]
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// ---------------------------------------------------------------------------
+// Main loop v2: direct global -> LDS loads (global_load_lds_dwordx4), a ring
+// of S::STAGES stages, no register staging.  A stage holds 128 bytes of k for
+// the TN rows of W^T followed by the TM rows of X.
+//
+// LDS layout: within a row the eight 16-byte chunks are XOR-swizzled by
+// ((row >> 1) & 7).  gfx950 serves a 64-lane ds_read_b128 in 16-lane groups
+// over 64 four-byte banks; the 16 lanes of a group read one chunk column of 16
+// consecutive rows, and this swizzle puts them on 16 distinct 16-byte bank
+// groups (rows 2j and 2j+1 differ by 128 bytes, the pairs by the swizzle).
+// A wave-wide load writes 1 KB of consecutive LDS = 8 rows, lane i filling
+// row i/8 at chunk position i%8.
+//
+// Schedule of one stage: the fragments of MFMA step ks+1 are read while the
+// MFMAs of step ks issue, and the wave-wide loads of stage kt+S-1 are spread
+// between the MFMAs (sched_group_barrier), so neither LDS latency nor load
+// issue stalls the matrix pipe.  Loads past the last stage re-read the last
+// stage into a buffer that is no longer read, which keeps every iteration's
+// vmcnt bookkeeping identical.
+//
+// Rows past M (or N) are clamped to the last valid row: they only feed output
+// rows/columns that the epilogue masks.
+// ---------------------------------------------------------------------------
+template <class S>
+__device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
+                                            const typename S::T* __restrict__ X,
+                                            const typename S::T* __restrict__ W,
+                                            const GemmRowsParams& p, int m0, int n0,
+                                            char* smem, int lane, int wave, int wm, int wn) {
+  using T = typename S::T;
+#pragma unroll
+  for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+    for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[bm][bn][i] = 0.0f;
+
+  const int KT = p.K / S::V2_TK;
+  const char* src[S::V2_PER_WAVE];
+#pragma unroll
+  for (int j = 0; j < S::V2_PER_WAVE; ++j) {
+    const int row = (wave + j * S::NW) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    if (row < S::TN) {
+      const int n = min(n0 + row, p.N - 1);
+      src[j] = reinterpret_cast<const char*>(W + (int64_t)n * p.ldw) + c * 16;
+    } else {
+      const int m = min(m0 + row - S::TN, p.M - 1);
+      src[j] = reinterpret_cast<const char*>(X + (int64_t)m * p.ldx) + c * 16;
+    }
+  }
+  auto dma = [&](int j, int kt) {
+    const int ks = kt < KT ? kt : KT - 1;
+    dma16(src[j] + (int64_t)ks * S::V2_ROWB,
+          smem + (kt % S::STAGES) * S::V2_STAGE + (wave + j * S::NW) * 1024);
+  };
+
+  constexpr int KS = S::V2_TK / S::KSTEP;          // MFMA steps per stage
+  constexpr int NFR = S::BN + S::BM;               // fragment reads per step
+  constexpr int NMF = S::BN * S::BM;               // MFMAs per step
+  constexpr int DPS = (S::V2_PER_WAVE + KS - 1) / KS;   // loads issued per step
+  const int lr = lane & 31, lg = lane >> 5, sw = (lr >> 1) & 7;
+
+#pragma unroll
+  for (int s = 0; s < S::STAGES - 1; ++s)
+#pragma unroll
+    for (int j = 0; j < S::V2_PER_WAVE; ++j) dma(j, s);
+
+  for (int kt = 0; kt < KT; ++kt) {
+    // This wave's loads of stage kt have landed once at most the younger
+    // stages' loads are outstanding; the barrier then covers every wave.
+    wait_vmcnt<S::V2_PER_WAVE * (S::STAGES - 2)>();
+    lds_barrier();
+    const int buf = kt % S::STAGES;
+    const char* sA = smem + buf * S::V2_STAGE + (wn * S::WTN + lr) * S::V2_ROWB;
+    const char* sB = smem + buf * S::V2_STAGE + (S::TN + wm * S::WTM + lr) * S::V2_ROWB;
+    u32x4_t a[2][S::BN], b[2][S::BM];
+    auto frag = [&](int ks, int r) {
+      const int off = ((2 * ks + lg) ^ sw) << 4;
+#pragma unroll
+      for (int bn = 0; bn < S::BN; ++bn) a[r][bn] = lds_read16(sA + bn * 32 * S::V2_ROWB + off);
+#pragma unroll
+      for (int bm = 0; bm < S::BM; ++bm) b[r][bm] = lds_read16(sB + bm * 32 * S::V2_ROWB + off);
+    };
+    frag(0, 0);
+    const int nxt = kt + S::STAGES - 1;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) frag(ks + 1, (ks + 1) & 1);
+#pragma unroll
+      for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+        for (int bn = 0; bn < S::BN; ++bn) Mma<T>::run(acc[bm][bn], a[ks & 1][bn], b[ks & 1][bm]);
+#pragma unroll
+      for (int d = 0; d < DPS; ++d)
+        if (ks * DPS + d < S::V2_PER_WAVE) dma(ks * DPS + d, nxt);
+    }
+    // Issue order: first step's fragment reads, then per step MFMAs
+    // interleaved one-to-one with the next step's reads and the loads.
+    __builtin_amdgcn_sched_group_barrier(0x100, NFR, 0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int i = 0; i < NMF; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, Mma<T>::kInstrs, 0);
+        if (ks + 1 < KS && i < NFR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        if (i < DPS && ks * DPS + i < S::V2_PER_WAVE) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
+    }
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+}
+
 // ---------------------------------------------------------------------------
 // Row reductions over the values a workgroup holds (levels 1 and 2).
 // v[bm] is this lane's partial for row (wm*WTM + bm*32 + lane%32).
@@ -214,36 +366,44 @@ __device__ __forceinline__ void wg_row_reduce(float (&v)[S::BM], float* red, int
   }
 }
 
-// Level 3, ROWS_CLUSTER: publish one float2 per row, wait for the cn peers of
-// this row block, gather all cn partials (in peer order) into out[bm][c].
-// Arrival: each peer adds kArriveUnit / cn to its group's counter; the group
-// is complete when the counter reaches the next multiple of kArriveUnit.
-template <class S, int CNMAX>
-__device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int stage, int slot, int c,
-                                                 int m0, const float2 (&val)[S::BM],
-                                                 float2 (&out)[S::BM][CNMAX], int tid,
-                                                 int lane, int wm, int wn) {
+// Level 3, ROWS_CLUSTER: publish one float2 per row for this peer, then wait
+// until all cn peers of the row block have published.  Arrival: each peer
+// adds kArriveUnit / cn to its group's counter; the group is complete when the
+// counter reaches the next multiple of kArriveUnit.  Partials are then read
+// back peer by peer with cluster_read (in the same order in every peer).
+//
+// Ordering without L2 writeback/invalidate: every datum that crosses
+// workgroups (partials and counter) is accessed only with device-coherent
+// atomic loads/stores/RMWs (relaxed, agent scope; on gfx950 these bypass the
+// non-coherent caches).  A writer waits until its partial stores have
+// completed (vmcnt 0) before the barrier that precedes its counter increment;
+// a reader issues its partial loads only after observing the completed
+// counter.  So a reader can only see the counter value after the stores it
+// depends on have completed at the coherence point.  Agent-scope release /
+// acquire fences are avoided on purpose: on gfx950 they write back and
+// invalidate the whole L2, evicting the operands of every workgroup sharing it.
+template <class S>
+__device__ __forceinline__ void cluster_publish_wait(const GemmRowsParams& p, int stage, int slot, int c,
+                                                     int m0, const float2 (&val)[S::BM], int tid,
+                                                     int lane, int wm, int wn) {
   const int M = p.M, cn = p.cn;
   unsigned long long* part = reinterpret_cast<unsigned long long*>(p.ws_part) + (int64_t)stage * M * cn;
   const int lr = lane & 31;
-  if (wn == 0) {
-    if (lane < 32) {
+  if (wn == 0 && lane < 32) {
 #pragma unroll
-      for (int bm = 0; bm < S::BM; ++bm) {
-        const int m = m0 + wm * S::WTM + bm * 32 + lr;
-        if (m < M)
-          __hip_atomic_store(part + (int64_t)m * cn + c, __builtin_bit_cast(unsigned long long, val[bm]),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
+    for (int bm = 0; bm < S::BM; ++bm) {
+      const int m = m0 + wm * S::WTM + bm * 32 + lr;
+      if (m < M)
+        __hip_atomic_store(part + (int64_t)m * cn + c, __builtin_bit_cast(unsigned long long, val[bm]),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    __threadfence();
   }
+  wait_vmcnt<0>();            // this wave's partial stores have completed
   __syncthreads();
   if (tid == 0) {
     unsigned long long* ctr = p.ws_arrive + slot;
-    const unsigned long long old =
-        __hip_atomic_fetch_add(ctr, kArriveUnit / (unsigned long long)cn, __ATOMIC_RELEASE,
-                               __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned long long old = __hip_atomic_fetch_add(ctr, kArriveUnit / (unsigned long long)cn,
+                                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const unsigned long long target = (old / kArriveUnit + 1ull) * kArriveUnit;
     int spins = 0;
     while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
@@ -251,24 +411,70 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
         __hip_atomic_store(p.ws_err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
       }
-      __builtin_amdgcn_s_sleep(4);
+      __builtin_amdgcn_s_sleep(2);
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
   __syncthreads();
+}
+
+__device__ __forceinline__ float2 cluster_read(const GemmRowsParams& p, int stage, int m, int cc) {
+  const unsigned long long* part =
+      reinterpret_cast<const unsigned long long*>(p.ws_part) + (int64_t)stage * p.M * p.cn;
+  const int mm = m < p.M ? m : p.M - 1;
+  return __builtin_bit_cast(float2, __hip_atomic_load(part + (int64_t)mm * p.cn + cc, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT));
+}
+
+// ---------------------------------------------------------------------------
+// Output tile store through LDS.  The accumulator layout gives each lane 4
+// consecutive columns of 32 different rows, which as direct global stores
+// leaves 16-byte pieces in many cache lines (and roughly doubles HBM write
+// traffic for bf16).  Instead the tile is written to LDS in row-major order
+// (row pitch padded by 8 or 16 bytes so the 32 rows of one write hit
+// different banks), then stored as coalesced 16-byte chunks, consecutive
+// lanes covering consecutive bytes of a row.  Columns >= N and rows >= M are
+// not stored.  Needs TM * (TN * esz + pad) bytes of LDS; callers reach it
+// after the main loop's final barrier.
+// ---------------------------------------------------------------------------
+template <class S>
+__device__ __forceinline__ void store_tile_staged(const f32x16_t (&x)[S::BM][S::BN], void* Ybase, int64_t ldy,
+                                                  int y_f32, int M, int N, int m0, int n0, char* smem,
+                                                  int tid, int lane, int wm, int wn) {
+  const int lr = lane & 31, lg = lane >> 5;
+  const int esz = y_f32 ? 4 : 2;
+  const int pitch = S::TN * esz + (y_f32 ? 16 : 8);
 #pragma unroll
   for (int bm = 0; bm < S::BM; ++bm) {
-    const int m = m0 + wm * S::WTM + bm * 32 + lr;
-    const int mm = m < M ? m : M - 1;
+    const int r = wm * S::WTM + bm * 32 + lr;
 #pragma unroll
-    for (int cc = 0; cc < CNMAX; ++cc) {
-      if (cc < cn) {
-        const unsigned long long u = __hip_atomic_load(part + (int64_t)mm * cn + cc, __ATOMIC_RELAXED,
-                                                       __HIP_MEMORY_SCOPE_AGENT);
-        out[bm][cc] = __builtin_bit_cast(float2, u);
+    for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int cidx = wn * S::WTN + bn * 32 + 8 * g + 4 * lg;
+        char* dst = smem + r * pitch + cidx * esz;
+        if (y_f32) {
+          f32x4_t o = {x[bm][bn][4 * g], x[bm][bn][4 * g + 1], x[bm][bn][4 * g + 2], x[bm][bn][4 * g + 3]};
+          *reinterpret_cast<f32x4_t*>(dst) = o;
+        } else {
+          u32x2_t o = {pack_bf16x2(x[bm][bn][4 * g], x[bm][bn][4 * g + 1]),
+                       pack_bf16x2(x[bm][bn][4 * g + 2], x[bm][bn][4 * g + 3])};
+          *reinterpret_cast<u32x2_t*>(dst) = o;
+        }
       }
+  }
+  __syncthreads();
+  const int cpr = S::TN * esz / 16;            // 16-byte chunks per tile row
+  const int epc = 16 / esz;                    // elements per chunk
+  char* Y = reinterpret_cast<char*>(Ybase);
+  for (int id = tid; id < S::TM * cpr; id += S::NT) {
+    const int r = id / cpr, cc = id % cpr;
+    const int m = m0 + r, n = n0 + cc * epc;
+    if (m < M && n < N) {
+      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(smem + r * pitch + cc * 16);
+      *reinterpret_cast<u32x4_t*>(Y + ((int64_t)m * ldy + n) * esz) = v;
     }
   }
+  __syncthreads();   // the staging area is reused by the next reduction
 }
 
 // ---------------------------------------------------------------------------
@@ -279,7 +485,6 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
                                          int m0, int n0, int slot, int c, int bz, char* smem,
                                          int tid, int lane, int wm, int wn) {
   using T = typename S::T;
-  constexpr int CNMAX = 16;
   const RowEpi& e = p.epi;
   const int M = p.M, N = p.N;
   const int lr = lane & 31, lg = lane >> 5;
@@ -335,6 +540,18 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
           }
         }
     }
+  }
+
+  if (n0 + S::TN > N) {   // clamped or zero-filled columns past N contribute nothing
+#pragma unroll
+    for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        if (ncol(bn, g) >= N)
+#pragma unroll
+          for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) x[bm][bn][4 * g + q] = 0.0f;
   }
 
   bool exchanged = false;
@@ -399,31 +616,25 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
 
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
       float2 val[S::BM];
-      float2 all[S::BM][CNMAX];
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) val[bm] = make_float2(mean[bm], m2[bm]);
-      cluster_exchange<S, CNMAX>(p, 0, slot, c, m0, val, all, tid, lane, wm, wn);
+      cluster_publish_wait<S>(p, 0, slot, c, m0, val, tid, lane, wm, wn);
       exchanged = true;
-      // Equal-count merge (every peer holds S::TN columns):
-      //   mean = avg(mean_c);  M2 = sum(M2_c) + TN * sum((mean_c - mean)^2)
-      const float inv_cn = 1.0f / (float)p.cn;
+      // Pairwise merge (Chan, Golub, LeVeque) of the peers' (TN, mean, M2),
+      // peer 0 first, identical in every peer.
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) {
-        float t = 0.0f;
-#pragma unroll
-        for (int cc = 0; cc < CNMAX; ++cc)
-          if (cc < p.cn) t += all[bm][cc].x;
-        const float mu = t * inv_cn;
-        float a = 0.0f, b = 0.0f;
-#pragma unroll
-        for (int cc = 0; cc < CNMAX; ++cc)
-          if (cc < p.cn) {
-            a += all[bm][cc].y;
-            const float d = all[bm][cc].x - mu;
-            b += d * d;
-          }
+        float n_acc = 0.0f, mu = 0.0f, sq = 0.0f;
+        for (int cc = 0; cc < p.cn; ++cc) {
+          const float2 pb = cluster_read(p, 0, mrow[bm], cc);
+          const float nb = (float)S::TN, nn = n_acc + nb;
+          const float d = pb.x - mu;
+          mu += d * (nb / nn);
+          sq += pb.y + d * d * (n_acc * nb / nn);
+          n_acc = nn;
+        }
         mean[bm] = mu;
-        m2[bm] = a + (float)S::TN * b;
+        m2[bm] = sq;
       }
     }
 
@@ -463,17 +674,14 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
     wg_row_reduce<S, false>(s, red, lane, wm, wn);
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
       float2 val[S::BM];
-      float2 all[S::BM][CNMAX];
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) val[bm] = make_float2(s[bm], 0.0f);
-      cluster_exchange<S, CNMAX>(p, 0, slot, c, m0, val, all, tid, lane, wm, wn);
+      cluster_publish_wait<S>(p, 0, slot, c, m0, val, tid, lane, wm, wn);
       exchanged = true;
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) {
         float t = 0.0f;
-#pragma unroll
-        for (int cc = 0; cc < CNMAX; ++cc)
-          if (cc < p.cn) t += all[bm][cc].x;
+        for (int cc = 0; cc < p.cn; ++cc) t += cluster_read(p, 0, mrow[bm], cc).x;
         s[bm] = t;
       }
     }
@@ -505,20 +713,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
   }
   if (e.Y) {
     char* Yb = reinterpret_cast<char*>(e.Y) + (int64_t)bz * e.sy * (e.y_f32 ? 4 : 2);
-#pragma unroll
-    for (int bm = 0; bm < S::BM; ++bm) {
-      if (!mval[bm]) continue;
-#pragma unroll
-      for (int bn = 0; bn < S::BN; ++bn)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int n = ncol(bn, g);
-          if (n < N) {
-            float v[4] = {x[bm][bn][4 * g], x[bm][bn][4 * g + 1], x[bm][bn][4 * g + 2], x[bm][bn][4 * g + 3]};
-            store4(Yb, (int64_t)mrow[bm] * e.ldy + n, e.y_f32, v);
-          }
-        }
-    }
+    store_tile_staged<S>(x, Yb, e.ldy, e.y_f32, M, N, m0, n0, smem, tid, lane, wm, wn);
   }
 
   // ---- stage 4: row amax -> scale -> E4M3 codes
@@ -536,17 +731,15 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
     wg_row_reduce<S, true>(a, red, lane, wm, wn);
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
       float2 val[S::BM];
-      float2 all[S::BM][CNMAX];
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) val[bm] = make_float2(a[bm], 0.0f);
-      cluster_exchange<S, CNMAX>(p, exchanged ? 1 : 0, slot, c, m0, val, all, tid, lane, wm, wn);
+      const int stage = exchanged ? 1 : 0;
+      cluster_publish_wait<S>(p, stage, slot, c, m0, val, tid, lane, wm, wn);
       exchanged = true;
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) {
         float t = 0.0f;
-#pragma unroll
-        for (int cc = 0; cc < CNMAX; ++cc)
-          if (cc < p.cn) t = fmaxf(t, all[bm][cc].x);
+        for (int cc = 0; cc < p.cn; ++cc) t = fmaxf(t, cluster_read(p, stage, mrow[bm], cc).x);
         a[bm] = t;
       }
     }
@@ -576,10 +769,47 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
   }
 }
 
+// ---------------------------------------------------------------------------
+// Plain epilogue: C = alpha * acc + bias, stored (bf16 or fp32).
+// ---------------------------------------------------------------------------
 template <class S>
-__global__ __launch_bounds__(S::NT, 1) void gemm_rows_kernel(GemmRowsParams p) {
+__device__ __forceinline__ void epilogue_plain(f32x16_t (&x)[S::BM][S::BN], const GemmRowsParams& p,
+                                               int m0, int n0, int bz, char* smem, int tid, int lane,
+                                               int wm, int wn) {
+  const RowEpi& e = p.epi;
+  const int lg = lane >> 5;
+#pragma unroll
+  for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+    for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) x[bm][bn][i] *= e.alpha;
+  if (e.bias) {   // only a given bias is added (x + 0 would turn -0 into +0)
+#pragma unroll
+    for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = n0 + wn * S::WTN + bn * 32 + 8 * g + 4 * lg;
+        if (n >= p.N) continue;
+        const f32x4_t b = *reinterpret_cast<const f32x4_t*>(e.bias + n);
+#pragma unroll
+        for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) x[bm][bn][4 * g + q] += b[q];
+      }
+  }
+  char* Yb = reinterpret_cast<char*>(e.Y) + (int64_t)bz * e.sy * (e.y_f32 ? 4 : 2);
+  store_tile_staged<S>(x, Yb, e.ldy, e.y_f32, p.M, p.N, m0, n0, smem, tid, lane, wm, wn);
+}
+
+// LOOP: 0 = register-staged main loop (any layout, ragged K),
+//       1 = direct-to-LDS pipeline (W stored N x K, K a multiple of the stage).
+// EPI:  0 = plain epilogue (alpha, bias, store), 1 = row-subgraph epilogue.
+template <class S, int LOOP, int EPI>
+__global__ __launch_bounds__(S::NT, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_rows_kernel(GemmRowsParams p) {
   using T = typename S::T;
-  __shared__ __attribute__((aligned(16))) char smem[S::LDS];
+  __shared__ __attribute__((aligned(16))) char smem[LOOP ? S::SMEM_V2 : S::SMEM_V1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / S::WN, wn = wave % S::WN;
   const int bz = blockIdx.y;
@@ -594,84 +824,12 @@ __global__ __launch_bounds__(S::NT, 1) void gemm_rows_kernel(GemmRowsParams p) {
     if (rb >= p.num_rb) break;
     const int m0 = rb * S::TM, n0 = c * S::TN;
     f32x16_t acc[S::BM][S::BN];
-    mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn);
-    epilogue<S>(acc, p, m0, n0, q * 8 + xcd, c, bz, smem, tid, lane, wm, wn);
+    if constexpr (LOOP == 1) mainloop_v2<S>(acc, X, W, p, m0, n0, smem, lane, wave, wm, wn);
+    else mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn);
+    if constexpr (EPI == 1) epilogue<S>(acc, p, m0, n0, q * 8 + xcd, c, bz, smem, tid, lane, wm, wn);
+    else epilogue_plain<S>(acc, p, m0, n0, bz, smem, tid, lane, wm, wn);
     __syncthreads();
   }
-}
-
-// ---------------------------------------------------------------------------
-// Configurations.  Whole-row tiles (TM = 32, TN up to 768 for bf16) keep the
-// full row in one workgroup; 128-row tiles serve the cluster and split paths
-// and the plain GEMM.
-// ---------------------------------------------------------------------------
-#define CF_TILE_LIST(X)                                       \
-  X(0, bf16_t, 1, 1, 1, 4, 64)  /* TM 32,  TN 128 */          \
-  X(1, bf16_t, 1, 2, 1, 4, 64)  /* TM 32,  TN 256 */          \
-  X(2, bf16_t, 1, 3, 1, 4, 64)  /* TM 32,  TN 384 */          \
-  X(3, bf16_t, 1, 4, 1, 4, 64)  /* TM 32,  TN 512 */          \
-  X(4, bf16_t, 1, 6, 1, 4, 64)  /* TM 32,  TN 768 */          \
-  X(5, bf16_t, 2, 2, 2, 2, 128) /* TM 128, TN 128 */          \
-  X(6, bf16_t, 2, 3, 2, 2, 128) /* TM 128, TN 192 */          \
-  X(7, bf16_t, 2, 4, 2, 2, 128) /* TM 128, TN 256 */          \
-  X(8, float, 1, 1, 1, 4, 64)   /* TM 32,  TN 128 */          \
-  X(9, float, 1, 2, 1, 4, 64)   /* TM 32,  TN 256 */          \
-  X(10, float, 1, 3, 1, 4, 64)  /* TM 32,  TN 384 */          \
-  X(11, float, 1, 4, 1, 4, 64)  /* TM 32,  TN 512 */          \
-  X(12, float, 1, 6, 1, 4, 64)  /* TM 32,  TN 768 */          \
-  X(13, float, 2, 2, 2, 2, 128) /* TM 128, TN 128 */          \
-  X(14, float, 2, 4, 2, 2, 128) /* TM 128, TN 256 */
-
-#define CF_TILE_SHAPE(id, T, BM, BN, WM, WN, TKB) TileShape<T, BM, BN, WM, WN, TKB>
-
-static const TileCfg kTiles[] = {
-#define X(id, T, BM, BN, WM, WN, TKB) \
-  {id, CF_TILE_SHAPE(id, T, BM, BN, WM, WN, TKB)::TM, CF_TILE_SHAPE(id, T, BM, BN, WM, WN, TKB)::TN, \
-   sizeof(T) == 4, CF_TILE_SHAPE(id, T, BM, BN, WM, WN, TKB)::NT},
-    CF_TILE_LIST(X)
-#undef X
-};
-
-int tile_cfg_count() { return (int)(sizeof(kTiles) / sizeof(kTiles[0])); }
-const TileCfg& tile_cfg(int i) { return kTiles[i]; }
-
-static const void* kernel_ptr(int cfg) {
-  switch (cfg) {
-#define X(id, T, BM, BN, WM, WN, TKB) \
-    case id: return reinterpret_cast<const void*>(&gemm_rows_kernel<CF_TILE_SHAPE(id, T, BM, BN, WM, WN, TKB)>);
-    CF_TILE_LIST(X)
-#undef X
-    default: return nullptr;
-  }
-}
-
-int resident_wgs(int cfg) {
-  static int cache[64] = {0};
-  if (cfg < 0 || cfg >= tile_cfg_count()) return 0;
-  if (cache[cfg]) return cache[cfg];
-  int dev = 0, cus = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel_ptr(cfg), kTiles[cfg].threads, 0) !=
-      hipSuccess)
-    return 0;
-  cache[cfg] = cus * per_cu;
-  return cache[cfg];
-}
-
-hipError_t launch_gemm_rows(const GemmRowsParams& p, int in_f32, int cfg, hipStream_t st) {
-  (void)in_f32;
-  const void* fn = kernel_ptr(cfg);
-  if (!fn) return hipErrorInvalidValue;
-  dim3 grid((unsigned)(8 * p.slots * p.cn), (unsigned)p.batch), block((unsigned)kTiles[cfg].threads);
-  switch (cfg) {
-#define X(id, T, BM, BN, WM, WN, TKB) \
-    case id: hipLaunchKernelGGL((gemm_rows_kernel<CF_TILE_SHAPE(id, T, BM, BN, WM, WN, TKB)>), grid, block, 0, st, p); break;
-    CF_TILE_LIST(X)
-#undef X
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
 }
 
 }  // namespace cf

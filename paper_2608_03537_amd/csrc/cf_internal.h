@@ -77,19 +77,20 @@ struct RowKernelParams {
 
 struct B2BParams;  // defined with the B2B kernels
 
-// Launchers (return hipSuccess or the launch error).
-hipError_t launch_gemm_rows(const GemmRowsParams& p, int in_f32, int cfg, hipStream_t st);
-hipError_t launch_row_kernel(const RowKernelParams& p, hipStream_t st);
-
-// Tile configurations known to the host planner.
-struct TileCfg {
-  int id;          // index passed to launch_gemm_rows
-  int tm, tn;      // workgroup tile
-  int in_f32;      // operand type
-  int threads;
+// Compiled GEMM kernels (instantiations of gemm_rows_kernel<S, LOOP, EPI>).
+struct GemmKernel {
+  int tm, tn, in_f32, loop, epi, threads;
+  const void* fn;
 };
-int tile_cfg_count();
-const TileCfg& tile_cfg(int i);
-int resident_wgs(int cfg);   // co-resident workgroups of this config on the device
+const GemmKernel* gemm_kernels_v2(int* n);     // direct-to-LDS pipeline
+const GemmKernel* gemm_kernels_v1(int* n);     // register-staged, any layout
+const GemmKernel* gemm_kernels_wr(int* n);     // whole-row tiles (register-staged)
+int find_gemm_kernel(int in_f32, int tm, int tn, int loop, int epi);   // -1 if none
+const GemmKernel& gemm_kernel(int idx);
+int resident_wgs(int idx);   // co-resident workgroups of this kernel on the device
+
+// Launchers (return hipSuccess or the launch error).
+hipError_t launch_gemm_rows(const GemmRowsParams& p, int idx, hipStream_t st);
+hipError_t launch_row_kernel(const RowKernelParams& p, hipStream_t st);
 
 }  // namespace cf

