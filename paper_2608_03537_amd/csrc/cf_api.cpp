@@ -109,16 +109,18 @@ int pick_tile(int64_t M, int64_t N, int in_f32, int loop, int epi, bool divides,
   return best;
 }
 
-// Chooses kernel and row path for a GEMM (+ row subgraph).  `need_rows` is
-// false when the epilogue has no row reduction (then any tiling is valid).
-cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int path, bool need_rows,
+// Chooses kernel and row path for a GEMM (+ row subgraph).  `epi` selects the
+// epilogue: 0 = plain (alpha, bias, store), 1 = row subgraph.  `need_rows` is
+// true when the subgraph has a row reduction (then rows must be completed
+// across tiles); without one any tiling is valid.
+cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int path, int epi, bool need_rows,
                     bool probe_device, Plan& pl) {
   pl = Plan();
   const int tk = in_f32 ? 32 : 64;                     // k per 128-byte stage
   const int loop = (w_nk && K % tk == 0) ? 1 : 0;
   if (!need_rows) {
-    pl.kidx = pick_tile(M, N, in_f32, loop, 0, false, 0);
-    if (pl.kidx < 0) pl.kidx = pick_tile(M, N, in_f32, 0, 0, false, 0);
+    pl.kidx = pick_tile(M, N, in_f32, loop, epi, false, 0);
+    if (pl.kidx < 0) pl.kidx = pick_tile(M, N, in_f32, 0, epi, false, 0);
     pl.mode = ROWS_LOCAL;
   } else {
     if (path == PATH_AUTO) {
@@ -345,10 +347,14 @@ cf_status rows_common(int64_t M, int64_t N, int64_t K, cf_dtype in, const void* 
   if ((s = check_matrix("X", X, M, K, ldx, in, true)) != CF_OK) return s;
   if ((s = check_matrix("W", W, 1, wl == CF_LAYOUT_NK ? K : N, ldw, in, true)) != CF_OK) return s;
   const bool need_rows = epi.norm != NORM_NONE || epi.quant;
+  // The plain epilogue only applies alpha and bias; anything else runs the
+  // row-subgraph epilogue.
+  const int epi_kind = (need_rows || epi.R || epi.act != ACT_NONE) ? 1 : 0;
   Plan pl;
   // Validation and sizing never touch the device; residency is queried only
   // right before a launch.
-  if ((s = plan_rows(M, N, K, in == CF_F32, wl == CF_LAYOUT_NK, path, need_rows, false, pl)) != CF_OK) return s;
+  if ((s = plan_rows(M, N, K, in == CF_F32, wl == CF_LAYOUT_NK, path, epi_kind, need_rows, false, pl)) != CF_OK)
+    return s;
   if (size_only) {
     *ws_out = pl.ws;
     return CF_OK;
@@ -364,7 +370,7 @@ cf_status rows_common(int64_t M, int64_t N, int64_t K, cf_dtype in, const void* 
   }
   if (M == 0) return CF_OK;
   if (pl.mode == ROWS_CLUSTER &&
-      (s = plan_rows(M, N, K, in == CF_F32, wl == CF_LAYOUT_NK, path, need_rows, true, pl)) != CF_OK)
+      (s = plan_rows(M, N, K, in == CF_F32, wl == CF_LAYOUT_NK, path, epi_kind, need_rows, true, pl)) != CF_OK)
     return s;
   GemmRowsParams p{};
   p.batch = 1;
@@ -515,7 +521,7 @@ cf_status cf_gemm(int64_t batch, int64_t M, int64_t N, int64_t K, cf_dtype in, c
     if (outputs_alias(C, {A, B, (const void*)bias})) return fail(CF_ERR_ALIAS, "C aliases an input");
     if (M == 0 || batch == 0) return CF_OK;
     Plan pl;
-    if ((s = plan_rows(M, N, K, in == CF_F32, b_layout == CF_LAYOUT_NK, PATH_AUTO, false, false, pl)) != CF_OK)
+    if ((s = plan_rows(M, N, K, in == CF_F32, b_layout == CF_LAYOUT_NK, PATH_AUTO, 0, false, false, pl)) != CF_OK)
       return s;
     GemmRowsParams p{};
     p.batch = (int)batch;

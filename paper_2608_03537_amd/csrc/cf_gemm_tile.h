@@ -27,6 +27,8 @@
 //     stages 2..4.
 #pragma once
 
+#include <type_traits>
+
 #include "cf_device.h"
 #include "cf_internal.h"
 
@@ -417,6 +419,22 @@ __device__ __forceinline__ void cluster_publish_wait(const GemmRowsParams& p, in
   __syncthreads();
 }
 
+// Reads the partials of peers c0 .. c0+kPeerBatch-1 (those < cn) of row m,
+// all loads issued before any is used.
+constexpr int kPeerBatch = 8;
+__device__ __forceinline__ void cluster_read_batch(const GemmRowsParams& p, int stage, int m, int c0,
+                                                   float2 (&out)[kPeerBatch]) {
+  const unsigned long long* part =
+      reinterpret_cast<const unsigned long long*>(p.ws_part) + (int64_t)stage * p.M * p.cn;
+  const int mm = m < p.M ? m : p.M - 1;
+#pragma unroll
+  for (int j = 0; j < kPeerBatch; ++j) {
+    const int cc = c0 + j < p.cn ? c0 + j : p.cn - 1;
+    out[j] = __builtin_bit_cast(float2, __hip_atomic_load(part + (int64_t)mm * p.cn + cc, __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_AGENT));
+  }
+}
+
 __device__ __forceinline__ float2 cluster_read(const GemmRowsParams& p, int stage, int m, int cc) {
   const unsigned long long* part =
       reinterpret_cast<const unsigned long long*>(p.ws_part) + (int64_t)stage * p.M * p.cn;
@@ -478,12 +496,54 @@ __device__ __forceinline__ void store_tile_staged(const f32x16_t (&x)[S::BM][S::
 }
 
 // ---------------------------------------------------------------------------
+// Epilogue operands fetched BEFORE the main loop: the residual tile (in the
+// accumulator layout) and the bias.  Their load latency then overlaps the
+// pipeline fill instead of stalling the epilogue (the bypass operands of the
+// Stage-Stream chain are ready when the accumulator tile is).
+// ---------------------------------------------------------------------------
+template <class S>
+struct EpiPrefetch {
+  using RVec = typename std::conditional<sizeof(typename S::T) == 2, u32x2_t, u32x4_t>::type;
+  // The residual is prefetched when its registers fit (bf16, or small fp32 tiles).
+  static constexpr bool PF_R = sizeof(typename S::T) == 2 || S::BM * S::BN <= 4;
+  RVec r[PF_R ? S::BM : 1][PF_R ? S::BN : 1][4];   // 4 consecutive residual elements per (bm, bn, g)
+  f32x4_t b[S::BN][4];                             // bias for the 4 columns of (bn, g)
+};
+
+template <class S>
+__device__ __forceinline__ void epi_prefetch(EpiPrefetch<S>& pf, const GemmRowsParams& p, int m0, int n0,
+                                             int bz, int lane, int wm, int wn) {
+  using T = typename S::T;
+  using RVec = typename EpiPrefetch<S>::RVec;
+  const RowEpi& e = p.epi;
+  const int lr = lane & 31, lg = lane >> 5;
+  const T* R = reinterpret_cast<const T*>(e.R) + (int64_t)bz * e.sr;
+#pragma unroll
+  for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int n = n0 + wn * S::WTN + bn * 32 + 8 * g + 4 * lg;
+      const bool nv = n < p.N;
+      pf.b[bn][g] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+      if (e.bias && nv) pf.b[bn][g] = *reinterpret_cast<const f32x4_t*>(e.bias + n);
+      if constexpr (EpiPrefetch<S>::PF_R) {
+#pragma unroll
+        for (int bm = 0; bm < S::BM; ++bm) {
+          const int m = m0 + wm * S::WTM + bm * 32 + lr;
+          pf.r[bm][bn][g] = RVec{};
+          if (e.R && nv && m < p.M) pf.r[bm][bn][g] = *reinterpret_cast<const RVec*>(R + (int64_t)m * e.ldr + n);
+        }
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Epilogue on the register tile.
 // ---------------------------------------------------------------------------
 template <class S>
-__device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const GemmRowsParams& p,
-                                         int m0, int n0, int slot, int c, int bz, char* smem,
-                                         int tid, int lane, int wm, int wn) {
+__device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiPrefetch<S>& pf,
+                                         const GemmRowsParams& p, int m0, int n0, int slot, int c, int bz,
+                                         char* smem, int tid, int lane, int wm, int wn) {
   using T = typename S::T;
   const RowEpi& e = p.epi;
   const int M = p.M, N = p.N;
@@ -507,22 +567,17 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
     for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
       for (int i = 0; i < 16; ++i) x[bm][bn][i] *= alpha;
-  if (e.bias) {
+  if (e.bias) {   // only given terms are added (x + 0 would turn -0 into +0)
 #pragma unroll
     for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = ncol(bn, g);
-        if (n < N) {
-          const f32x4_t b = *reinterpret_cast<const f32x4_t*>(e.bias + n);
+      for (int g = 0; g < 4; ++g)
 #pragma unroll
-          for (int bm = 0; bm < S::BM; ++bm)
+        for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) x[bm][bn][4 * g + q] += b[q];
-        }
-      }
+          for (int q = 0; q < 4; ++q) x[bm][bn][4 * g + q] += pf.b[bn][g][q];
   }
-  if (e.R) {
+  if (e.R && !EpiPrefetch<S>::PF_R) {
     const T* R = reinterpret_cast<const T*>(e.R) + (int64_t)bz * e.sr;
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm) {
@@ -540,6 +595,25 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
           }
         }
     }
+  }
+  if constexpr (EpiPrefetch<S>::PF_R) if (e.R) {
+#pragma unroll
+    for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+      for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          if constexpr (sizeof(T) == 2) {
+            const u32x2_t u = pf.r[bm][bn][g];
+            x[bm][bn][4 * g + 0] += bf16_to_f32(u[0] & 0xFFFFu);
+            x[bm][bn][4 * g + 1] += bf16_to_f32(u[0] >> 16);
+            x[bm][bn][4 * g + 2] += bf16_to_f32(u[1] & 0xFFFFu);
+            x[bm][bn][4 * g + 3] += bf16_to_f32(u[1] >> 16);
+          } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) x[bm][bn][4 * g + q] += __uint_as_float(pf.r[bm][bn][g][q]);
+          }
+        }
   }
 
   if (n0 + S::TN > N) {   // clamped or zero-filled columns past N contribute nothing
@@ -625,13 +699,18 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) {
         float n_acc = 0.0f, mu = 0.0f, sq = 0.0f;
-        for (int cc = 0; cc < p.cn; ++cc) {
-          const float2 pb = cluster_read(p, 0, mrow[bm], cc);
-          const float nb = (float)S::TN, nn = n_acc + nb;
-          const float d = pb.x - mu;
-          mu += d * (nb / nn);
-          sq += pb.y + d * d * (n_acc * nb / nn);
-          n_acc = nn;
+        for (int c0 = 0; c0 < p.cn; c0 += kPeerBatch) {
+          float2 pb[kPeerBatch];
+          cluster_read_batch(p, 0, mrow[bm], c0, pb);   // loads in flight together
+#pragma unroll
+          for (int j = 0; j < kPeerBatch; ++j) {
+            if (c0 + j >= p.cn) break;
+            const float nb = (float)S::TN, nn = n_acc + nb;
+            const float d = pb[j].x - mu;
+            mu += d * (nb / nn);
+            sq += pb[j].y + d * d * (n_acc * nb / nn);
+            n_acc = nn;
+          }
         }
         mean[bm] = mu;
         m2[bm] = sq;
@@ -681,7 +760,13 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) {
         float t = 0.0f;
-        for (int cc = 0; cc < p.cn; ++cc) t += cluster_read(p, 0, mrow[bm], cc).x;
+        for (int c0 = 0; c0 < p.cn; c0 += kPeerBatch) {
+          float2 pb[kPeerBatch];
+          cluster_read_batch(p, 0, mrow[bm], c0, pb);
+#pragma unroll
+          for (int j = 0; j < kPeerBatch; ++j)
+            if (c0 + j < p.cn) t += pb[j].x;
+        }
         s[bm] = t;
       }
     }
@@ -739,7 +824,13 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const Gemm
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) {
         float t = 0.0f;
-        for (int cc = 0; cc < p.cn; ++cc) t = fmaxf(t, cluster_read(p, stage, mrow[bm], cc).x);
+        for (int c0 = 0; c0 < p.cn; c0 += kPeerBatch) {
+          float2 pb[kPeerBatch];
+          cluster_read_batch(p, stage, mrow[bm], c0, pb);
+#pragma unroll
+          for (int j = 0; j < kPeerBatch; ++j)
+            if (c0 + j < p.cn) t = fmaxf(t, pb[j].x);
+        }
         a[bm] = t;
       }
     }
@@ -824,9 +915,11 @@ void gemm_rows_kernel(GemmRowsParams p) {
     if (rb >= p.num_rb) break;
     const int m0 = rb * S::TM, n0 = c * S::TN;
     f32x16_t acc[S::BM][S::BN];
+    EpiPrefetch<S> pf;
+    if constexpr (EPI == 1) epi_prefetch<S>(pf, p, m0, n0, bz, lane, wm, wn);
     if constexpr (LOOP == 1) mainloop_v2<S>(acc, X, W, p, m0, n0, smem, lane, wave, wm, wn);
     else mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn);
-    if constexpr (EPI == 1) epilogue<S>(acc, p, m0, n0, q * 8 + xcd, c, bz, smem, tid, lane, wm, wn);
+    if constexpr (EPI == 1) epilogue<S>(acc, pf, p, m0, n0, q * 8 + xcd, c, bz, smem, tid, lane, wm, wn);
     else epilogue_plain<S>(acc, p, m0, n0, bz, smem, tid, lane, wm, wn);
     __syncthreads();
   }

@@ -157,3 +157,25 @@ def test_rowop_matches_fused_chain():
     assert_close_bf16(host(Z), z, "unfused chain")
     np.testing.assert_allclose(s.cpu().numpy(), sr, rtol=1e-3)
     check_codes(Q.cpu().numpy(), q, min_equal=0.999)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("act", ["none", "gelu", "relu"])
+def test_subgraph_without_reduction(act, dtype):
+    # Residual / activation without a row reduction: any tiling, row epilogue.
+    inp = I.postnorm_inputs(150, 64, 320, dtype, seed=16, with_affine=False, bias_std=0.3)
+    X, W = dev(inp.X, dtype), dev(I.lay_out_weight(inp.W, "nk"), dtype)
+    b, R = dev(inp.bias, "f32"), dev(inp.R, dtype)
+    Y = torch.empty((inp.M, inp.N), dtype=torch.float32, device="cuda")
+    spec = [dict(kind=cf.CF_N_SCALE, f0=0.5), dict(kind=cf.CF_N_BIAS, v0=b),
+            dict(kind=cf.CF_N_RESIDUAL, **{"in": R}, ld=inp.N, dtype=cf._dt(R))]
+    if act == "gelu":
+        spec.append(dict(kind=cf.CF_N_GELU))
+    if act == "relu":
+        spec.append(dict(kind=cf.CF_N_RELU))
+    spec.append(dict(kind=cf.CF_N_STORE, out=Y, ld=inp.N, dtype=cf.CF_F32))
+    cf.gemm_subgraph(X, W, spec)
+    torch.cuda.synchronize()
+    x = O.bias_residual(O.matmul(inp.X, inp.W), inp.bias, inp.R, alpha=0.5)
+    ref = {"none": x, "gelu": O.gelu_erf(x), "relu": O.relu(x)}[act]
+    assert_close_f32(host(Y), ref, f"no-reduction {act} {dtype}")
