@@ -186,11 +186,15 @@ cf_status cf_gemm_subgraph(const cf_subgraph_args* a, void* workspace,
  *   out = CF_OUT_STORE     : Y = O (+ b2 if given)
  *   out = CF_OUT_BIAS_RESIDUAL_LN : Y = LN(O + b2 + R) * gamma + beta
  *
- * FFN: batch = 1, K = N2 = d.  Attention: batch = B*H, M = Lq, K = d,
- * N1 = Lk, N2 = d, W1 = keys stored Lk x d (CF_LAYOUT_NK, i.e. Q.K^T),
- * W2 = values stored Lk x d (CF_LAYOUT_KN).  dtype: CF_BF16.
- * Shape rules: K % 32 == 0, N2 % 32 == 0; FFN: N1 % 32 == 0, N1 <= 1024,
- * N2 <= 512; attention: K == N2 in {64, 128}, N1 >= 1.
+ * FFN: W1 is given as W1^T (N1 x K, CF_LAYOUT_NK), W2 as W2^T (N2 x N1,
+ * CF_LAYOUT_NK); K % 64 == 0; (N1, N2) in {(512, 256), (256, 256),
+ * (256, 128), (128, 64)}; b1 [N1] fp32 or NULL; R (M x N2) or NULL; the
+ * FFN block Y = LN(GELU(X W1 + b1) W2 + b2 + X) passes R = X, N2 = K.
+ * Attention: batch = B*H, M = Lq, K = N2 = d in {64, 128}, N1 = Lk >= 1,
+ * W1 = keys stored Lk x d (CF_LAYOUT_NK, i.e. Q.K^T), W2 = values stored
+ * Lk x d (CF_LAYOUT_KN); out = CF_OUT_STORE, b1 = b2 = R = NULL.
+ * All matrices bf16 (dtype = CF_BF16), 16-byte aligned, leading dimensions
+ * and batch strides multiples of 8 elements.  Output O is M x N2 bf16.
  * Workspace: none (cf_b2bgemm_workspace returns 0).
  * ------------------------------------------------------------------------ */
 typedef enum { CF_MID_GELU_BIAS = 0, CF_MID_SOFTMAX = 1 } cf_mid_op;

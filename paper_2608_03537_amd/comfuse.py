@@ -318,3 +318,54 @@ def rowop(P, spec, stream=None):
     nodes = make_nodes(spec)
     M, N = P.shape
     _check(cf_rowop(M, N, _dt(P), _ptr(P), _ld(P), nodes, len(nodes), _stream(stream)))
+
+
+def _b2b_args(**kw):
+    a = B2BArgs()
+    a.struct_size = C.sizeof(B2BArgs)
+    for k, v in kw.items():
+        setattr(a, k, v)
+    return a
+
+
+def b2b_ffn(X, W1t, b1, W2t, b2=None, R=None, gamma=None, beta=None, *, eps=1e-5, layernorm=True, out=None,
+            stream=None):
+    """Fused FFN block O = LN(GELU(X W1 + b1) W2 + b2 + R) * gamma + beta.
+
+    X [M, K] bf16; W1t = W1^T [N1, K]; W2t = W2^T [N2, N1]; R [M, N2] (pass X
+    for the residual FFN block).  With layernorm=False, O = S W2 (+ b2 + R).
+    """
+    torch = _torch()
+    M, K = X.shape
+    N1, N2 = W1t.shape[0], W2t.shape[0]
+    O = out if out is not None else torch.empty((M, N2), dtype=torch.bfloat16, device=X.device)
+    a = _b2b_args(batch=1, M=M, K=K, N1=N1, N2=N2, dtype=CF_BF16,
+                  X=_ptr(X), ldx=_ld(X), sx=0, W1=_ptr(W1t), ldw1=_ld(W1t), sw1=0, w1_layout=CF_LAYOUT_NK,
+                  b1=_ptr(b1), mid=CF_MID_GELU_BIAS, mid_scale=1.0,
+                  W2=_ptr(W2t), ldw2=_ld(W2t), sw2=0, w2_layout=CF_LAYOUT_NK,
+                  out=CF_OUT_BIAS_RESIDUAL_LN if layernorm else CF_OUT_STORE, b2=_ptr(b2),
+                  R=_ptr(R), ldr=(_ld(R) if R is not None else 0), sr=0,
+                  gamma=_ptr(gamma), beta=_ptr(beta), eps=eps, O=_ptr(O), ldo=_ld(O), so=0)
+    _check(cf_b2bgemm(a, None, 0, _stream(stream)))
+    return O
+
+
+def b2b_attention(Q, K, V, scale=None, out=None, stream=None):
+    """O = softmax(scale * Q K^T) V for Q [B, H, Lq, d], K, V [B, H, Lk, d] (bf16, contiguous)."""
+    torch = _torch()
+    B, H, Lq, d = Q.shape
+    Lk = K.shape[2]
+    if scale is None:
+        scale = d ** -0.5
+    for t in (Q, K, V):
+        if not t.is_contiguous():
+            raise ValueError("attention operands must be contiguous [B, H, L, d]")
+    O = out if out is not None else torch.empty((B, H, Lq, d), dtype=torch.bfloat16, device=Q.device)
+    a = _b2b_args(batch=B * H, M=Lq, K=d, N1=Lk, N2=d, dtype=CF_BF16,
+                  X=_ptr(Q), ldx=d, sx=Lq * d, W1=_ptr(K), ldw1=d, sw1=Lk * d, w1_layout=CF_LAYOUT_NK,
+                  b1=None, mid=CF_MID_SOFTMAX, mid_scale=scale,
+                  W2=_ptr(V), ldw2=d, sw2=Lk * d, w2_layout=CF_LAYOUT_KN,
+                  out=CF_OUT_STORE, b2=None, R=None, ldr=0, sr=0, gamma=None, beta=None, eps=0.0,
+                  O=_ptr(O), ldo=d, so=Lq * d)
+    _check(cf_b2bgemm(a, None, 0, _stream(stream)))
+    return O

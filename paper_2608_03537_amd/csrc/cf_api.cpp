@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -575,6 +576,90 @@ cf_status cf_rowop(int64_t M, int64_t N, cf_dtype in, const void* P, int64_t ldp
 size_t cf_b2bgemm_workspace(const cf_b2b_args* a) {
   (void)a;
   return 0;
+}
+
+cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, void* hip_stream) {
+  (void)workspace;
+  (void)ws_bytes;
+  try {
+    if (!a) return fail(CF_ERR_NULL, "args is NULL");
+    if (a->struct_size != sizeof(cf_b2b_args))
+      return fail(CF_ERR_STRUCT, "struct_size %zu != %zu", a->struct_size, sizeof(cf_b2b_args));
+    if (a->dtype != CF_BF16) return fail(CF_ERR_DTYPE, "cf_b2bgemm computes in bf16 only");
+    if (a->batch < 0 || a->batch > 65535 || a->M < 0 || a->K <= 0 || a->N1 <= 0 || a->N2 <= 0)
+      return fail(CF_ERR_SHAPE, "need 0 <= batch <= 65535, M >= 0, K, N1, N2 > 0");
+    if (a->M > (int64_t)1 << 30 || a->N1 > (int64_t)1 << 30) return fail(CF_ERR_SHAPE, "size exceeds 2^30");
+    const bool ffn = a->mid == CF_MID_GELU_BIAS;
+    if (!ffn && a->mid != CF_MID_SOFTMAX) return fail(CF_ERR_UNSUPPORTED, "unknown mid op");
+    if (a->out != CF_OUT_STORE && a->out != CF_OUT_BIAS_RESIDUAL_LN) return fail(CF_ERR_UNSUPPORTED, "unknown out op");
+    cf_status s;
+    if (ffn) {
+      if (a->w1_layout != CF_LAYOUT_NK || a->w2_layout != CF_LAYOUT_NK)
+        return fail(CF_ERR_UNSUPPORTED, "FFN weights must be stored N x K (W1^T: N1 x K, W2^T: N2 x N1)");
+      if (a->K % 64 != 0) return fail(CF_ERR_SHAPE, "FFN needs K %% 64 == 0 (K = %lld)", (long long)a->K);
+      if (!b2b_ffn_supported((int)a->N1, (int)a->N2))
+        return fail(CF_ERR_UNSUPPORTED, "FFN (N1, N2) = (%lld, %lld) not compiled", (long long)a->N1,
+                    (long long)a->N2);
+      if ((s = check_vec("b1", a->b1)) != CF_OK) return s;
+    } else {
+      if (a->w1_layout != CF_LAYOUT_NK || a->w2_layout != CF_LAYOUT_KN)
+        return fail(CF_ERR_UNSUPPORTED, "attention: keys stored Lk x d (NK), values Lk x d (KN)");
+      if (a->K != a->N2 || !b2b_attention_supported((int)a->K))
+        return fail(CF_ERR_UNSUPPORTED, "attention head dim %lld not compiled (64, 128)", (long long)a->K);
+      if (a->out != CF_OUT_STORE || a->b2 || a->R || a->b1)
+        return fail(CF_ERR_UNSUPPORTED, "attention supports the plain store of O only");
+      if (!std::isfinite(a->mid_scale)) return fail(CF_ERR_SHAPE, "mid_scale must be finite");
+    }
+    const bool empty = a->M == 0 || a->batch == 0;
+    const int64_t w1_rows = ffn ? a->N1 : a->N1, w1_cols = a->K;
+    const int64_t w2_rows = ffn ? a->N2 : a->N1, w2_cols = ffn ? a->N1 : a->N2;
+    if ((s = check_matrix("X", a->X, empty ? 0 : a->M, a->K, a->ldx, CF_BF16, true)) != CF_OK) return s;
+    if ((s = check_matrix("W1", a->W1, empty ? 0 : w1_rows, w1_cols, a->ldw1, CF_BF16, true)) != CF_OK) return s;
+    if ((s = check_matrix("W2", a->W2, empty ? 0 : w2_rows, w2_cols, a->ldw2, CF_BF16, true)) != CF_OK) return s;
+    if ((s = check_matrix("O", a->O, empty ? 0 : a->M, a->N2, a->ldo, CF_BF16, true)) != CF_OK) return s;
+    if ((s = check_matrix("R", a->R, empty ? 0 : a->M, a->N2, a->ldr, CF_BF16, false)) != CF_OK) return s;
+    if ((s = check_vec("b2", a->b2)) != CF_OK || (s = check_vec("gamma", a->gamma)) != CF_OK ||
+        (s = check_vec("beta", a->beta)) != CF_OK)
+      return s;
+    if (a->batch > 1)
+      for (int64_t st : {a->sx, a->sw1, a->sw2, a->so, a->R ? a->sr : (int64_t)0})
+        if (st < 0 || st % 8 != 0) return fail(CF_ERR_ALIGN, "batch strides must be non-negative multiples of 8");
+    if (outputs_alias(a->O, {a->X, a->W1, a->W2, a->R})) return fail(CF_ERR_ALIAS, "O aliases an input");
+    if (!(a->eps >= 0.0f)) return fail(CF_ERR_SHAPE, "eps must be >= 0");
+    if (empty) return CF_OK;
+    B2BParams p{};
+    p.batch = (int)a->batch;
+    p.M = (int)a->M;
+    p.K = (int)a->K;
+    p.N1 = (int)a->N1;
+    p.N2 = (int)a->N2;
+    p.X = reinterpret_cast<const uint16_t*>(a->X);
+    p.ldx = a->ldx;
+    p.sx = a->sx;
+    p.W1 = reinterpret_cast<const uint16_t*>(a->W1);
+    p.ldw1 = a->ldw1;
+    p.sw1 = a->sw1;
+    p.b1 = a->b1;
+    p.mid_scale = a->mid_scale;
+    p.W2 = reinterpret_cast<const uint16_t*>(a->W2);
+    p.ldw2 = a->ldw2;
+    p.sw2 = a->sw2;
+    p.out_ln = a->out == CF_OUT_BIAS_RESIDUAL_LN;
+    p.b2 = a->b2;
+    p.R = reinterpret_cast<const uint16_t*>(a->R);
+    p.ldr = a->ldr;
+    p.sr = a->sr;
+    p.gamma = a->gamma;
+    p.beta = a->beta;
+    p.eps = a->eps;
+    p.O = reinterpret_cast<uint16_t*>(a->O);
+    p.ldo = a->ldo;
+    p.so = a->so;
+    hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+    return hip_status(ffn ? launch_b2b_ffn(p, st) : launch_b2b_attention(p, st), "B2B launch");
+  } catch (...) {
+    return fail(CF_ERR_HIP, "internal error");
+  }
 }
 
 }  // extern "C"

@@ -75,7 +75,6 @@ struct RowKernelParams {
   RowEpi epi;
 };
 
-struct B2BParams;  // defined with the B2B kernels
 
 // Compiled GEMM kernels (instantiations of gemm_rows_kernel<S, LOOP, EPI>).
 struct GemmKernel {
@@ -89,8 +88,29 @@ int find_gemm_kernel(int in_f32, int tm, int tn, int loop, int epi);   // -1 if 
 const GemmKernel& gemm_kernel(int idx);
 int resident_wgs(int idx);   // co-resident workgroups of this kernel on the device
 
+// Back-to-back GEMM (Sec. IV, Eq. 2).  All matrices bf16; weights stored as
+// the transposed operand (rows = output features, contiguous along the
+// contraction).  Batched over blockIdx.y with element strides.
+struct B2BParams {
+  int batch, M, K, N1, N2;
+  const uint16_t* X; int64_t ldx, sx;     // M x K
+  const uint16_t* W1; int64_t ldw1, sw1;  // N1 x K (FFN W1^T; attention keys Lk x d)
+  const float* b1;                         // [N1] (FFN) or NULL
+  float mid_scale;                         // attention: scale of Q.K^T
+  const uint16_t* W2; int64_t ldw2, sw2;  // FFN: N2 x N1 (W2^T); attention: values Lk x d
+  int out_ln;                              // 1: Y = LN(O + b2 + R) * gamma + beta
+  const float* b2;                         // [N2] or NULL
+  const uint16_t* R; int64_t ldr, sr;     // residual M x N2 or NULL
+  const float* gamma; const float* beta; float eps;
+  uint16_t* O; int64_t ldo, so;           // M x N2 output (bf16)
+};
+
 // Launchers (return hipSuccess or the launch error).
 hipError_t launch_gemm_rows(const GemmRowsParams& p, int idx, hipStream_t st);
 hipError_t launch_row_kernel(const RowKernelParams& p, hipStream_t st);
+hipError_t launch_b2b_ffn(const B2BParams& p, hipStream_t st);        // -> hipErrorInvalidValue if N1/N2 not compiled
+hipError_t launch_b2b_attention(const B2BParams& p, hipStream_t st);  // -> hipErrorInvalidValue if d not compiled
+bool b2b_ffn_supported(int N1, int N2);
+bool b2b_attention_supported(int d);
 
 }  // namespace cf

@@ -1,0 +1,100 @@
+"""GPU parity of cf_b2bgemm (back-to-back GEMM with the intermediate in
+registers) against the fp64 oracle.
+
+FFN:  Y = LN(GELU(X W1 + b1) W2 + b2 + X), bf16, max-abs 2e-2 and rel-RMS
+5e-3 (the on-chip intermediate S is rounded to bf16 as the second product's
+operand; the oracle keeps it exact).  Full size M=65536, d=256, N1=512 is
+compared over every element.
+Attention: O = softmax(Q K^T / sqrt(d)) V per head, online softmax; rel-RMS
+5e-3 is the binding check (|O| is small, so max-abs 2e-2 is loose), plus the
+invariants V = 1 -> O = 1 and Q = 0 -> O = mean_j V_j.
+"""
+import numpy as np
+import pytest
+
+from oracle import comfuse_oracle as O
+from paper_2608_03537_amd import inputs as I
+from tests.helpers import assert_close_bf16, dev, host, max_abs, rel_rms
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2608_03537_amd import comfuse as cf  # noqa: E402
+
+
+def run_ffn(inp, layernorm=True, residual=True):
+    X = dev(inp.X)
+    W1t = dev(I.lay_out_weight(inp.W1, "nk"))
+    W2t = dev(I.lay_out_weight(inp.W2, "nk"))
+    Y = cf.b2b_ffn(X, W1t, dev(inp.b1, "f32"), W2t, dev(inp.b2, "f32"), X if residual else None,
+                   eps=inp.eps, layernorm=layernorm)
+    torch.cuda.synchronize()
+    return host(Y)
+
+
+@pytest.mark.parametrize("M,d,N1", [(300, 64, 128), (129, 128, 256), (257, 256, 256), (200, 256, 512)])
+def test_ffn_small(M, d, N1):
+    inp = I.ffn_inputs(seed=2, M=M, d=d, N1=N1)
+    ref = O.ffn_b2b(inp.X, inp.W1, inp.b1, inp.W2, inp.b2, eps=inp.eps)
+    assert_close_bf16(run_ffn(inp), ref, f"FFN {M}x{d}x{N1}")
+
+
+def test_ffn_without_layernorm():
+    inp = I.ffn_inputs(seed=3, M=160, d=128, N1=256)
+    got = run_ffn(inp, layernorm=False, residual=False)
+    S = O.gelu_erf(O.bias_residual(O.matmul(inp.X, inp.W1), inp.b1))
+    ref = O.bias_residual(O.matmul(S, inp.W2), inp.b2)
+    assert rel_rms(got, ref) < 5e-3 and max_abs(got, ref) < 2e-2
+
+
+def test_ffn_zero_second_weight_is_layernorm_of_input():
+    inp = I.ffn_inputs(seed=4, M=256, d=256, N1=512)
+    inp.W2[:] = 0.0
+    inp.b2[:] = 0.0
+    got = run_ffn(inp)
+    assert_close_bf16(got, O.layernorm(inp.X), "W2 = 0")
+
+
+def test_ffn_full_size():
+    inp = I.ffn_inputs()
+    ref = O.ffn_b2b(inp.X, inp.W1, inp.b1, inp.W2, inp.b2, eps=inp.eps)
+    assert_close_bf16(run_ffn(inp), ref, "FFN 65536x256x512")
+
+
+def run_attn(Q, K, V, scale=None):
+    o = cf.b2b_attention(dev(Q), dev(K), dev(V), scale)
+    torch.cuda.synchronize()
+    return host(o)
+
+
+@pytest.mark.parametrize("B,H,Lq,Lk,d", [(1, 2, 200, 300, 64), (2, 1, 129, 64, 128), (1, 3, 64, 1, 128),
+                                         (1, 1, 256, 333, 128)])
+def test_attention_small(B, H, Lq, Lk, d):
+    a = I.attention_inputs(seed=5, B=B, H=H, Lq=Lq, Lk=Lk, d=d)
+    got = run_attn(a.Q, a.K, a.V)
+    ref = O.attention(a.Q, a.K, a.V)
+    assert rel_rms(got, ref) < 5e-3, rel_rms(got, ref)
+    assert max_abs(got, ref) < 2e-2
+
+
+def test_attention_invariants():
+    a = I.attention_inputs(seed=6, B=1, H=2, Lq=128, Lk=200, d=128)
+    ones = run_attn(a.Q, a.K, np.ones_like(a.V))
+    assert np.max(np.abs(ones - 1.0)) < 8e-3
+    zq = run_attn(np.zeros_like(a.Q), a.K, a.V)
+    mean_v = a.V.astype(np.float64).mean(axis=2, keepdims=True)
+    assert max_abs(zq, np.broadcast_to(mean_v, zq.shape)) < 4e-3
+
+
+def test_attention_full_size_sampled_rows():
+    a = I.attention_inputs()
+    got = run_attn(a.Q, a.K, a.V)
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, a.Lq - 1],
+                                     np.random.default_rng(0).choice(a.Lq, 27, replace=False)]))
+    ref = O.attention(a.Q[:, :, rows], a.K, a.V)
+    g = got[:, :, rows]
+    assert rel_rms(g, ref) < 5e-3, rel_rms(g, ref)
+    assert max_abs(g, ref) < 2e-2
