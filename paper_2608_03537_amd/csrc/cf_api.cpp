@@ -95,12 +95,14 @@ void size_workspace(Plan& pl, int64_t M, int64_t N) {
 // Picks the 128-row tile width: the one whose workgroups, laid out in waves
 // of one workgroup per CU, give the least work per CU (rounds x width).
 // `divides` restricts to widths that split N exactly into <= max_cn peers.
-int pick_tile(int64_t M, int64_t N, int in_f32, int loop, int epi, bool divides, int max_cn) {
+int pick_tile(int64_t M, int64_t N, int64_t K, int in_f32, int loop, int epi, bool divides, int max_cn) {
   int best = -1;
   double best_cost = 1e300;
   for (int tn : {256, 192, 128}) {
     const int idx = find_gemm_kernel(in_f32, 128, tn, loop, epi);
     if (idx < 0) continue;
+    // the direct-to-LDS ring is filled with stages-1 stages before the first MFMA
+    if (loop == 1 && K / (in_f32 ? 32 : 64) < gemm_kernel(idx).stages - 1) continue;
     const int64_t cn = (N + tn - 1) / tn;
     if (divides && (N % tn != 0 || cn > max_cn)) continue;
     const int64_t wgs = ((M + 127) / 128) * cn;
@@ -120,16 +122,16 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
   const int tk = in_f32 ? 32 : 64;                     // k per 128-byte stage
   const int loop = (w_nk && K % tk == 0) ? 1 : 0;
   if (!need_rows) {
-    pl.kidx = pick_tile(M, N, in_f32, loop, epi, false, 0);
-    if (pl.kidx < 0) pl.kidx = pick_tile(M, N, in_f32, 0, epi, false, 0);
+    pl.kidx = pick_tile(M, N, K, in_f32, loop, epi, false, 0);
+    if (pl.kidx < 0) pl.kidx = pick_tile(M, N, K, in_f32, 0, epi, false, 0);
     pl.mode = ROWS_LOCAL;
   } else {
     if (path == PATH_AUTO) {
       // Row clusters when N splits into <= kClusterMaxPeers tiles and the
       // peers fit on the device; else whole rows for narrow N; else split-N.
       path = PATH_SPLIT;
-      if (pick_tile(M, N, in_f32, loop, 1, true, kClusterMaxPeers) >= 0 ||
-          pick_tile(M, N, in_f32, 0, 1, true, kClusterMaxPeers) >= 0)
+      if (pick_tile(M, N, K, in_f32, loop, 1, true, kClusterMaxPeers) >= 0 ||
+          pick_tile(M, N, K, in_f32, 0, 1, true, kClusterMaxPeers) >= 0)
         path = PATH_CLUSTER;
       else if (N <= kWholeRowMaxN)
         path = PATH_WHOLE_ROW;
@@ -141,15 +143,15 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
         if (tn >= N) { pl.kidx = find_gemm_kernel(in_f32, 32, tn, 0, 1); break; }
       pl.mode = ROWS_LOCAL;
     } else if (path == PATH_CLUSTER) {
-      pl.kidx = pick_tile(M, N, in_f32, loop, 1, true, kClusterMaxPeers);
-      if (pl.kidx < 0) pl.kidx = pick_tile(M, N, in_f32, 0, 1, true, kClusterMaxPeers);
+      pl.kidx = pick_tile(M, N, K, in_f32, loop, 1, true, kClusterMaxPeers);
+      if (pl.kidx < 0) pl.kidx = pick_tile(M, N, K, in_f32, 0, 1, true, kClusterMaxPeers);
       if (pl.kidx < 0)
         return fail(CF_ERR_UNSUPPORTED, "cluster path: no tile width divides N = %lld into <= %d peers",
                     (long long)N, kClusterMaxPeers);
       pl.mode = ROWS_CLUSTER;
     } else if (path == PATH_SPLIT) {
-      pl.kidx = pick_tile(M, N, in_f32, loop, 1, false, 0);
-      if (pl.kidx < 0) pl.kidx = pick_tile(M, N, in_f32, 0, 1, false, 0);
+      pl.kidx = pick_tile(M, N, K, in_f32, loop, 1, false, 0);
+      if (pl.kidx < 0) pl.kidx = pick_tile(M, N, K, in_f32, 0, 1, false, 0);
       pl.mode = ROWS_SPLIT;
     } else {
       return fail(CF_ERR_UNSUPPORTED, "unknown path %d", path);

@@ -3,23 +3,20 @@
 
 namespace cf {
 
+using S0 = TileShape<bf16_t, 2, 2, 2, 2, 128, 0>;
+using S1 = TileShape<bf16_t, 2, 4, 2, 2, 128, 0>;
+using S2 = TileShape<float, 2, 2, 2, 2, 128, 0>;
+using S3 = TileShape<float, 2, 4, 2, 2, 128, 0>;
+
 static const GemmKernel kTable[] = {
-    {TileShape<bf16_t, 2, 2, 2, 2, 128, 0>::TM, TileShape<bf16_t, 2, 2, 2, 2, 128, 0>::TN, 0, 0, 0, TileShape<bf16_t, 2, 2, 2, 2, 128, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 2, 2, 2, 128, 0>, 0, 0>)},
-    {TileShape<bf16_t, 2, 2, 2, 2, 128, 0>::TM, TileShape<bf16_t, 2, 2, 2, 2, 128, 0>::TN, 0, 0, 1, TileShape<bf16_t, 2, 2, 2, 2, 128, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 2, 2, 2, 128, 0>, 0, 1>)},
-    {TileShape<bf16_t, 2, 4, 2, 2, 128, 0>::TM, TileShape<bf16_t, 2, 4, 2, 2, 128, 0>::TN, 0, 0, 0, TileShape<bf16_t, 2, 4, 2, 2, 128, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 4, 2, 2, 128, 0>, 0, 0>)},
-    {TileShape<bf16_t, 2, 4, 2, 2, 128, 0>::TM, TileShape<bf16_t, 2, 4, 2, 2, 128, 0>::TN, 0, 0, 1, TileShape<bf16_t, 2, 4, 2, 2, 128, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 4, 2, 2, 128, 0>, 0, 1>)},
-    {TileShape<float, 2, 2, 2, 2, 128, 0>::TM, TileShape<float, 2, 2, 2, 2, 128, 0>::TN, 1, 0, 0, TileShape<float, 2, 2, 2, 2, 128, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 2, 2, 2, 2, 128, 0>, 0, 0>)},
-    {TileShape<float, 2, 2, 2, 2, 128, 0>::TM, TileShape<float, 2, 2, 2, 2, 128, 0>::TN, 1, 0, 1, TileShape<float, 2, 2, 2, 2, 128, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 2, 2, 2, 2, 128, 0>, 0, 1>)},
-    {TileShape<float, 2, 4, 2, 2, 128, 0>::TM, TileShape<float, 2, 4, 2, 2, 128, 0>::TN, 1, 0, 0, TileShape<float, 2, 4, 2, 2, 128, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 2, 4, 2, 2, 128, 0>, 0, 0>)},
-    {TileShape<float, 2, 4, 2, 2, 128, 0>::TM, TileShape<float, 2, 4, 2, 2, 128, 0>::TN, 1, 0, 1, TileShape<float, 2, 4, 2, 2, 128, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 2, 4, 2, 2, 128, 0>, 0, 1>)},
+    CF_GEMM_ENTRY(S0, 0, 0),
+    CF_GEMM_ENTRY(S0, 0, 1),
+    CF_GEMM_ENTRY(S1, 0, 0),
+    CF_GEMM_ENTRY(S1, 0, 1),
+    CF_GEMM_ENTRY(S2, 0, 0),
+    CF_GEMM_ENTRY(S2, 0, 1),
+    CF_GEMM_ENTRY(S3, 0, 0),
+    CF_GEMM_ENTRY(S3, 0, 1),
 };
 
 const GemmKernel* gemm_kernels_v1(int* n) {

@@ -3,27 +3,23 @@
 
 namespace cf {
 
+using S0 = TileShape<bf16_t, 2, 2, 2, 2, 128, 4>;
+using S1 = TileShape<bf16_t, 2, 3, 2, 2, 128, 4>;
+using S2 = TileShape<bf16_t, 2, 4, 2, 2, 128, 3>;
+using S3 = TileShape<float, 2, 2, 2, 2, 128, 3>;
+using S4 = TileShape<float, 2, 4, 2, 2, 128, 3>;
+
 static const GemmKernel kTable[] = {
-    {TileShape<bf16_t, 2, 2, 2, 2, 128, 4>::TM, TileShape<bf16_t, 2, 2, 2, 2, 128, 4>::TN, 0, 1, 0, TileShape<bf16_t, 2, 2, 2, 2, 128, 4>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 2, 2, 2, 128, 4>, 1, 0>)},
-    {TileShape<bf16_t, 2, 2, 2, 2, 128, 4>::TM, TileShape<bf16_t, 2, 2, 2, 2, 128, 4>::TN, 0, 1, 1, TileShape<bf16_t, 2, 2, 2, 2, 128, 4>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 2, 2, 2, 128, 4>, 1, 1>)},
-    {TileShape<bf16_t, 2, 3, 2, 2, 128, 4>::TM, TileShape<bf16_t, 2, 3, 2, 2, 128, 4>::TN, 0, 1, 0, TileShape<bf16_t, 2, 3, 2, 2, 128, 4>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 3, 2, 2, 128, 4>, 1, 0>)},
-    {TileShape<bf16_t, 2, 3, 2, 2, 128, 4>::TM, TileShape<bf16_t, 2, 3, 2, 2, 128, 4>::TN, 0, 1, 1, TileShape<bf16_t, 2, 3, 2, 2, 128, 4>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 3, 2, 2, 128, 4>, 1, 1>)},
-    {TileShape<bf16_t, 2, 4, 2, 2, 128, 3>::TM, TileShape<bf16_t, 2, 4, 2, 2, 128, 3>::TN, 0, 1, 0, TileShape<bf16_t, 2, 4, 2, 2, 128, 3>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 4, 2, 2, 128, 3>, 1, 0>)},
-    {TileShape<bf16_t, 2, 4, 2, 2, 128, 3>::TM, TileShape<bf16_t, 2, 4, 2, 2, 128, 3>::TN, 0, 1, 1, TileShape<bf16_t, 2, 4, 2, 2, 128, 3>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 2, 4, 2, 2, 128, 3>, 1, 1>)},
-    {TileShape<float, 2, 2, 2, 2, 128, 3>::TM, TileShape<float, 2, 2, 2, 2, 128, 3>::TN, 1, 1, 0, TileShape<float, 2, 2, 2, 2, 128, 3>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 2, 2, 2, 2, 128, 3>, 1, 0>)},
-    {TileShape<float, 2, 2, 2, 2, 128, 3>::TM, TileShape<float, 2, 2, 2, 2, 128, 3>::TN, 1, 1, 1, TileShape<float, 2, 2, 2, 2, 128, 3>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 2, 2, 2, 2, 128, 3>, 1, 1>)},
-    {TileShape<float, 2, 4, 2, 2, 128, 3>::TM, TileShape<float, 2, 4, 2, 2, 128, 3>::TN, 1, 1, 0, TileShape<float, 2, 4, 2, 2, 128, 3>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 2, 4, 2, 2, 128, 3>, 1, 0>)},
-    {TileShape<float, 2, 4, 2, 2, 128, 3>::TM, TileShape<float, 2, 4, 2, 2, 128, 3>::TN, 1, 1, 1, TileShape<float, 2, 4, 2, 2, 128, 3>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 2, 4, 2, 2, 128, 3>, 1, 1>)},
+    CF_GEMM_ENTRY(S0, 1, 0),
+    CF_GEMM_ENTRY(S0, 1, 1),
+    CF_GEMM_ENTRY(S1, 1, 0),
+    CF_GEMM_ENTRY(S1, 1, 1),
+    CF_GEMM_ENTRY(S2, 1, 0),
+    CF_GEMM_ENTRY(S2, 1, 1),
+    CF_GEMM_ENTRY(S3, 1, 0),
+    CF_GEMM_ENTRY(S3, 1, 1),
+    CF_GEMM_ENTRY(S4, 1, 0),
+    CF_GEMM_ENTRY(S4, 1, 1),
 };
 
 const GemmKernel* gemm_kernels_v2(int* n) {

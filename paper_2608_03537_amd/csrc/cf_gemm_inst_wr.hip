@@ -3,27 +3,28 @@
 
 namespace cf {
 
+using S0 = TileShape<bf16_t, 1, 1, 1, 4, 64, 0>;
+using S1 = TileShape<bf16_t, 1, 2, 1, 4, 64, 0>;
+using S2 = TileShape<bf16_t, 1, 3, 1, 4, 64, 0>;
+using S3 = TileShape<bf16_t, 1, 4, 1, 4, 64, 0>;
+using S4 = TileShape<bf16_t, 1, 6, 1, 4, 64, 0>;
+using S5 = TileShape<float, 1, 1, 1, 4, 64, 0>;
+using S6 = TileShape<float, 1, 2, 1, 4, 64, 0>;
+using S7 = TileShape<float, 1, 3, 1, 4, 64, 0>;
+using S8 = TileShape<float, 1, 4, 1, 4, 64, 0>;
+using S9 = TileShape<float, 1, 6, 1, 4, 64, 0>;
+
 static const GemmKernel kTable[] = {
-    {TileShape<bf16_t, 1, 1, 1, 4, 64, 0>::TM, TileShape<bf16_t, 1, 1, 1, 4, 64, 0>::TN, 0, 0, 1, TileShape<bf16_t, 1, 1, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 1, 1, 1, 4, 64, 0>, 0, 1>)},
-    {TileShape<bf16_t, 1, 2, 1, 4, 64, 0>::TM, TileShape<bf16_t, 1, 2, 1, 4, 64, 0>::TN, 0, 0, 1, TileShape<bf16_t, 1, 2, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 1, 2, 1, 4, 64, 0>, 0, 1>)},
-    {TileShape<bf16_t, 1, 3, 1, 4, 64, 0>::TM, TileShape<bf16_t, 1, 3, 1, 4, 64, 0>::TN, 0, 0, 1, TileShape<bf16_t, 1, 3, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 1, 3, 1, 4, 64, 0>, 0, 1>)},
-    {TileShape<bf16_t, 1, 4, 1, 4, 64, 0>::TM, TileShape<bf16_t, 1, 4, 1, 4, 64, 0>::TN, 0, 0, 1, TileShape<bf16_t, 1, 4, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 1, 4, 1, 4, 64, 0>, 0, 1>)},
-    {TileShape<bf16_t, 1, 6, 1, 4, 64, 0>::TM, TileShape<bf16_t, 1, 6, 1, 4, 64, 0>::TN, 0, 0, 1, TileShape<bf16_t, 1, 6, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<bf16_t, 1, 6, 1, 4, 64, 0>, 0, 1>)},
-    {TileShape<float, 1, 1, 1, 4, 64, 0>::TM, TileShape<float, 1, 1, 1, 4, 64, 0>::TN, 1, 0, 1, TileShape<float, 1, 1, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 1, 1, 1, 4, 64, 0>, 0, 1>)},
-    {TileShape<float, 1, 2, 1, 4, 64, 0>::TM, TileShape<float, 1, 2, 1, 4, 64, 0>::TN, 1, 0, 1, TileShape<float, 1, 2, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 1, 2, 1, 4, 64, 0>, 0, 1>)},
-    {TileShape<float, 1, 3, 1, 4, 64, 0>::TM, TileShape<float, 1, 3, 1, 4, 64, 0>::TN, 1, 0, 1, TileShape<float, 1, 3, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 1, 3, 1, 4, 64, 0>, 0, 1>)},
-    {TileShape<float, 1, 4, 1, 4, 64, 0>::TM, TileShape<float, 1, 4, 1, 4, 64, 0>::TN, 1, 0, 1, TileShape<float, 1, 4, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 1, 4, 1, 4, 64, 0>, 0, 1>)},
-    {TileShape<float, 1, 6, 1, 4, 64, 0>::TM, TileShape<float, 1, 6, 1, 4, 64, 0>::TN, 1, 0, 1, TileShape<float, 1, 6, 1, 4, 64, 0>::NT,
-     reinterpret_cast<const void*>(&gemm_rows_kernel<TileShape<float, 1, 6, 1, 4, 64, 0>, 0, 1>)},
+    CF_GEMM_ENTRY(S0, 0, 1),
+    CF_GEMM_ENTRY(S1, 0, 1),
+    CF_GEMM_ENTRY(S2, 0, 1),
+    CF_GEMM_ENTRY(S3, 0, 1),
+    CF_GEMM_ENTRY(S4, 0, 1),
+    CF_GEMM_ENTRY(S5, 0, 1),
+    CF_GEMM_ENTRY(S6, 0, 1),
+    CF_GEMM_ENTRY(S7, 0, 1),
+    CF_GEMM_ENTRY(S8, 0, 1),
+    CF_GEMM_ENTRY(S9, 0, 1),
 };
 
 const GemmKernel* gemm_kernels_wr(int* n) {

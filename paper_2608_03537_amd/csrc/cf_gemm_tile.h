@@ -68,9 +68,26 @@ struct TileShape {
   static constexpr int A_PT = (A_CHUNKS + NT - 1) / NT;
   static constexpr int B_PT = (B_CHUNKS + NT - 1) / NT;
   static constexpr int LDS_STORE = TM * (TN * 4 + 16);   // staged output tile (fp32 worst case)
-  static constexpr int SMEM_V1 = LDS_V1 > LDS_STORE ? LDS_V1 : LDS_STORE;
-  static constexpr int SMEM_V2 = LDS_V2 > LDS_STORE ? LDS_V2 : LDS_STORE;
+  // Row-reduction scratch sits at the end of LDS, past the staged output tile.
+  static constexpr int RED_BYTES = WN * TM * 4, TAIL_BYTES = RED_BYTES;
+  static constexpr int SMEM_V1 = LDS_V1 > LDS_STORE + TAIL_BYTES ? LDS_V1 : LDS_STORE + TAIL_BYTES;
+  static constexpr int SMEM_V2 = LDS_V2 > LDS_STORE + TAIL_BYTES ? LDS_V2 : LDS_STORE + TAIL_BYTES;
   static_assert(SMEM_V1 <= 160 * 1024 && SMEM_V2 <= 160 * 1024, "LDS budget");
+  // Epilogue operands of the bf16 direct-to-LDS loop (residual tile and the
+  // per-column vectors) are loaded by the last main-loop iterations into the
+  // two ring slots that free up first (slots 0 and 1): residual rows [0, RA)
+  // and the four 1 KB vector regions in slot 0, rows [RA, TM) in slot 1.
+  static constexpr bool STG = STAGES >= 3 && sizeof(T) == 2;
+  static constexpr int STG_VEC = 4096;
+  static constexpr int STG_RA0 = STAGES ? (V2_STAGE - STG_VEC) / (TN * 2) / 32 * 32 : 0;
+  static constexpr int STG_RA = STG_RA0 < TM ? STG_RA0 : TM;
+  static constexpr int STG_RB = TM - STG_RA;
+  static constexpr int STG_CPR = TN * 2 / 16;                      // 16-byte chunks per residual row
+  static constexpr int STG_IA = STG_RA * STG_CPR / (64 * NW);      // wave-wide loads per wave, rows [0, RA)
+  static constexpr int STG_IB = STG_RB * STG_CPR / (64 * NW);      // rows [RA, TM)
+  static_assert(!STG || ((STG_RA * STG_CPR) % (64 * NW) == 0 && (STG_RB * STG_CPR) % (64 * NW) == 0 &&
+                         STG_RB * TN * 2 <= V2_STAGE && STG_RA > 0), "epilogue staging split");
+  static_assert(!STG || V2_PER_WAVE * (STAGES - 2) + STG_IA + 1 + STG_IB < 64, "vmcnt range (staging)");
   static_assert(TK % KSTEP == 0, "stage must hold whole MFMA steps");
 };
 
@@ -226,7 +243,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 // ---------------------------------------------------------------------------
 // Main loop v2: direct global -> LDS loads (global_load_lds_dwordx4), a ring
 // of S::STAGES stages, no register staging.  A stage holds 128 bytes of k for
-// the TN rows of W^T followed by the TM rows of X.
+// the TN rows of W^T followed by the TM rows of X.  Needs K / V2_TK >= STAGES-1
+// (the host plans the register-staged loop otherwise).
 //
 // LDS layout: within a row the eight 16-byte chunks are XOR-swizzled by
 // ((row >> 1) & 7).  gfx950 serves a 64-lane ds_read_b128 in 16-lane groups
@@ -236,21 +254,25 @@ __device__ __forceinline__ void wait_vmcnt() {
 // A wave-wide load writes 1 KB of consecutive LDS = 8 rows, lane i filling
 // row i/8 at chunk position i%8.
 //
-// Schedule of one stage: the fragments of MFMA step ks+1 are read while the
-// MFMAs of step ks issue, and the wave-wide loads of stage kt+S-1 are spread
-// between the MFMAs (sched_group_barrier), so neither LDS latency nor load
-// issue stalls the matrix pipe.  Loads past the last stage re-read the last
-// stage into a buffer that is no longer read, which keeps every iteration's
-// vmcnt bookkeeping identical.
+// Schedule of one stage (KS MFMA steps).  All fragments of a stage live in
+// registers.  Iteration kt first reads the fragments of its last step, then
+// issues the MFMAs of steps 0..KS-2 with this wave's share of the loads of
+// stage kt+S-1 spread between them.  It then waits until stage kt+1 has landed
+// (vmcnt) and all of this wave's LDS reads are done (lgkmcnt), meets the other
+// waves at a barrier, and reads the fragments of steps 0..KS-2 of stage kt+1
+// while the MFMAs of its last step run.  So LDS latency is hidden behind MFMAs
+// and the one barrier per stage also frees the ring slot that the next
+// iteration's loads overwrite (its last reader finished before the barrier).
+// The last S-1 iterations issue no loads; their waits shrink accordingly.
 //
 // Rows past M (or N) are clamped to the last valid row: they only feed output
 // rows/columns that the epilogue masks.
 // ---------------------------------------------------------------------------
-template <class S>
+template <class S, bool STG>
 __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
                                             const typename S::T* __restrict__ X,
                                             const typename S::T* __restrict__ W,
-                                            const GemmRowsParams& p, int m0, int n0,
+                                            const GemmRowsParams& p, int m0, int n0, int bz,
                                             char* smem, int lane, int wave, int wm, int wn) {
   using T = typename S::T;
 #pragma unroll
@@ -260,10 +282,14 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[bm][bn][i] = 0.0f;
 
+  constexpr int NS = S::STAGES, PW = S::V2_PER_WAVE;
   const int KT = p.K / S::V2_TK;
-  const char* src[S::V2_PER_WAVE];
+  // Ring slot of stage st: rotated so that the last stage lands in slot NS-1
+  // and the slots freed during the last iterations are 0, 1, ...
+  const int rot = (NS - KT % NS) % NS;
+  const char* src[PW];
 #pragma unroll
-  for (int j = 0; j < S::V2_PER_WAVE; ++j) {
+  for (int j = 0; j < PW; ++j) {
     const int row = (wave + j * S::NW) * 8 + (lane >> 3);
     const int c = (lane & 7) ^ ((row >> 1) & 7);
     if (row < S::TN) {
@@ -274,65 +300,136 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
       src[j] = reinterpret_cast<const char*>(X + (int64_t)m * p.ldx) + c * 16;
     }
   }
-  auto dma = [&](int j, int kt) {
-    const int ks = kt < KT ? kt : KT - 1;
-    dma16(src[j] + (int64_t)ks * S::V2_ROWB,
-          smem + (kt % S::STAGES) * S::V2_STAGE + (wave + j * S::NW) * 1024);
+  auto slot = [&](int st) { return smem + ((st + rot) % NS) * S::V2_STAGE; };
+  auto dma = [&](int j, int st) {
+    dma16(src[j] + (int64_t)st * S::V2_ROWB, slot(st) + (wave + j * S::NW) * 1024);
+  };
+  // Epilogue staging loads: residual rows (part 0: rows [0, RA) into slot 0,
+  // part 1: rows [RA, TM) into slot 1) with the 16-byte chunk of column group
+  // c of row r stored at chunk position c ^ (r & 7); and one vector region per
+  // wave (bias, gamma, beta, unused).  Absent operands load a valid dummy so
+  // every wave issues the same number of loads.
+  auto stage_dma = [&](int part, int i) {
+    if constexpr (STG) {
+      const RowEpi& e = p.epi;
+      const int q = (wave * (part ? S::STG_IB : S::STG_IA) + i) * 64 + lane;
+      const int rr = (part ? S::STG_RA : 0) + q / S::STG_CPR;
+      const int c = (q % S::STG_CPR) ^ (rr & 7);
+      const char* g = reinterpret_cast<const char*>(X);
+      if (e.R) {
+        const int m = min(m0 + rr, p.M - 1), n = min(n0 + c * 8, p.N - 8);
+        g = reinterpret_cast<const char*>(reinterpret_cast<const T*>(e.R) + (int64_t)bz * e.sr +
+                                          (int64_t)m * e.ldr + n);
+      }
+      dma16(g, smem + part * S::V2_STAGE + (wave * (part ? S::STG_IB : S::STG_IA) + i) * 1024);
+    }
+  };
+  auto vec_dma = [&]() {
+    if constexpr (STG) {
+      const RowEpi& e = p.epi;
+      const float* v = wave == 0 ? e.bias : wave == 1 ? e.gamma : wave == 2 ? e.beta : nullptr;
+      const char* g = reinterpret_cast<const char*>(X);
+      if (v) g = reinterpret_cast<const char*>(v + min(n0 + 4 * lane, p.N - 4));
+      dma16(g, smem + S::STG_RA * S::TN * 2 + wave * 1024);
+    }
   };
 
   constexpr int KS = S::V2_TK / S::KSTEP;          // MFMA steps per stage
-  constexpr int NFR = S::BN + S::BM;               // fragment reads per step
   constexpr int NMF = S::BN * S::BM;               // MFMAs per step
-  constexpr int DPS = (S::V2_PER_WAVE + KS - 1) / KS;   // loads issued per step
   const int lr = lane & 31, lg = lane >> 5, sw = (lr >> 1) & 7;
+  u32x4_t fa[KS][S::BN], fb[KS][S::BM];
+  // Fragment `idx` of MFMA step ks of stage st: idx < BN -> W^T block idx, else X block idx-BN.
+  auto frag1 = [&](int st, int ks, int idx) {
+    const int off = ((2 * ks + lg) ^ sw) << 4;
+    if (idx < S::BN)
+      fa[ks][idx] = lds_read16(slot(st) + (wn * S::WTN + idx * 32 + lr) * S::V2_ROWB + off);
+    else
+      fb[ks][idx - S::BN] = lds_read16(slot(st) + (S::TN + wm * S::WTM + (idx - S::BN) * 32 + lr) * S::V2_ROWB + off);
+  };
+  constexpr int NFR = S::BN + S::BM;               // fragments per step
 
 #pragma unroll
-  for (int s = 0; s < S::STAGES - 1; ++s)
+  for (int st = 0; st < NS - 1; ++st)
 #pragma unroll
-    for (int j = 0; j < S::V2_PER_WAVE; ++j) dma(j, s);
+    for (int j = 0; j < PW; ++j) dma(j, st);
+  wait_vmcnt<PW * (NS - 2)>();
+  lds_barrier();
+#pragma unroll
+  for (int ks = 0; ks < KS - 1; ++ks)
+#pragma unroll
+    for (int f = 0; f < NFR; ++f) frag1(0, ks, f);
 
-  for (int kt = 0; kt < KT; ++kt) {
-    // This wave's loads of stage kt have landed once at most the younger
-    // stages' loads are outstanding; the barrier then covers every wave.
-    wait_vmcnt<S::V2_PER_WAVE * (S::STAGES - 2)>();
-    lds_barrier();
-    const int buf = kt % S::STAGES;
-    const char* sA = smem + buf * S::V2_STAGE + (wn * S::WTN + lr) * S::V2_ROWB;
-    const char* sB = smem + buf * S::V2_STAGE + (S::TN + wm * S::WTM + lr) * S::V2_ROWB;
-    u32x4_t a[2][S::BN], b[2][S::BM];
-    auto frag = [&](int ks, int r) {
-      const int off = ((2 * ks + lg) ^ sw) << 4;
-#pragma unroll
-      for (int bn = 0; bn < S::BN; ++bn) a[r][bn] = lds_read16(sA + bn * 32 * S::V2_ROWB + off);
-#pragma unroll
-      for (int bm = 0; bm < S::BM; ++bm) b[r][bm] = lds_read16(sB + bm * 32 * S::V2_ROWB + off);
+  // One iteration.  J < 0: steady state (loads stage kt+NS-1).  J = 0..NS-2:
+  // the last NS-1 iterations (kt = KT-NS+1+J), which load the epilogue
+  // operands instead (J = 0: residual part 0 and vectors, J = 1: part 1).
+  // The instruction order is pinned (sched_barrier) because MFMAs, being pure
+  // register operations, would otherwise drift across the LDS barrier.
+  auto body = [&](int kt, auto j_t) {
+    constexpr int J = decltype(j_t)::value;
+    constexpr bool MORE = J < NS - 2;              // stage kt+1 exists
+    constexpr int NL = J < 0 ? PW : !STG ? 0 : J == 0 ? S::STG_IA + 1 : J == 1 ? S::STG_IB : 0;
+    // Loads this wave issued after stage kt+1's (the wait below allows them).
+    constexpr int AFTER = J < 0 ? PW * (NS - 2)
+                                : PW * (NS - 3 - J) + (!STG ? 0 : J == 0 ? S::STG_IA + 1 : S::STG_IA + 1 + S::STG_IB);
+    static_assert(NL <= (KS - 1) * NMF, "one load per MFMA slot");
+    const int nxt = kt + NS - 1;
+    auto load = [&](int l) {
+      if constexpr (J < 0) dma(l, nxt);
+      else if constexpr (J == 0) { if (l < S::STG_IA) stage_dma(0, l); else vec_dma(); }
+      else stage_dma(1, l);
     };
-    frag(0, 0);
-    const int nxt = kt + S::STAGES - 1;
+    // Steps 0..KS-2; behind each of the first MFMAs one fragment read of the
+    // last step (issued after an MFMA so that the MFMA's operands, read during
+    // the previous iteration, need no wait on these) and one load.
+    constexpr int RPF = (NFR + NMF - 1) / NMF;               // last-step reads per MFMA slot
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (ks + 1 < KS) frag(ks + 1, (ks + 1) & 1);
+    for (int ks = 0; ks < KS - 1; ++ks)
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-        for (int bn = 0; bn < S::BN; ++bn) Mma<T>::run(acc[bm][bn], a[ks & 1][bn], b[ks & 1][bm]);
+        for (int bn = 0; bn < S::BN; ++bn) {
+          Mma<T>::run(acc[bm][bn], fa[ks][bn], fb[ks][bm]);
+          __builtin_amdgcn_sched_barrier(0);
+          const int i = (ks * S::BM + bm) * S::BN + bn;
 #pragma unroll
-      for (int d = 0; d < DPS; ++d)
-        if (ks * DPS + d < S::V2_PER_WAVE) dma(ks * DPS + d, nxt);
+          for (int r = 0; r < RPF; ++r)
+            if (i * RPF + r < NFR) frag1(kt, KS - 1, i * RPF + r);
+          if (i < NL) load(i);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+    if constexpr (MORE) {
+      static_assert(AFTER >= 0 && AFTER < 64, "vmcnt range");
+      wait_vmcnt<AFTER>();
+      __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14));   // lgkmcnt(0); vmcnt, expcnt unconstrained
+      lds_barrier();
+      __builtin_amdgcn_sched_barrier(0);
     }
-    // Issue order: first step's fragment reads, then per step MFMAs
-    // interleaved one-to-one with the next step's reads and the loads.
-    __builtin_amdgcn_sched_group_barrier(0x100, NFR, 0);
+    // Last step; its MFMAs interleaved with the next stage's fragment reads.
+    constexpr int RPM = ((KS - 1) * NFR + NMF - 1) / NMF;   // reads per MFMA
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
+    for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-      for (int i = 0; i < NMF; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, Mma<T>::kInstrs, 0);
-        if (ks + 1 < KS && i < NFR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        if (i < DPS && ks * DPS + i < S::V2_PER_WAVE) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      for (int bn = 0; bn < S::BN; ++bn) {
+        Mma<T>::run(acc[bm][bn], fa[KS - 1][bn], fb[KS - 1][bm]);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (MORE) {
+          const int i = bm * S::BN + bn;
+#pragma unroll
+          for (int r = 0; r < RPM; ++r) {
+            const int fr = i * RPM + r;
+            if (fr < (KS - 1) * NFR) frag1(kt + 1, fr / NFR, fr % NFR);
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
-    }
-  }
+  };
+  int kt = 0;
+  for (; kt < KT - (NS - 1); ++kt) body(kt, std::integral_constant<int, -1>{});
+  static_assert(NS <= 5, "tail unrolled for at most 4 iterations");
+  body(kt, std::integral_constant<int, 0>{});
+  if constexpr (NS > 2) body(kt + 1, std::integral_constant<int, 1>{});
+  if constexpr (NS > 3) body(kt + 2, std::integral_constant<int, 2>{});
+  if constexpr (NS > 4) body(kt + 3, std::integral_constant<int, 3>{});
   wait_vmcnt<0>();
   __syncthreads();
 }
@@ -540,15 +637,21 @@ __device__ __forceinline__ void epi_prefetch(EpiPrefetch<S>& pf, const GemmRowsP
 // ---------------------------------------------------------------------------
 // Epilogue on the register tile.
 // ---------------------------------------------------------------------------
-template <class S>
+// STG: the residual tile and the vectors were staged in LDS by the main loop
+// (slots 0 and 1); otherwise they come from `pf` or straight from memory.
+template <class S, bool STG>
 __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiPrefetch<S>& pf,
                                          const GemmRowsParams& p, int m0, int n0, int slot, int c, int bz,
-                                         char* smem, int tid, int lane, int wm, int wn) {
+                                         char* smem, float* red, int tid, int lane, int wm, int wn) {
   using T = typename S::T;
   const RowEpi& e = p.epi;
   const int M = p.M, N = p.N;
   const int lr = lane & 31, lg = lane >> 5;
-  float* red = reinterpret_cast<float*>(smem);
+  // Staged vector v (0 bias, 1 gamma, 2 beta) at tile column cl.
+  auto vec_lds = [&](int v, int cl) {
+    return *reinterpret_cast<const f32x4_t*>(smem + S::STG_RA * S::TN * 2 + v * 1024 + cl * 4);
+  };
+  auto col_l = [&](int bn, int g) { return wn * S::WTN + bn * 32 + 8 * g + 4 * lg; };
 
   int mrow[S::BM];
   bool mval[S::BM];
@@ -575,9 +678,32 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
 #pragma unroll
         for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) x[bm][bn][4 * g + q] += pf.b[bn][g][q];
+          for (int q = 0; q < 4; ++q) {
+            if constexpr (STG) x[bm][bn][4 * g + q] += vec_lds(0, col_l(bn, g))[q];
+            else x[bm][bn][4 * g + q] += pf.b[bn][g][q];
+          }
   }
-  if (e.R && !EpiPrefetch<S>::PF_R) {
+  if constexpr (STG) if (e.R) {
+    // Residual row r, columns 4j..4j+3 of chunk group c = j / 2: chunk position
+    // c ^ (r & 7) of that row's slot line.
+#pragma unroll
+    for (int bm = 0; bm < S::BM; ++bm) {
+      const int r = wm * S::WTM + bm * 32 + lr;
+      const char* rowp = r < S::STG_RA ? smem + r * S::TN * 2 : smem + S::V2_STAGE + (r - S::STG_RA) * S::TN * 2;
+#pragma unroll
+      for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int cl = col_l(bn, g);
+          const u32x2_t u = *reinterpret_cast<const u32x2_t*>(rowp + (((cl >> 3) ^ (r & 7)) << 4) + (cl & 7) * 2);
+          x[bm][bn][4 * g + 0] += bf16_to_f32(u[0] & 0xFFFFu);
+          x[bm][bn][4 * g + 1] += bf16_to_f32(u[0] >> 16);
+          x[bm][bn][4 * g + 2] += bf16_to_f32(u[1] & 0xFFFFu);
+          x[bm][bn][4 * g + 3] += bf16_to_f32(u[1] >> 16);
+        }
+    }
+  }
+  if (!STG && e.R && !EpiPrefetch<S>::PF_R) {
     const T* R = reinterpret_cast<const T*>(e.R) + (int64_t)bz * e.sr;
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm) {
@@ -596,7 +722,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
         }
     }
   }
-  if constexpr (EpiPrefetch<S>::PF_R) if (e.R) {
+  if constexpr (!STG && EpiPrefetch<S>::PF_R) if (e.R) {
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
@@ -729,8 +855,13 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
           const int n = ncol(bn, g);
           f32x4_t ga = {1.0f, 1.0f, 1.0f, 1.0f}, be = {0.0f, 0.0f, 0.0f, 0.0f};
           if (n < N) {
-            if (e.gamma) ga = *reinterpret_cast<const f32x4_t*>(e.gamma + n);
-            if (e.beta) be = *reinterpret_cast<const f32x4_t*>(e.beta + n);
+            if constexpr (STG) {
+              if (e.gamma) ga = vec_lds(1, col_l(bn, g));
+              if (e.beta) be = vec_lds(2, col_l(bn, g));
+            } else {
+              if (e.gamma) ga = *reinterpret_cast<const f32x4_t*>(e.gamma + n);
+              if (e.beta) be = *reinterpret_cast<const f32x4_t*>(e.beta + n);
+            }
           }
 #pragma unroll
           for (int bm = 0; bm < S::BM; ++bm)
@@ -779,7 +910,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
       for (int g = 0; g < 4; ++g) {
         const int n = ncol(bn, g);
         f32x4_t ga = {1.0f, 1.0f, 1.0f, 1.0f};
-        if (n < N && e.gamma) ga = *reinterpret_cast<const f32x4_t*>(e.gamma + n);
+        if (n < N && e.gamma) ga = STG ? vec_lds(1, col_l(bn, g)) : *reinterpret_cast<const f32x4_t*>(e.gamma + n);
 #pragma unroll
         for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
@@ -798,6 +929,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
   }
   if (e.Y) {
     char* Yb = reinterpret_cast<char*>(e.Y) + (int64_t)bz * e.sy * (e.y_f32 ? 4 : 2);
+    if constexpr (STG) __syncthreads();   // staged vectors are no longer read
     store_tile_staged<S>(x, Yb, e.ldy, e.y_f32, M, N, m0, n0, smem, tid, lane, wm, wn);
   }
 
@@ -900,7 +1032,10 @@ template <class S, int LOOP, int EPI>
 __global__ __launch_bounds__(S::NT, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_rows_kernel(GemmRowsParams p) {
   using T = typename S::T;
-  __shared__ __attribute__((aligned(16))) char smem[LOOP ? S::SMEM_V2 : S::SMEM_V1];
+  constexpr int SMEM = LOOP ? S::SMEM_V2 : S::SMEM_V1;
+  constexpr bool STG = LOOP == 1 && EPI == 1 && S::STG;   // epilogue operands staged by the main loop
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  float* red = reinterpret_cast<float*>(smem + SMEM - S::TAIL_BYTES);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / S::WN, wn = wave % S::WN;
   const int bz = blockIdx.y;
@@ -916,13 +1051,20 @@ void gemm_rows_kernel(GemmRowsParams p) {
     const int m0 = rb * S::TM, n0 = c * S::TN;
     f32x16_t acc[S::BM][S::BN];
     EpiPrefetch<S> pf;
-    if constexpr (EPI == 1) epi_prefetch<S>(pf, p, m0, n0, bz, lane, wm, wn);
-    if constexpr (LOOP == 1) mainloop_v2<S>(acc, X, W, p, m0, n0, smem, lane, wave, wm, wn);
+    if constexpr (EPI == 1 && !STG) epi_prefetch<S>(pf, p, m0, n0, bz, lane, wm, wn);
+    if constexpr (LOOP == 1) mainloop_v2<S, STG>(acc, X, W, p, m0, n0, bz, smem, lane, wave, wm, wn);
     else mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn);
-    if constexpr (EPI == 1) epilogue<S>(acc, pf, p, m0, n0, q * 8 + xcd, c, bz, smem, tid, lane, wm, wn);
+    if constexpr (EPI == 1) epilogue<S, STG>(acc, pf, p, m0, n0, q * 8 + xcd, c, bz, smem, red, tid, lane, wm, wn);
     else epilogue_plain<S>(acc, p, m0, n0, bz, smem, tid, lane, wm, wn);
     __syncthreads();
   }
 }
+
+// Registry entry of one instantiation: <tile shape S, main loop, epilogue>.
+#define CF_GEMM_ENTRY(S, LOOP, EPI)                                                                  \
+  GemmKernel {                                                                                       \
+    S::TM, S::TN, std::is_same<typename S::T, float>::value ? 1 : 0, LOOP, EPI, S::NT, S::STAGES,    \
+        reinterpret_cast<const void*>(&gemm_rows_kernel<S, LOOP, EPI>)                               \
+  }
 
 }  // namespace cf

@@ -79,6 +79,7 @@ struct RowKernelParams {
 // Compiled GEMM kernels (instantiations of gemm_rows_kernel<S, LOOP, EPI>).
 struct GemmKernel {
   int tm, tn, in_f32, loop, epi, threads;
+  int stages;   // direct-to-LDS ring depth (needs K / k_per_stage >= stages - 1); 0 for other loops
   const void* fn;
 };
 const GemmKernel* gemm_kernels_v2(int* n);     // direct-to-LDS pipeline
