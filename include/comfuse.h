@@ -187,9 +187,10 @@ cf_status cf_gemm_subgraph(const cf_subgraph_args* a, void* workspace,
  *   out = CF_OUT_BIAS_RESIDUAL_LN : Y = LN(O + b2 + R) * gamma + beta
  *
  * FFN: W1 is given as W1^T (N1 x K, CF_LAYOUT_NK), W2 as W2^T (N2 x N1,
- * CF_LAYOUT_NK); K % 64 == 0; (N1, N2) in {(512, 256), (256, 256),
- * (256, 128), (128, 64)}; b1 [N1] fp32 or NULL; R (M x N2) or NULL; the
- * FFN block Y = LN(GELU(X W1 + b1) W2 + b2 + X) passes R = X, N2 = K.
+ * CF_LAYOUT_NK); the model width d = K = N2 (CF_ERR_UNSUPPORTED otherwise);
+ * (N1, d) in {(512, 256), (256, 256), (256, 128), (128, 64)}; b1 [N1] fp32
+ * or NULL; R (M x d) or NULL; the FFN block Y = LN(GELU(X W1 + b1) W2 + b2
+ * + X) passes R = X.
  * Attention: batch = B*H, M = Lq, K = N2 = d in {64, 128}, N1 = Lk >= 1,
  * W1 = keys stored Lk x d (CF_LAYOUT_NK, i.e. Q.K^T), W2 = values stored
  * Lk x d (CF_LAYOUT_KN); out = CF_OUT_STORE, b1 = b2 = R = NULL.

@@ -598,7 +598,7 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, voi
     if (ffn) {
       if (a->w1_layout != CF_LAYOUT_NK || a->w2_layout != CF_LAYOUT_NK)
         return fail(CF_ERR_UNSUPPORTED, "FFN weights must be stored N x K (W1^T: N1 x K, W2^T: N2 x N1)");
-      if (a->K % 64 != 0) return fail(CF_ERR_SHAPE, "FFN needs K %% 64 == 0 (K = %lld)", (long long)a->K);
+      if (a->K != a->N2) return fail(CF_ERR_UNSUPPORTED, "FFN needs K == N2 = d (K = %lld, N2 = %lld)", (long long)a->K, (long long)a->N2);
       if (!b2b_ffn_supported((int)a->N1, (int)a->N2))
         return fail(CF_ERR_UNSUPPORTED, "FFN (N1, N2) = (%lld, %lld) not compiled", (long long)a->N1,
                     (long long)a->N2);

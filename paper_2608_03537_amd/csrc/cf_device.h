@@ -76,9 +76,24 @@ __device__ __forceinline__ uint32_t f32_to_e4m3(float f) {
   return sign | code;
 }
 
-// GELU, erf form: x * Phi(x).
+// erf by Abramowitz and Stegun, Handbook of Mathematical Functions, 7.1.26:
+// erf(x) = 1 - (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2) with
+// t = 1 / (1 + p x) for x >= 0, |error| <= 1.5e-7; odd extension.  Branch-free
+// (one reciprocal, one exp), so a wave never runs two code paths.
+__device__ __forceinline__ float erf_as(float x) {
+  const float ax = fabsf(x);
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
+  float y = fmaf(1.061405429f, t, -1.453152027f);
+  y = fmaf(y, t, 1.421413741f);
+  y = fmaf(y, t, -0.284496736f);
+  y = fmaf(y, t, 0.254829592f);
+  const float e = __builtin_amdgcn_exp2f(-(ax * ax) * 1.4426950408889634f);   // exp(-x^2)
+  return copysignf(fmaf(-(y * t), e, 1.0f), x);
+}
+
+// GELU, erf form: x * Phi(x) = x/2 (1 + erf(x / sqrt 2)).
 __device__ __forceinline__ float gelu_erf(float x) {
-  return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+  return 0.5f * x * (1.0f + erf_as(x * 0.70710678118654752f));
 }
 // GELU, tanh approximation.
 __device__ __forceinline__ float gelu_tanh(float x) {

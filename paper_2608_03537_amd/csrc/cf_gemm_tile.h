@@ -942,7 +942,10 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
 #pragma unroll
       for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) t = fmaxf(t, fabsf(x[bm][bn][i]));
+        for (int g = 0; g < 4; ++g)
+          if (ncol(bn, g) < N)   // padding columns of a ragged tile are not zero after the PostOps
+#pragma unroll
+            for (int q = 0; q < 4; ++q) t = fmaxf(t, fabsf(x[bm][bn][4 * g + q]));
       a[bm] = t;
     }
     wg_row_reduce<S, true>(a, red, lane, wm, wn);

@@ -62,6 +62,20 @@ def test_chain_small(N, path):
     check_codes(Qg, q, min_equal=0.999)
 
 
+@pytest.mark.parametrize("N", [160, 320])
+def test_chain_ragged_tile_whole_row(N):
+    # N = 160 / 320 leave 96 / 64 padding columns in the 256 / 384-wide tile;
+    # after LayerNorm they hold -mean/std, and must not enter the row amax.
+    # A residual shifted by -10 makes that about +7, above every real |z|.
+    inp = I.postnorm_inputs(70, 128, N, "bf16", seed=21, with_affine=False)
+    inp.R = I.round_to_bf16(inp.R - 10.0)
+    z, s, q = O.ln_gelu_amax(inp.X, inp.W, inp.bias, inp.R, eps=inp.eps)
+    Zg, sg, Qg = run_chain(inp, 1)
+    assert_close_bf16(Zg, z, f"Z N={N} whole-row")
+    np.testing.assert_allclose(sg, s, rtol=1e-3)
+    check_codes(Qg, q, min_equal=0.999)
+
+
 @pytest.mark.parametrize("path", [1, 2, 3])
 def test_chain_quant_exact_against_own_z(path):
     inp = I.postnorm_inputs(97, 64, 512, "f32", seed=12, with_affine=False)
