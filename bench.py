@@ -1,20 +1,31 @@
 #!/usr/bin/env python
-"""Benchmark of the fused GEMM + post-norm hot path on one MI355X.
+"""Benchmark of the fused GEMM + row-subgraph hot path on one MI355X.
 
-Workload (one step): the BERT-base post-norm Y = LayerNorm(X.W + b + R),
-M = 8192 (16 x 512 tokens), K = N = 768, bf16 operands, fp32 accumulation,
-bf16 output — one cf_gemm_postnorm call.  Operands are seeded synthetic data
-(see paper_2608_03537_amd/inputs.py).
+Headline workload (one step): the BERT-base post-norm Y = LayerNorm(X.W + b + R),
+M = 8192 (16 x 512 tokens), K = N = 768, bf16 operands, fp32 accumulation, bf16
+output -- one cf_gemm_postnorm call.  The JSON line's `value` is its TFLOP/s;
+`roofline` prices it against HBM (its bounding roof), `cpu_baseline` times the
+fp64 oracle on the host.
 
-Protocol: K steps are captured in one HIP graph and replayed once, bracketed
-by events on the stream the kernels run on; the steps rotate over `--sets`
-distinct buffer sets (16 x 39 MB > the 256 MB Infinity Cache), so operands
-come from HBM.  The unfused comparator (cf_gemm writing bf16 P, then cf_rowop
-for residual + LayerNorm) and the plain GEMM are timed the same way.
+Alongside (unless --only-main), the other four workloads, each fused vs its
+unfused in-house path (cf_gemm + cf_rowop kernels), with TFLOP/s, GB/s and the
+fraction of the bounding roofline (lower bound / time):
+  postnorm_tiny_fp32   Y = LN(X.W + b + R), fp32, 128 x 256 x 256
+  ln_gelu_amax_fp8     Z = GELU(LN(X.W + b + R)), s = rowmax|Z|/448, Q = e4m3(Z/s),
+                       bf16, 16384 x 4096 x 4096
+  ffn_b2b              Y = LN(GELU(X.W1 + b1).W2 + b2 + X), bf16, 65536 x 256 x 512
+  attention_b2b        O = softmax(Q.K^T / sqrt(128)).V, bf16, 4 x 16 heads, 2048 x 2048 x 128
+Operands are seeded synthetic data (paper_2608_03537_amd/inputs.py).
+
+Protocol: K steps are captured in one HIP graph and replayed once, bracketed by
+events on the stream the kernels run on; steps rotate over distinct buffer sets
+so that operands come from HBM (the 256 MB Infinity Cache would otherwise hold
+them).  A few output rows of every timed kernel are checked against the oracle.
 
 Prints ONE JSON line.  --gpus above 1 exits: this benchmark runs on one GPU.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -27,6 +38,24 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
+F32_PEAK_TFLOPS = 157.3        # dense fp32 MFMA
+
+# HBM traffic of the headline kernel per launch, from rocprofv3 FETCH_SIZE and
+# WRITE_SIZE runs (each scaled by a plain-copy calibration: bytes = 2.0 x
+# FETCH_SIZE KiB x 1024 and 1.0 x WRITE_SIZE KiB x 1024), valid only for the
+# kernel sources they were taken on (sha256 over csrc/, see kernel_hash()).
+TRAFFIC = {"kernel_hash": "790391a56654cc13", "bytes": 50782208}
+
+
+def kernel_hash():
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2608_03537_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if not f.endswith((".h", ".hip", ".cpp")):
+            continue
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
 
 
 def parse():
@@ -38,7 +67,8 @@ def parse():
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 whole-row, 2 cluster, 3 split-N")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--no-compare", action="store_true")
+    ap.add_argument("--no-compare", action="store_true", help="skip the unfused comparator of the headline")
+    ap.add_argument("--only-main", action="store_true", help="skip the other four workloads")
     return ap.parse_args()
 
 
@@ -81,14 +111,155 @@ def cpu_baseline(inp, seconds):
             "sample": f"full {inp.M}x{inp.K}x{inp.N} post-norm, fp64 numpy oracle, {reps} reps in {el:.1f} s"}
 
 
+def summarize(fused_ms, unfused_ms, flop, nbytes, bound, peak, parity, **extra):
+    """Per-workload record: throughput, roofline fraction (lower bound / time), speedup."""
+    sec = fused_ms * 1e-3
+    lower = flop / (peak * 1e12) if bound != "hbm" else nbytes / (HBM_PEAK_GBS * 1e9)
+    out = {"fused_us": fused_ms * 1e3, "unfused_us": unfused_ms * 1e3, "speedup_vs_unfused": unfused_ms / fused_ms,
+           "tflops": flop / sec / 1e12, "gbs": nbytes / sec / 1e9, "bound": bound,
+           "roofline_frac": lower / sec, "lower_bound_us": lower * 1e6, "parity": parity}
+    out.update(extra)
+    return out
+
+
+def tensor(torch, a, dt, dev):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dt).to(dev)
+
+
+def verdict(err, tol):
+    return "ok" if err <= tol else f"FAIL max-abs {err:.3e}"
+
+
+def workload_tiny(torch, cf, I, O, dev):
+    inp = I.postnorm_tiny_fp32()
+    M, K, N = inp.M, inp.K, inp.N
+    f = torch.float32
+    X, W, R = tensor(torch, inp.X, f, dev), tensor(torch, I.lay_out_weight(inp.W, "nk"), f, dev), tensor(torch, inp.R, f, dev)
+    b, g, be = tensor(torch, inp.bias, f, dev), tensor(torch, inp.gamma, f, dev), tensor(torch, inp.beta, f, dev)
+    Y = torch.empty((M, N), dtype=f, device=dev)
+    P = torch.empty((M, N), dtype=f, device=dev)
+    ws = cf.workspace(1 << 20, dev)
+    fused = time_steps(torch, [lambda: cf.gemm_postnorm(X, W, b, R, g, be, eps=inp.eps, out=Y, ws=ws)], 400, 20)
+    ref = O.postnorm(inp.X, inp.W, inp.bias, inp.R, inp.gamma, inp.beta, 1.0, inp.eps)
+    err = float(np.max(np.abs(Y.cpu().numpy() - ref)))
+    spec = [dict(kind=cf.CF_N_RESIDUAL, **{"in": R}, ld=N, dtype=cf.CF_F32),
+            dict(kind=cf.CF_N_LAYERNORM, v0=g, v1=be, f0=inp.eps), dict(kind=cf.CF_N_STORE, out=Y, ld=N, dtype=cf.CF_F32)]
+
+    def unf():
+        cf.gemm(X, W, bias=b, out=P)
+        cf.rowop(P, spec)
+    unfused = time_steps(torch, [unf], 400, 20)
+    flop = 2.0 * M * N * K
+    nbytes = 4 * (M * K + K * N + 2 * M * N) + 3 * 4 * N
+    return summarize(fused, unfused, flop, nbytes, "mfma_f32", F32_PEAK_TFLOPS, verdict(err, 1e-4),
+                     shape={"M": M, "K": K, "N": N, "dtype": "f32"})
+
+
+def workload_chain(torch, cf, I, O, dev):
+    inp = I.ln_gelu_amax_inputs()
+    M, K, N = inp.M, inp.K, inp.N
+    bf = torch.bfloat16
+    X, W, R = tensor(torch, inp.X, bf, dev), tensor(torch, I.lay_out_weight(inp.W, "nk"), bf, dev), tensor(torch, inp.R, bf, dev)
+    b = tensor(torch, inp.bias, torch.float32, dev)
+    Z = torch.empty((M, N), dtype=bf, device=dev)
+    s = torch.empty((M,), dtype=torch.float32, device=dev)
+    Q = torch.empty((M, N), dtype=torch.uint8, device=dev)
+    P = torch.empty((M, N), dtype=torch.float32, device=dev)
+    spec = [dict(kind=cf.CF_N_BIAS, v0=b), dict(kind=cf.CF_N_RESIDUAL, **{"in": R}, ld=N, dtype=cf.CF_BF16),
+            dict(kind=cf.CF_N_LAYERNORM, f0=inp.eps), dict(kind=cf.CF_N_GELU),
+            dict(kind=cf.CF_N_STORE, out=Z, ld=N, dtype=cf.CF_BF16),
+            dict(kind=cf.CF_N_ROWAMAX_QUANT, out=s, out2=Q, ld=N, f0=448.0)]
+    nodes = cf.make_nodes(spec)
+    a = cf.subgraph_args(X, W, nodes)
+    ws = cf.workspace(cf.cf_gemm_subgraph_workspace(a), dev)
+    fused = time_steps(torch, [lambda: cf.gemm_subgraph(X, W, spec, ws=ws)], 16, 2)
+    rows = np.array([0, 1, 4095, M - 1])
+    z, sr, _ = O.ln_gelu_amax(inp.X[rows], inp.W, inp.bias, inp.R[rows], eps=inp.eps)
+    err = float(np.max(np.abs(Z[torch.from_numpy(rows).to(dev)].float().cpu().numpy() - z)))
+    rest = spec[1:]
+
+    def unf():
+        cf.gemm(X, W, bias=b, out=P)
+        cf.rowop(P, rest)
+    unfused = time_steps(torch, [unf], 16, 2)
+    flop = 2.0 * M * N * K
+    nbytes = 2 * (M * K + K * N + M * N) + 2 * M * N + M * N + 4 * M + 4 * N
+    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2),
+                     shape={"M": M, "K": K, "N": N, "dtype": "bf16", "outputs": "Z bf16, s f32, Q e4m3"})
+
+
+def workload_ffn(torch, cf, I, O, dev):
+    inp = I.ffn_inputs()
+    M, d, N1 = inp.M, inp.d, inp.N1
+    bf = torch.bfloat16
+    W1t, W2t = tensor(torch, I.lay_out_weight(inp.W1, "nk"), bf, dev), tensor(torch, I.lay_out_weight(inp.W2, "nk"), bf, dev)
+    b1, b2 = tensor(torch, inp.b1, torch.float32, dev), tensor(torch, inp.b2, torch.float32, dev)
+    X0 = tensor(torch, inp.X, bf, dev)
+    sets = [dict(X=X0.clone(), Y=torch.empty((M, d), dtype=bf, device=dev), P=torch.empty((M, N1), dtype=bf, device=dev),
+                 S=torch.empty((M, N1), dtype=bf, device=dev), O2=torch.empty((M, d), dtype=bf, device=dev))
+            for _ in range(4)]
+    fused = time_steps(torch, [(lambda s=s: cf.b2b_ffn(s["X"], W1t, b1, W2t, b2, s["X"], eps=inp.eps, out=s["Y"]))
+                               for s in sets], 64, 8)
+    rows = np.array([0, 1, 127, M - 1])
+    ref = O.ffn_b2b(inp.X[rows], inp.W1, inp.b1, inp.W2, inp.b2, eps=inp.eps)
+    err = float(np.max(np.abs(sets[0]["Y"][torch.from_numpy(rows).to(dev)].float().cpu().numpy() - ref)))
+
+    def unf(s):
+        g1 = [dict(kind=cf.CF_N_GELU), dict(kind=cf.CF_N_STORE, out=s["S"], ld=N1, dtype=cf.CF_BF16)]
+        g2 = [dict(kind=cf.CF_N_RESIDUAL, **{"in": s["X"]}, ld=d, dtype=cf.CF_BF16),
+              dict(kind=cf.CF_N_LAYERNORM, f0=inp.eps), dict(kind=cf.CF_N_STORE, out=s["Y"], ld=d, dtype=cf.CF_BF16)]
+
+        def run():
+            cf.gemm(s["X"], W1t, bias=b1, out=s["P"])
+            cf.rowop(s["P"], g1)
+            cf.gemm(s["S"], W2t, bias=b2, out=s["O2"])
+            cf.rowop(s["O2"], g2)
+        return run
+    unfused = time_steps(torch, [unf(s) for s in sets], 64, 8)
+    flop = 2.0 * M * N1 * d * 2
+    nbytes = 2 * (2 * M * d + 2 * d * N1) + 4 * (N1 + 3 * d)
+    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2),
+                     shape={"M": M, "d": d, "N1": N1, "dtype": "bf16"})
+
+
+def workload_attention(torch, cf, I, O, dev):
+    a = I.attention_inputs()
+    B, H, L, Lk, d = a.B, a.H, a.Lq, a.Lk, a.d
+    bf = torch.bfloat16
+    sets = []
+    for _ in range(2):
+        sets.append(dict(Q=tensor(torch, a.Q, bf, dev), K=tensor(torch, a.K, bf, dev), V=tensor(torch, a.V, bf, dev),
+                         O=torch.empty((B, H, L, d), dtype=bf, device=dev)))
+    fused = time_steps(torch, [(lambda s=s: cf.b2b_attention(s["Q"], s["K"], s["V"], out=s["O"])) for s in sets], 16, 2)
+    rows = np.array([0, 777, L - 1])
+    ref = O.attention(a.Q[:, :, rows], a.K, a.V)
+    err = float(np.max(np.abs(sets[0]["O"][:, :, torch.from_numpy(rows).to(dev)].float().cpu().numpy() - ref)))
+    Sx = torch.empty((B * H, L, Lk), dtype=bf, device=dev)
+    Px = torch.empty_like(Sx)
+    sm = [dict(kind=cf.CF_N_SOFTMAX, out=Px.view(-1, Lk), ld=Lk, dtype=cf.CF_BF16, f0=d ** -0.5)]
+
+    def unf(s):
+        def run():
+            cf.gemm(s["Q"].view(B * H, L, d), s["K"].view(B * H, Lk, d), b_layout=cf.CF_LAYOUT_NK, out=Sx)
+            cf.rowop(Sx.view(-1, Lk), sm)
+            cf.gemm(Px, s["V"].view(B * H, Lk, d), b_layout=cf.CF_LAYOUT_KN, out=s["O"].view(B * H, L, d))
+        return run
+    unfused = time_steps(torch, [unf(s) for s in sets], 8, 2)
+    flop = 2.0 * B * H * L * Lk * d * 2
+    nbytes = 2 * 4 * B * H * L * d
+    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2),
+                     shape={"B": B, "H": H, "Lq": L, "Lk": Lk, "d": d, "dtype": "bf16"})
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU; multi-GPU runs are not part of this build "
-              "(the post-norm shards rows with no exchange).", file=sys.stderr)
+              "(every workload shards rows or heads with no exchange).", file=sys.stderr)
         sys.exit(2)
     import torch
 
+    from oracle import comfuse_oracle as O
     from paper_2608_03537_amd import comfuse as cf
     from paper_2608_03537_amd import inputs as I
 
@@ -97,7 +268,7 @@ def main():
     dev = torch.device("cuda:0")
 
     def t(a, dt=torch.bfloat16):
-        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dt).to(dev)
+        return tensor(torch, a, dt, dev)
 
     X0, W0, R0 = t(inp.X), t(I.lay_out_weight(inp.W, "nk")), t(inp.R)
     b, g, be = t(inp.bias, torch.float32), t(inp.gamma, torch.float32), t(inp.beta, torch.float32)
@@ -122,30 +293,27 @@ def main():
         spec = [dict(kind=cf.CF_N_RESIDUAL, **{"in": s["R"]}, ld=N, dtype=cf.CF_BF16),
                 dict(kind=cf.CF_N_LAYERNORM, v0=g, v1=be, f0=inp.eps),
                 dict(kind=cf.CF_N_STORE, out=s["Y"], ld=N, dtype=cf.CF_BF16)]
-        nodes = cf.make_nodes(spec)
 
         def run():
             cf.gemm(s["X"], s["W"], bias=b, out=s["P"])
-            cf._check(cf.cf_rowop(M, N, cf.CF_BF16, s["P"].data_ptr(), N, nodes, len(nodes),
-                                  torch.cuda.current_stream().cuda_stream))
-        run.nodes = nodes
+            cf.rowop(s["P"], spec)
         return run
 
     ms = time_steps(torch, [fused(s) for s in sets], args.steps, args.warmup)
     ms_hot = time_steps(torch, [fused(sets[0])], args.steps, args.warmup)
 
     # Parity spot check of the timed kernel's output (64 rows vs the oracle).
-    from oracle import comfuse_oracle as O
     rows = np.random.default_rng(1).choice(M, 64, replace=False)
     ref = O.postnorm(inp.X[rows], inp.W, inp.bias, inp.R[rows], inp.gamma, inp.beta, 1.0, inp.eps)
     got = sets[0]["Y"][torch.from_numpy(rows).to(dev)].float().cpu().numpy()
     err = float(np.max(np.abs(got - ref)))
-    parity = "ok" if err <= 2e-2 else f"FAIL max-abs {err:.3e}"
 
     flops = 2.0 * M * N * K
     alg_bytes = 2 * (M * K + K * N + 2 * M * N) + 3 * 4 * N
     sec = ms * 1e-3
     gbs = alg_bytes / sec / 1e9
+    khash = kernel_hash()
+    traffic = TRAFFIC["bytes"] if TRAFFIC["kernel_hash"] == khash else None
     out = {
         "metric": "fused GEMM+postnorm TFLOP/s & % bounding roofline; speedup vs unfused",
         "value": flops / sec / 1e12,
@@ -162,10 +330,11 @@ def main():
         "config": {"workload": "bert_base_postnorm_bf16", "M": M, "K": K, "N": N, "w_layout": "nk",
                    "path": args.path, "rotated_sets": args.sets},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": gbs / HBM_PEAK_GBS, "traffic": None},
-        "parity": parity,
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": traffic},
+        "parity": verdict(err, 2e-2),
         "cache_hot_ms": ms_hot,
         "mfma_frac": flops / sec / 1e12 / BF16_PEAK_TFLOPS,
+        "kernel_hash": khash,
     }
     if not args.no_compare:
         ms_gemm = time_steps(torch, [plain_gemm(s) for s in sets], args.steps, args.warmup)
@@ -174,6 +343,15 @@ def main():
         out["gemm_only_ms"] = ms_gemm
         out["speedup_vs_unfused"] = ms_unf / ms
         out["residual_time_us"] = {"fused": (ms - ms_gemm) * 1e3, "unfused": (ms_unf - ms_gemm) * 1e3}
+    del sets
+    torch.cuda.empty_cache()
+    if not args.only_main:
+        wl = {}
+        for name, fn in [("postnorm_tiny_fp32", workload_tiny), ("ln_gelu_amax_fp8", workload_chain),
+                         ("ffn_b2b", workload_ffn), ("attention_b2b", workload_attention)]:
+            wl[name] = fn(torch, cf, I, O, dev)
+            torch.cuda.empty_cache()
+        out["workloads"] = wl
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
     print(json.dumps(out))
