@@ -51,7 +51,7 @@ extern "C" {
 #endif
 
 #define CF_VERSION 1
-#define CF_WS_HEADER_BYTES 33024  /* 256 + 8 * 4096 */
+#define CF_WS_HEADER_BYTES 8392704  /* 4096 + 2 * 128 * 16 * 128 * 16 */
 
 typedef enum {
   CF_F32 = 0,       /* IEEE binary32 */
@@ -93,11 +93,12 @@ typedef enum {
  * Shape rules: N % 32 == 0, K % 16 == 0, 32 <= N <= 8192.
  * Workspace: cf_gemm_postnorm_workspace() bytes (0 on the whole-row path),
  * 16-byte aligned.  Every non-empty workspace begins with CF_WS_HEADER_BYTES
- * of library state (an error word and the arrival counters of the row-cluster
- * path): zero-fill that header once before first use and do not modify it
- * afterwards; every call leaves it valid for any later call, whatever its
- * shape or path.  A non-zero first 32-bit word means a wait for peer
- * workgroups exceeded its bound (results of that call are invalid).
+ * of library state (an error word, the round counters and the exchange
+ * records of the row-cluster path): zero-fill that header once before first
+ * use and do not modify it afterwards; every call leaves it valid for any
+ * later call, whatever its shape or path.  A non-zero first 32-bit word means
+ * a wait for peer workgroups exceeded its bound (results of that call are
+ * invalid).
  * ------------------------------------------------------------------------ */
 typedef struct {
   size_t struct_size;            /* = sizeof(cf_postnorm_args) */

@@ -67,6 +67,7 @@ enum Path { PATH_AUTO = 0, PATH_WHOLE_ROW = 1, PATH_CLUSTER = 2, PATH_SPLIT = 3 
 
 constexpr int kWholeRowMaxN = 768;
 constexpr int kClusterMaxPeers = 16;
+constexpr int kAutoClusterPeers = 8;
 
 struct Plan {
   int kidx = -1, mode = ROWS_LOCAL, cn = 1, num_rb = 0, slots = 0, tm = 0, tn = 0;
@@ -76,13 +77,14 @@ struct Plan {
 
 constexpr int kAssumedCUs = 256;   // MI355X; used only to rank tile widths
 
-// Every non-empty workspace starts with the fixed header (error word and
-// arrival counters; only the cluster path writes it).  Then the cluster path
-// keeps part[2][M][cn] float2, the split path part[M][cn] float2 and x[M][N].
+// Every non-empty workspace starts with the fixed header (error word, round
+// counters and exchange records; only the cluster path writes it), which is
+// all the cluster path needs.  The split path keeps part[M][cn] float2 and
+// x[M][N] after it.
 void size_workspace(Plan& pl, int64_t M, int64_t N) {
   if (pl.mode == ROWS_CLUSTER) {
-    pl.off_part = kWsHeaderBytes;
-    pl.ws = pl.off_part + round_up((size_t)2 * M * pl.cn * 8, 256);
+    pl.off_part = kWsCounterBytes;
+    pl.ws = kWsHeaderBytes;
   } else if (pl.mode == ROWS_SPLIT) {
     pl.off_part = kWsHeaderBytes;
     pl.off_x = pl.off_part + round_up((size_t)M * pl.cn * 8, 256);
@@ -127,14 +129,23 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
     pl.mode = ROWS_LOCAL;
   } else {
     if (path == PATH_AUTO) {
-      // Row clusters when N splits into <= kClusterMaxPeers tiles and the
-      // peers fit on the device; else whole rows for narrow N; else split-N.
+      // Row clusters when N splits into <= kAutoClusterPeers tiles; whole rows
+      // instead when N is narrow and they give more workgroups (small M);
+      // else split-N.  Every tile's exchange waits for the slowest of its
+      // peers, and with 16 peers that wait costs more than split-N's fp32
+      // round trip of x, so wide rows go to split-N unless a caller asks
+      // for the cluster path.
       path = PATH_SPLIT;
-      if (pick_tile(M, N, K, in_f32, loop, 1, true, kClusterMaxPeers) >= 0 ||
-          pick_tile(M, N, K, in_f32, 0, 1, true, kClusterMaxPeers) >= 0)
+      int ck = pick_tile(M, N, K, in_f32, loop, 1, true, kAutoClusterPeers);
+      if (ck < 0) ck = pick_tile(M, N, K, in_f32, 0, 1, true, kAutoClusterPeers);
+      if (ck >= 0) {
         path = PATH_CLUSTER;
-      else if (N <= kWholeRowMaxN)
+        const GemmKernel& t = gemm_kernel(ck);
+        const int64_t cluster_wgs = ((M + t.tm - 1) / t.tm) * ((N + t.tn - 1) / t.tn);
+        if (N <= kWholeRowMaxN && (M + 31) / 32 > cluster_wgs) path = PATH_WHOLE_ROW;
+      } else if (N <= kWholeRowMaxN) {
         path = PATH_WHOLE_ROW;
+      }
     }
     if (path == PATH_WHOLE_ROW) {
       if (N > kWholeRowMaxN)
@@ -171,6 +182,9 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
     if (slots < 1) return fail(CF_ERR_UNSUPPORTED, "cluster path: %d peers do not fit the device", pl.cn);
     pl.slots = std::min(pl.slots, std::min(slots, kMaxSlots / 8));
   }
+  if (pl.mode == ROWS_CLUSTER && (pl.tm > kRecRows || pl.cn > kRecPeers))
+    return fail(CF_ERR_UNSUPPORTED, "cluster path: tile of %d rows x %d peers exceeds the exchange records",
+                pl.tm, pl.cn);
   size_workspace(pl, M, N);
   return CF_OK;
 }
@@ -180,6 +194,7 @@ void bind_workspace(const Plan& pl, void* ws, GemmRowsParams& p) {
   if (pl.mode == ROWS_CLUSTER) {
     p.ws_err = reinterpret_cast<unsigned*>(b);
     p.ws_arrive = reinterpret_cast<unsigned long long*>(b + 256);
+    static_assert(kWsCounterBytes % 256 == 0, "records alignment");
     p.ws_part = reinterpret_cast<float*>(b + pl.off_part);
   } else if (pl.mode == ROWS_SPLIT) {
     p.ws_part = reinterpret_cast<float*>(b + pl.off_part);

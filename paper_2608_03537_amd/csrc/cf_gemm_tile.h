@@ -34,7 +34,7 @@
 
 namespace cf {
 
-constexpr int kSpinLimit = 1 << 22;   // bounded wait for peers (~1 s)
+constexpr int kSpinLimit = 1 << 20;   // bounded wait for peers (each poll is one device-scope round trip: ~1 s)
 
 template <typename TIn, int BM_, int BN_, int WM_, int WN_, int TKB_, int STAGES_ = 0>
 struct TileShape {
@@ -465,79 +465,118 @@ __device__ __forceinline__ void wg_row_reduce(float (&v)[S::BM], float* red, int
   }
 }
 
-// Level 3, ROWS_CLUSTER: publish one float2 per row for this peer, then wait
-// until all cn peers of the row block have published.  Arrival: each peer
-// adds kArriveUnit / cn to its group's counter; the group is complete when the
-// counter reaches the next multiple of kArriveUnit.  Partials are then read
-// back peer by peer with cluster_read (in the same order in every peer).
+// Level 3, ROWS_CLUSTER: the cn workgroups of a row block exchange per-row
+// partials through records in the workspace header.
 //
-// Ordering without L2 writeback/invalidate: every datum that crosses
-// workgroups (partials and counter) is accessed only with device-coherent
-// atomic loads/stores/RMWs (relaxed, agent scope; on gfx950 these bypass the
-// non-coherent caches).  A writer waits until its partial stores have
-// completed (vmcnt 0) before the barrier that precedes its counter increment;
-// a reader issues its partial loads only after observing the completed
-// counter.  So a reader can only see the counter value after the stores it
-// depends on have completed at the coherence point.  Agent-scope release /
-// acquire fences are avoided on purpose: on gfx950 they write back and
-// invalidate the whole L2, evicting the operands of every workgroup sharing it.
-template <class S>
-__device__ __forceinline__ void cluster_publish_wait(const GemmRowsParams& p, int stage, int slot, int c,
-                                                     int m0, const float2 (&val)[S::BM], int tid,
-                                                     int lane, int wm, int wn) {
-  const int M = p.M, cn = p.cn;
-  unsigned long long* part = reinterpret_cast<unsigned long long*>(p.ws_part) + (int64_t)stage * M * cn;
+// Rounds.  Every wave adds kArriveUnit / (cn * NW) to its peer group's counter
+// when it starts a tile (round_tag), so a round adds exactly kArriveUnit and
+// old / kArriveUnit numbers the round, identically in all its waves.  A wave
+// waits for that add to return before its workgroup's first epilogue barrier,
+// so all adds of a round have landed before any record of the round can be
+// seen, and the next round's adds see the next round number.
+//
+// Records.  record(stage, slot, peer, row) holds one or two 64-bit words,
+// each a 32-bit value with the round number + 1 in its upper half.  A word is
+// written and read with single 64-bit device-coherent atomics (relaxed, agent
+// scope; on gfx950 these bypass the non-coherent caches), so a reader that
+// sees the current round in a word also sees that round's value: no fence,
+// no completion wait on the writer and no separate arrival flag.  Only this
+// path writes the records and a slot's round numbers only grow, so a stale
+// or zero-filled record never carries the current tag.  Agent-scope release
+// / acquire fences are avoided on purpose: on gfx950 they write back and
+// invalidate the whole L2, evicting the operands of every workgroup sharing
+// it.
+__device__ __forceinline__ unsigned long long round_begin(const GemmRowsParams& p, int slot, int lane, int nw) {
+  unsigned long long old = 0;
+  if (lane == 0)
+    old = __hip_atomic_fetch_add(p.ws_arrive + slot, kArriveUnit / (unsigned long long)(p.cn * nw),
+                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return old;
+}
+
+// Tag of the round whose counter value `old` lane 0 of this wave received.
+__device__ __forceinline__ unsigned round_tag(unsigned long long old) {
+  const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)old);
+  const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(old >> 32));
+  return (unsigned)((((unsigned long long)hi << 32) | lo) / kArriveUnit) + 1u;
+}
+
+__device__ __forceinline__ unsigned long long rec_word(float v, unsigned tag) {
+  return ((unsigned long long)tag << 32) | __float_as_uint(v);
+}
+
+// Publishes (a, b) (MAX: a only) of this workgroup's rows, then reads every
+// peer's records of the lane's rows, peer 0 first, until all carry `tag`, and
+// merges them in that order: MAX -> a = max over peers; otherwise (a, b) =
+// (mean, M2) of tiles of TN columns, merged pairwise (Chan, Golub, LeVeque).
+// Every workgroup merges in the same order, so all get bit-identical values.
+template <class S, bool MAX>
+__device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int stage, int slot, int c, unsigned tag,
+                                                 float (&a)[S::BM], float (&b)[S::BM], int lane, int wm, int wn) {
+  static_assert(S::TM <= kRecRows, "records hold kRecRows rows per peer");
+  constexpr int NV = MAX ? 1 : 2;
+  constexpr int PB = 4;   // peers read per batch
+  unsigned long long* rec = reinterpret_cast<unsigned long long*>(p.ws_part) + stage * kRecStageWords +
+                            (size_t)slot * kRecPeers * kRecRows * 2;
   const int lr = lane & 31;
   if (wn == 0 && lane < 32) {
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm) {
-      const int m = m0 + wm * S::WTM + bm * 32 + lr;
-      if (m < M)
-        __hip_atomic_store(part + (int64_t)m * cn + c, __builtin_bit_cast(unsigned long long, val[bm]),
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      unsigned long long* w = rec + ((size_t)c * kRecRows + wm * S::WTM + bm * 32 + lr) * 2;
+      __hip_atomic_store(w, rec_word(a[bm], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (!MAX) __hip_atomic_store(w + 1, rec_word(b[bm], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
-  wait_vmcnt<0>();            // this wave's partial stores have completed
-  __syncthreads();
-  if (tid == 0) {
-    unsigned long long* ctr = p.ws_arrive + slot;
-    const unsigned long long old = __hip_atomic_fetch_add(ctr, kArriveUnit / (unsigned long long)cn,
-                                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const unsigned long long target = (old / kArriveUnit + 1ull) * kArriveUnit;
-    int spins = 0;
-    while (__hip_atomic_load(ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-      if (++spins > kSpinLimit) {
+  const int cn = p.cn;
+  float n_acc[S::BM], mu[S::BM], sq[S::BM];
+#pragma unroll
+  for (int bm = 0; bm < S::BM; ++bm) n_acc[bm] = mu[bm] = sq[bm] = 0.0f;
+  for (int c0 = 0; c0 < cn; c0 += PB) {
+    unsigned long long w[S::BM][PB][NV];
+    for (int spins = 0;; ++spins) {
+      bool ok = true;
+#pragma unroll
+      for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+        for (int j = 0; j < PB; ++j) {
+          const int cc = c0 + j < cn ? c0 + j : cn - 1;
+          const unsigned long long* r = rec + ((size_t)cc * kRecRows + wm * S::WTM + bm * 32 + lr) * 2;
+#pragma unroll
+          for (int v = 0; v < NV; ++v) {
+            w[bm][j][v] = __hip_atomic_load(r + v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            ok = ok && (unsigned)(w[bm][j][v] >> 32) == tag;
+          }
+        }
+      if (__all(ok)) break;
+      if (spins >= kSpinLimit) {
         __hip_atomic_store(p.ws_err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
       }
-      __builtin_amdgcn_s_sleep(2);
+      __builtin_amdgcn_s_sleep(1);
     }
-  }
-  __syncthreads();
-}
-
-// Reads the partials of peers c0 .. c0+kPeerBatch-1 (those < cn) of row m,
-// all loads issued before any is used.
-constexpr int kPeerBatch = 8;
-__device__ __forceinline__ void cluster_read_batch(const GemmRowsParams& p, int stage, int m, int c0,
-                                                   float2 (&out)[kPeerBatch]) {
-  const unsigned long long* part =
-      reinterpret_cast<const unsigned long long*>(p.ws_part) + (int64_t)stage * p.M * p.cn;
-  const int mm = m < p.M ? m : p.M - 1;
 #pragma unroll
-  for (int j = 0; j < kPeerBatch; ++j) {
-    const int cc = c0 + j < p.cn ? c0 + j : p.cn - 1;
-    out[j] = __builtin_bit_cast(float2, __hip_atomic_load(part + (int64_t)mm * p.cn + cc, __ATOMIC_RELAXED,
-                                                          __HIP_MEMORY_SCOPE_AGENT));
+    for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+      for (int j = 0; j < PB; ++j) {
+        if (c0 + j >= cn) break;
+        const float va = __uint_as_float((unsigned)w[bm][j][0]);
+        if constexpr (MAX) {
+          mu[bm] = fmaxf(mu[bm], va);
+        } else {
+          const float vb = __uint_as_float((unsigned)w[bm][j][NV - 1]);
+          const float nb = (float)S::TN, nn = n_acc[bm] + nb;
+          const float d = va - mu[bm];
+          mu[bm] += d * (nb / nn);
+          sq[bm] += vb + d * d * (n_acc[bm] * nb / nn);
+          n_acc[bm] = nn;
+        }
+      }
   }
-}
-
-__device__ __forceinline__ float2 cluster_read(const GemmRowsParams& p, int stage, int m, int cc) {
-  const unsigned long long* part =
-      reinterpret_cast<const unsigned long long*>(p.ws_part) + (int64_t)stage * p.M * p.cn;
-  const int mm = m < p.M ? m : p.M - 1;
-  return __builtin_bit_cast(float2, __hip_atomic_load(part + (int64_t)mm * p.cn + cc, __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT));
+#pragma unroll
+  for (int bm = 0; bm < S::BM; ++bm) {
+    a[bm] = mu[bm];
+    if (!MAX) b[bm] = sq[bm];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -589,7 +628,10 @@ __device__ __forceinline__ void store_tile_staged(const f32x16_t (&x)[S::BM][S::
       *reinterpret_cast<u32x4_t*>(Y + ((int64_t)m * ldy + n) * esz) = v;
     }
   }
-  __syncthreads();   // the staging area is reused by the next reduction
+  // The staging area is reused by the next reduction: every lane has read
+  // its chunks (the stores consumed them), so a bare barrier suffices and the
+  // global stores drain while the workgroup goes on.
+  lds_barrier();
 }
 
 // ---------------------------------------------------------------------------
@@ -641,8 +683,8 @@ __device__ __forceinline__ void epi_prefetch(EpiPrefetch<S>& pf, const GemmRowsP
 // (slots 0 and 1); otherwise they come from `pf` or straight from memory.
 template <class S, bool STG>
 __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiPrefetch<S>& pf,
-                                         const GemmRowsParams& p, int m0, int n0, int slot, int c, int bz,
-                                         char* smem, float* red, int tid, int lane, int wm, int wn) {
+                                         const GemmRowsParams& p, int m0, int n0, int slot, int c, unsigned tag,
+                                         int bz, char* smem, float* red, int tid, int lane, int wm, int wn) {
   using T = typename S::T;
   const RowEpi& e = p.epi;
   const int M = p.M, N = p.N;
@@ -664,12 +706,14 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
 
   // ---- stage 1: x = alpha * acc + bias + R (columns >= N stay exactly 0)
   const float alpha = e.alpha;
+  if (alpha != 1.0f) {
 #pragma unroll
-  for (int bm = 0; bm < S::BM; ++bm)
+    for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-    for (int bn = 0; bn < S::BN; ++bn)
+      for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) x[bm][bn][i] *= alpha;
+        for (int i = 0; i < 16; ++i) x[bm][bn][i] *= alpha;
+  }
   if (e.bias) {   // only given terms are added (x + 0 would turn -0 into +0)
 #pragma unroll
     for (int bn = 0; bn < S::BN; ++bn)
@@ -773,23 +817,30 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     const float inv_c = 1.0f / (float)cnt_c;
     float mean[S::BM], m2[S::BM];
 #pragma unroll
-    for (int bm = 0; bm < S::BM; ++bm) {
-      mean[bm] = s[bm] * inv_c;
-      float t = 0.0f;
+    for (int bm = 0; bm < S::BM; ++bm) mean[bm] = s[bm] * inv_c;
+    // sum of (x - mean)^2 over the tile's valid columns (padding columns of a
+    // ragged tile hold 0, not the mean, and are skipped)
+    auto dev2 = [&](auto ragged_t) {
+      constexpr bool RAGGED = decltype(ragged_t)::value;
 #pragma unroll
-      for (int bn = 0; bn < S::BN; ++bn)
+      for (int bm = 0; bm < S::BM; ++bm) {
+        float t = 0.0f;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          if (ncol(bn, g) < N) {
+        for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            if (RAGGED && ncol(bn, g) >= N) continue;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const float d = x[bm][bn][4 * g + q] - mean[bm];
-              t += d * d;
+              t = fmaf(d, d, t);
             }
           }
-        }
-      m2[bm] = t;
-    }
+        m2[bm] = t;
+      }
+    };
+    if (n0 + S::TN <= N) dev2(std::false_type{});
+    else dev2(std::true_type{});
     wg_row_reduce<S, false>(m2, red, lane, wm, wn);
 
     if (p.mode == ROWS_SPLIT) {
@@ -815,46 +866,30 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     }
 
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
-      float2 val[S::BM];
-#pragma unroll
-      for (int bm = 0; bm < S::BM; ++bm) val[bm] = make_float2(mean[bm], m2[bm]);
-      cluster_publish_wait<S>(p, 0, slot, c, m0, val, tid, lane, wm, wn);
+      cluster_exchange<S, false>(p, 0, slot, c, tag, mean, m2, lane, wm, wn);
       exchanged = true;
-      // Pairwise merge (Chan, Golub, LeVeque) of the peers' (TN, mean, M2),
-      // peer 0 first, identical in every peer.
-#pragma unroll
-      for (int bm = 0; bm < S::BM; ++bm) {
-        float n_acc = 0.0f, mu = 0.0f, sq = 0.0f;
-        for (int c0 = 0; c0 < p.cn; c0 += kPeerBatch) {
-          float2 pb[kPeerBatch];
-          cluster_read_batch(p, 0, mrow[bm], c0, pb);   // loads in flight together
-#pragma unroll
-          for (int j = 0; j < kPeerBatch; ++j) {
-            if (c0 + j >= p.cn) break;
-            const float nb = (float)S::TN, nn = n_acc + nb;
-            const float d = pb[j].x - mu;
-            mu += d * (nb / nn);
-            sq += pb[j].y + d * d * (n_acc * nb / nn);
-            n_acc = nn;
-          }
-        }
-        mean[bm] = mu;
-        m2[bm] = sq;
-      }
     }
 
     if (e.norm == NORM_LAYER) {
       const float invN = 1.0f / (float)N;
+      // y = (x - mean) * rstd (a constant row gives exactly 0), then
+      // y * gamma + beta when either is given.
       float rstd[S::BM];
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) rstd[bm] = rsqrtf(m2[bm] * invN + e.eps);
 #pragma unroll
-      for (int bn = 0; bn < S::BN; ++bn)
+      for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int n = ncol(bn, g);
-          f32x4_t ga = {1.0f, 1.0f, 1.0f, 1.0f}, be = {0.0f, 0.0f, 0.0f, 0.0f};
-          if (n < N) {
+        for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) x[bm][bn][i] = (x[bm][bn][i] - mean[bm]) * rstd[bm];
+      if (e.gamma || e.beta) {
+#pragma unroll
+        for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int n = min(ncol(bn, g), N - 4);   // padding columns are never stored
+            f32x4_t ga = {1.0f, 1.0f, 1.0f, 1.0f}, be = {0.0f, 0.0f, 0.0f, 0.0f};
             if constexpr (STG) {
               if (e.gamma) ga = vec_lds(1, col_l(bn, g));
               if (e.beta) be = vec_lds(2, col_l(bn, g));
@@ -862,13 +897,12 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
               if (e.gamma) ga = *reinterpret_cast<const f32x4_t*>(e.gamma + n);
               if (e.beta) be = *reinterpret_cast<const f32x4_t*>(e.beta + n);
             }
+#pragma unroll
+            for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) x[bm][bn][4 * g + q] = fmaf(x[bm][bn][4 * g + q], ga[q], be[q]);
           }
-#pragma unroll
-          for (int bm = 0; bm < S::BM; ++bm)
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-              x[bm][bn][4 * g + q] = (x[bm][bn][4 * g + q] - mean[bm]) * rstd[bm] * ga[q] + be[q];
-        }
+      }
     }
   } else if (e.norm == NORM_RMS) {
     float s[S::BM];
@@ -883,23 +917,12 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     }
     wg_row_reduce<S, false>(s, red, lane, wm, wn);
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
-      float2 val[S::BM];
+      // sum of squares: a merge of (mean, M2) pairs (0, s) keeps M2 = sum of s
+      float z[S::BM];
 #pragma unroll
-      for (int bm = 0; bm < S::BM; ++bm) val[bm] = make_float2(s[bm], 0.0f);
-      cluster_publish_wait<S>(p, 0, slot, c, m0, val, tid, lane, wm, wn);
+      for (int bm = 0; bm < S::BM; ++bm) z[bm] = 0.0f;
+      cluster_exchange<S, false>(p, 0, slot, c, tag, z, s, lane, wm, wn);
       exchanged = true;
-#pragma unroll
-      for (int bm = 0; bm < S::BM; ++bm) {
-        float t = 0.0f;
-        for (int c0 = 0; c0 < p.cn; c0 += kPeerBatch) {
-          float2 pb[kPeerBatch];
-          cluster_read_batch(p, 0, mrow[bm], c0, pb);
-#pragma unroll
-          for (int j = 0; j < kPeerBatch; ++j)
-            if (c0 + j < p.cn) t += pb[j].x;
-        }
-        s[bm] = t;
-      }
     }
     const float invN = 1.0f / (float)N;
 #pragma unroll
@@ -950,24 +973,8 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     }
     wg_row_reduce<S, true>(a, red, lane, wm, wn);
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
-      float2 val[S::BM];
-#pragma unroll
-      for (int bm = 0; bm < S::BM; ++bm) val[bm] = make_float2(a[bm], 0.0f);
-      const int stage = exchanged ? 1 : 0;
-      cluster_publish_wait<S>(p, stage, slot, c, m0, val, tid, lane, wm, wn);
+      cluster_exchange<S, true>(p, exchanged ? 1 : 0, slot, c, tag, a, a, lane, wm, wn);
       exchanged = true;
-#pragma unroll
-      for (int bm = 0; bm < S::BM; ++bm) {
-        float t = 0.0f;
-        for (int c0 = 0; c0 < p.cn; c0 += kPeerBatch) {
-          float2 pb[kPeerBatch];
-          cluster_read_batch(p, stage, mrow[bm], c0, pb);
-#pragma unroll
-          for (int j = 0; j < kPeerBatch; ++j)
-            if (c0 + j < p.cn) t = fmaxf(t, pb[j].x);
-        }
-        a[bm] = t;
-      }
     }
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm) {
@@ -1051,14 +1058,29 @@ void gemm_rows_kernel(GemmRowsParams p) {
   for (int it = 0;; ++it) {
     const int rb = (it * p.slots + q) * 8 + xcd;
     if (rb >= p.num_rb) break;
-    const int m0 = rb * S::TM, n0 = c * S::TN;
+    int m0 = rb * S::TM, n0 = c * S::TN;
+    // Opaque copies of the tile origin and lane ids for this iteration: the
+    // epilogue's addresses and column masks would otherwise be hoisted out of
+    // the tile loop and kept live (spilled) across the whole main loop.
+    int lane_t = lane, tid_t = tid;
+    asm volatile("" : "+s"(n0), "+s"(m0));
+    asm volatile("" : "+v"(lane_t), "+v"(tid_t));
     f32x16_t acc[S::BM][S::BN];
     EpiPrefetch<S> pf;
+    const bool cluster = EPI == 1 && p.mode == ROWS_CLUSTER && p.cn > 1;
+    unsigned long long round_old = 0;
+    if (cluster) round_old = round_begin(p, q * 8 + xcd, lane, S::NW);
     if constexpr (EPI == 1 && !STG) epi_prefetch<S>(pf, p, m0, n0, bz, lane, wm, wn);
     if constexpr (LOOP == 1) mainloop_v2<S, STG>(acc, X, W, p, m0, n0, bz, smem, lane, wave, wm, wn);
     else mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn);
-    if constexpr (EPI == 1) epilogue<S, STG>(acc, pf, p, m0, n0, q * 8 + xcd, c, bz, smem, red, tid, lane, wm, wn);
-    else epilogue_plain<S>(acc, p, m0, n0, bz, smem, tid, lane, wm, wn);
+    unsigned tag = 0;
+    if (cluster) {
+      tag = round_tag(round_old);
+      asm volatile("" ::"s"(tag) : "memory");   // this wave's add has returned before any epilogue barrier
+    }
+    if constexpr (EPI == 1)
+      epilogue<S, STG>(acc, pf, p, m0, n0, q * 8 + xcd, c, tag, bz, smem, red, tid_t, lane_t, wm, wn);
+    else epilogue_plain<S>(acc, p, m0, n0, bz, smem, tid_t, lane_t, wm, wn);
     __syncthreads();
   }
 }

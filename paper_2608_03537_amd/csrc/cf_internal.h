@@ -46,20 +46,30 @@ struct GemmRowsParams {
   int num_rb;          // row blocks = ceil(M / TM)
   int slots;           // row-block slots per XCD processed concurrently
   // Workspace views.  Every workspace starts with a fixed header that only
-  // the cluster path touches: an error word and one 64-bit arrival counter
-  // per concurrent peer group ("slot").  Counters only ever grow by whole
-  // multiples of kArriveUnit, so a zero-filled header stays valid across
-  // calls of any shape and path without a reset.
+  // the cluster path writes: an error word, one 64-bit round counter per
+  // concurrent peer group ("slot") and the exchange records.  Counters only
+  // ever grow by whole multiples of kArriveUnit and every record carries the
+  // round it belongs to, so a zero-filled header stays valid across calls of
+  // any shape and path without a reset.
   unsigned* ws_err;              // sticky flag: a peer wait exceeded its spin limit
-  unsigned long long* ws_arrive; // [kMaxSlots] arrival counters
-  float* ws_part;                // CLUSTER: [2][M][cn] float2; SPLIT: [M][cn] float2
+  unsigned long long* ws_arrive; // [kMaxSlots] round counters
+  float* ws_part;                // CLUSTER: records (kRecStageWords u64 per stage);
+                                 // SPLIT: [M][cn] float2
   float* ws_x;                   // SPLIT: [M][N] fp32 pre-norm x
 };
 
-// lcm(1..16): every peer of a group of cn <= 16 adds kArriveUnit / cn.
-constexpr unsigned long long kArriveUnit = 720720ull;
-constexpr int kMaxSlots = 4096;                      // concurrent peer groups
-constexpr size_t kWsHeaderBytes = 256 + 8 * kMaxSlots;   // err word, then the counters
+// Each of the NW waves of the cn workgroups of a peer group adds
+// kArriveUnit / (cn * NW) to the group's counter once per tile, so a round
+// adds exactly kArriveUnit.  lcm(1..16) * 8 is divisible by cn * NW for every
+// cn <= 16 and NW in {1, 2, 4, 8}.
+constexpr unsigned long long kArriveUnit = 720720ull * 8ull;
+constexpr int kMaxSlots = 128;                       // concurrent peer groups
+// Exchange records: [stage 2][slot][peer kRecPeers][row kRecRows] x 2 words.
+constexpr int kRecPeers = 16, kRecRows = 128;
+constexpr size_t kRecStageWords = (size_t)kMaxSlots * kRecPeers * kRecRows * 2;
+constexpr size_t kWsCounterBytes = 4096;             // err word, then the counters
+constexpr size_t kWsHeaderBytes = kWsCounterBytes + 2 * kRecStageWords * 8;
+static_assert(256 + 8 * kMaxSlots <= kWsCounterBytes, "counter area");
 
 // Wave-per-row kernel: the finish pass of the split path (merge the partial
 // (mean, M2) of each row's tiles, then stages 2..4 on the fp32 x the GEMM
