@@ -161,8 +161,8 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
                     (long long)N, kClusterMaxPeers);
       pl.mode = ROWS_CLUSTER;
     } else if (path == PATH_SPLIT) {
-      pl.kidx = pick_tile(M, N, K, in_f32, loop, 1, false, 0);
-      if (pl.kidx < 0) pl.kidx = pick_tile(M, N, K, in_f32, 0, 1, false, 0);
+      pl.kidx = pick_tile(M, N, K, in_f32, loop, 2, false, 0);
+      if (pl.kidx < 0) pl.kidx = pick_tile(M, N, K, in_f32, 0, 2, false, 0);
       pl.mode = ROWS_SPLIT;
     } else {
       return fail(CF_ERR_UNSUPPORTED, "unknown path %d", path);

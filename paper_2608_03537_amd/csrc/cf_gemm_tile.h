@@ -681,7 +681,9 @@ __device__ __forceinline__ void epi_prefetch(EpiPrefetch<S>& pf, const GemmRowsP
 // ---------------------------------------------------------------------------
 // STG: the residual tile and the vectors were staged in LDS by the main loop
 // (slots 0 and 1); otherwise they come from `pf` or straight from memory.
-template <class S, bool STG>
+// SPLIT: the split-N GEMM pass; stage 1, then publish fp32 x and the tile's
+// (mean, M2) for the finish pass (nothing else is compiled in).
+template <class S, bool STG, bool SPLIT>
 __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiPrefetch<S>& pf,
                                          const GemmRowsParams& p, int m0, int n0, int slot, int c, unsigned tag,
                                          int bz, char* smem, float* red, int tid, int lane, int wm, int wn) {
@@ -802,7 +804,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
   const int cnt_c = min(S::TN, N - n0);   // valid columns in this tile
 
   // ---- stage 2: row statistics and the normalising PostOp
-  if (e.norm == NORM_LAYER || p.mode == ROWS_SPLIT) {
+  if (SPLIT || e.norm == NORM_LAYER) {
     float s[S::BM];
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm) {
@@ -843,25 +845,16 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     else dev2(std::true_type{});
     wg_row_reduce<S, false>(m2, red, lane, wm, wn);
 
-    if (p.mode == ROWS_SPLIT) {
-      // Publish fp32 x and the tile's (mean, M2); the finish pass does the rest.
-      float* xb = p.ws_x;
+    if constexpr (SPLIT) {
+      // Publish the tile's (mean, M2) and fp32 x (coalesced through LDS); the
+      // finish pass does the rest.
+      if (wn == 0 && lane < 32) {
 #pragma unroll
-      for (int bm = 0; bm < S::BM; ++bm) {
-        if (!mval[bm]) continue;
-#pragma unroll
-        for (int bn = 0; bn < S::BN; ++bn)
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int n = ncol(bn, g);
-            if (n < N) {
-              float v[4] = {x[bm][bn][4 * g], x[bm][bn][4 * g + 1], x[bm][bn][4 * g + 2], x[bm][bn][4 * g + 3]};
-              store4(xb, (int64_t)mrow[bm] * N + n, 1, v);
-            }
-          }
-        if (wn == 0 && lane < 32)
-          reinterpret_cast<float2*>(p.ws_part)[(int64_t)mrow[bm] * p.cn + c] = make_float2(mean[bm], m2[bm]);
+        for (int bm = 0; bm < S::BM; ++bm)
+          if (mval[bm])
+            reinterpret_cast<float2*>(p.ws_part)[(int64_t)mrow[bm] * p.cn + c] = make_float2(mean[bm], m2[bm]);
       }
+      store_tile_staged<S>(x, p.ws_x, N, 1, M, N, m0, n0, smem, tid, lane, wm, wn);
       return;
     }
 
@@ -1037,13 +1030,14 @@ __device__ __forceinline__ void epilogue_plain(f32x16_t (&x)[S::BM][S::BN], cons
 
 // LOOP: 0 = register-staged main loop (any layout, ragged K),
 //       1 = direct-to-LDS pipeline (W stored N x K, K a multiple of the stage).
-// EPI:  0 = plain epilogue (alpha, bias, store), 1 = row-subgraph epilogue.
+// EPI:  0 = plain epilogue (alpha, bias, store), 1 = row-subgraph epilogue
+//       (whole rows or row clusters), 2 = the split-N GEMM pass.
 template <class S, int LOOP, int EPI>
 __global__ __launch_bounds__(S::NT, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_rows_kernel(GemmRowsParams p) {
   using T = typename S::T;
   constexpr int SMEM = LOOP ? S::SMEM_V2 : S::SMEM_V1;
-  constexpr bool STG = LOOP == 1 && EPI == 1 && S::STG;   // epilogue operands staged by the main loop
+  constexpr bool STG = LOOP == 1 && EPI >= 1 && S::STG;   // epilogue operands staged by the main loop
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   float* red = reinterpret_cast<float*>(smem + SMEM - S::TAIL_BYTES);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1070,7 +1064,7 @@ void gemm_rows_kernel(GemmRowsParams p) {
     const bool cluster = EPI == 1 && p.mode == ROWS_CLUSTER && p.cn > 1;
     unsigned long long round_old = 0;
     if (cluster) round_old = round_begin(p, q * 8 + xcd, lane, S::NW);
-    if constexpr (EPI == 1 && !STG) epi_prefetch<S>(pf, p, m0, n0, bz, lane, wm, wn);
+    if constexpr (EPI >= 1 && !STG) epi_prefetch<S>(pf, p, m0, n0, bz, lane, wm, wn);
     if constexpr (LOOP == 1) mainloop_v2<S, STG>(acc, X, W, p, m0, n0, bz, smem, lane, wave, wm, wn);
     else mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn);
     unsigned tag = 0;
@@ -1078,8 +1072,8 @@ void gemm_rows_kernel(GemmRowsParams p) {
       tag = round_tag(round_old);
       asm volatile("" ::"s"(tag) : "memory");   // this wave's add has returned before any epilogue barrier
     }
-    if constexpr (EPI == 1)
-      epilogue<S, STG>(acc, pf, p, m0, n0, q * 8 + xcd, c, tag, bz, smem, red, tid_t, lane_t, wm, wn);
+    if constexpr (EPI >= 1)
+      epilogue<S, STG, EPI == 2>(acc, pf, p, m0, n0, q * 8 + xcd, c, tag, bz, smem, red, tid_t, lane_t, wm, wn);
     else epilogue_plain<S>(acc, p, m0, n0, bz, smem, tid_t, lane_t, wm, wn);
     __syncthreads();
   }
