@@ -31,7 +31,8 @@
  *             restricted domain of the paper's frontend (Sec. V, frontend
  *             mapping).  M = 0 (or batch = 0) is a no-op returning CF_OK.
  * Alignment   Base pointers of matrices must be 16-byte aligned and leading
- *             dimensions multiples of 16 bytes (CF_ERR_ALIGN otherwise).
+ *             dimensions multiples of 16 bytes (CF_ERR_ALIGN otherwise);
+ *             a row pitch of 2^23 bytes or more returns CF_ERR_LD.
  * Aliasing    An output equal to an input pointer returns CF_ERR_ALIAS;
  *             partial overlap is undefined.
  * Determinism Results are bitwise reproducible run to run: no floating-point

@@ -35,6 +35,8 @@ size_t dsize(cf_dtype t) { return t == CF_F32 ? 4 : t == CF_BF16 ? 2 : 1; }
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+constexpr int64_t kMaxRowPitch = int64_t(1) << 23;   // bytes per row; 256 rows stay below 2^31
+
 cf_status check_matrix(const char* name, const void* p, int64_t rows, int64_t cols, int64_t ld,
                        cf_dtype t, bool required) {
   if (!p) {
@@ -47,6 +49,10 @@ cf_status check_matrix(const char* name, const void* p, int64_t rows, int64_t co
   if (!aligned16(p)) return fail(CF_ERR_ALIGN, "%s is not 16-byte aligned", name);
   if ((ld * (int64_t)dsize(t)) % 16 != 0)
     return fail(CF_ERR_ALIGN, "%s: leading dimension %lld is not a multiple of 16 bytes", name, (long long)ld);
+  // Kernels address a tile's rows with 32-bit byte offsets.
+  if (ld * (int64_t)dsize(t) >= kMaxRowPitch)
+    return fail(CF_ERR_LD, "%s: leading dimension %lld is %lld bytes or more", name, (long long)ld,
+                (long long)kMaxRowPitch);
   return CF_OK;
 }
 

@@ -590,13 +590,12 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
 // not stored.  Needs TM * (TN * esz + pad) bytes of LDS; callers reach it
 // after the main loop's final barrier.
 // ---------------------------------------------------------------------------
-template <class S>
-__device__ __forceinline__ void store_tile_staged(const f32x16_t (&x)[S::BM][S::BN], void* Ybase, int64_t ldy,
-                                                  int y_f32, int M, int N, int m0, int n0, char* smem,
-                                                  int tid, int lane, int wm, int wn) {
+template <class S, int ESZ>
+__device__ __forceinline__ void store_tile_staged_t(const f32x16_t (&x)[S::BM][S::BN], void* Ybase, int64_t ldy,
+                                                    int M, int N, int m0, int n0, char* smem, int tid, int lane,
+                                                    int wm, int wn) {
   const int lr = lane & 31, lg = lane >> 5;
-  const int esz = y_f32 ? 4 : 2;
-  const int pitch = S::TN * esz + (y_f32 ? 16 : 8);
+  constexpr int PITCH = S::TN * ESZ + (ESZ == 4 ? 16 : 8);
 #pragma unroll
   for (int bm = 0; bm < S::BM; ++bm) {
     const int r = wm * S::WTM + bm * 32 + lr;
@@ -605,8 +604,8 @@ __device__ __forceinline__ void store_tile_staged(const f32x16_t (&x)[S::BM][S::
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int cidx = wn * S::WTN + bn * 32 + 8 * g + 4 * lg;
-        char* dst = smem + r * pitch + cidx * esz;
-        if (y_f32) {
+        char* dst = smem + r * PITCH + cidx * ESZ;
+        if constexpr (ESZ == 4) {
           f32x4_t o = {x[bm][bn][4 * g], x[bm][bn][4 * g + 1], x[bm][bn][4 * g + 2], x[bm][bn][4 * g + 3]};
           *reinterpret_cast<f32x4_t*>(dst) = o;
         } else {
@@ -616,22 +615,48 @@ __device__ __forceinline__ void store_tile_staged(const f32x16_t (&x)[S::BM][S::
         }
       }
   }
-  __syncthreads();
-  const int cpr = S::TN * esz / 16;            // 16-byte chunks per tile row
-  const int epc = 16 / esz;                    // elements per chunk
-  char* Y = reinterpret_cast<char*>(Ybase);
-  for (int id = tid; id < S::TM * cpr; id += S::NT) {
-    const int r = id / cpr, cc = id % cpr;
-    const int m = m0 + r, n = n0 + cc * epc;
-    if (m < M && n < N) {
-      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(smem + r * pitch + cc * 16);
-      *reinterpret_cast<u32x4_t*>(Y + ((int64_t)m * ldy + n) * esz) = v;
+  __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14));   // lgkmcnt(0): this wave's LDS writes are done
+  lds_barrier();
+  constexpr int CPR = S::TN * ESZ / 16;   // 16-byte chunks per tile row
+  constexpr int EPC = 16 / ESZ;           // elements per chunk
+  constexpr int TOTAL = S::TM * CPR;
+  constexpr int ITER = (TOTAL + S::NT - 1) / S::NT;
+  constexpr int BATCH = ITER < 8 ? ITER : 8;   // LDS reads in flight before their stores
+  // Addresses are 32-bit offsets from the tile origin (the host keeps
+  // TM * ldy * ESZ below 2^31).
+  char* yb = reinterpret_cast<char*>(Ybase) + ((int64_t)m0 * ldy + n0) * ESZ;
+  const int ldyb = (int)ldy * ESZ;
+  const bool full = m0 + S::TM <= M && n0 + S::TN <= N;
+  const int rows = M - m0, cols = N - n0;
+#pragma unroll
+  for (int j0 = 0; j0 < ITER; j0 += BATCH) {
+    u32x4_t v[BATCH];
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int id = tid + (j0 + j) * S::NT;
+      if (j0 + j < ITER && (TOTAL % S::NT == 0 || id < TOTAL))
+        v[j] = *reinterpret_cast<const u32x4_t*>(smem + (id / CPR) * PITCH + (id % CPR) * 16);
+    }
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int id = tid + (j0 + j) * S::NT;
+      const int r = id / CPR, cc = id % CPR;
+      if (j0 + j < ITER && (TOTAL % S::NT == 0 || id < TOTAL) && (full || (r < rows && cc * EPC < cols)))
+        *reinterpret_cast<u32x4_t*>(yb + (unsigned)(r * ldyb + cc * 16)) = v[j];
     }
   }
   // The staging area is reused by the next reduction: every lane has read
   // its chunks (the stores consumed them), so a bare barrier suffices and the
   // global stores drain while the workgroup goes on.
   lds_barrier();
+}
+
+template <class S>
+__device__ __forceinline__ void store_tile_staged(const f32x16_t (&x)[S::BM][S::BN], void* Ybase, int64_t ldy,
+                                                  int y_f32, int M, int N, int m0, int n0, char* smem,
+                                                  int tid, int lane, int wm, int wn) {
+  if (y_f32) store_tile_staged_t<S, 4>(x, Ybase, ldy, M, N, m0, n0, smem, tid, lane, wm, wn);
+  else store_tile_staged_t<S, 2>(x, Ybase, ldy, M, N, m0, n0, smem, tid, lane, wm, wn);
 }
 
 // ---------------------------------------------------------------------------
@@ -716,18 +741,25 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
 #pragma unroll
         for (int i = 0; i < 16; ++i) x[bm][bn][i] *= alpha;
   }
+  // LDS operands are read a block at a time, all reads issued before the
+  // first use (sched_barrier), so their latencies overlap.
   if (e.bias) {   // only given terms are added (x + 0 would turn -0 into +0)
 #pragma unroll
-    for (int bn = 0; bn < S::BN; ++bn)
+    for (int bn = 0; bn < S::BN; ++bn) {
+      f32x4_t bv[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        if constexpr (STG) bv[g] = vec_lds(0, col_l(bn, g));
+        else bv[g] = pf.b[bn][g];
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int g = 0; g < 4; ++g)
 #pragma unroll
         for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            if constexpr (STG) x[bm][bn][4 * g + q] += vec_lds(0, col_l(bn, g))[q];
-            else x[bm][bn][4 * g + q] += pf.b[bn][g][q];
-          }
+          for (int q = 0; q < 4; ++q) x[bm][bn][4 * g + q] += bv[g][q];
+    }
   }
   if constexpr (STG) if (e.R) {
     // Residual row r, columns 4j..4j+3 of chunk group c = j / 2: chunk position
@@ -736,12 +768,20 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     for (int bm = 0; bm < S::BM; ++bm) {
       const int r = wm * S::WTM + bm * 32 + lr;
       const char* rowp = r < S::STG_RA ? smem + r * S::TN * 2 : smem + S::V2_STAGE + (r - S::STG_RA) * S::TN * 2;
+      u32x2_t rv[S::BN][4];
 #pragma unroll
       for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int cl = col_l(bn, g);
-          const u32x2_t u = *reinterpret_cast<const u32x2_t*>(rowp + (((cl >> 3) ^ (r & 7)) << 4) + (cl & 7) * 2);
+          rv[bn][g] = *reinterpret_cast<const u32x2_t*>(rowp + (((cl >> 3) ^ (r & 7)) << 4) + (cl & 7) * 2);
+        }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const u32x2_t u = rv[bn][g];
           x[bm][bn][4 * g + 0] += bf16_to_f32(u[0] & 0xFFFFu);
           x[bm][bn][4 * g + 1] += bf16_to_f32(u[0] >> 16);
           x[bm][bn][4 * g + 2] += bf16_to_f32(u[1] & 0xFFFFu);
@@ -878,23 +918,30 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
           for (int i = 0; i < 16; ++i) x[bm][bn][i] = (x[bm][bn][i] - mean[bm]) * rstd[bm];
       if (e.gamma || e.beta) {
 #pragma unroll
-        for (int bn = 0; bn < S::BN; ++bn)
+        for (int bn = 0; bn < S::BN; ++bn) {
+          f32x4_t ga[4], be[4];
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int n = min(ncol(bn, g), N - 4);   // padding columns are never stored
-            f32x4_t ga = {1.0f, 1.0f, 1.0f, 1.0f}, be = {0.0f, 0.0f, 0.0f, 0.0f};
+            ga[g] = f32x4_t{1.0f, 1.0f, 1.0f, 1.0f};
+            be[g] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
             if constexpr (STG) {
-              if (e.gamma) ga = vec_lds(1, col_l(bn, g));
-              if (e.beta) be = vec_lds(2, col_l(bn, g));
+              if (e.gamma) ga[g] = vec_lds(1, col_l(bn, g));
+              if (e.beta) be[g] = vec_lds(2, col_l(bn, g));
             } else {
-              if (e.gamma) ga = *reinterpret_cast<const f32x4_t*>(e.gamma + n);
-              if (e.beta) be = *reinterpret_cast<const f32x4_t*>(e.beta + n);
+              if (e.gamma) ga[g] = *reinterpret_cast<const f32x4_t*>(e.gamma + n);
+              if (e.beta) be[g] = *reinterpret_cast<const f32x4_t*>(e.beta + n);
             }
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
 #pragma unroll
             for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-              for (int q = 0; q < 4; ++q) x[bm][bn][4 * g + q] = fmaf(x[bm][bn][4 * g + q], ga[q], be[q]);
-          }
+              for (int q = 0; q < 4; ++q)
+                x[bm][bn][4 * g + q] = fmaf(x[bm][bn][4 * g + q], ga[g][q], be[g][q]);
+        }
       }
     }
   } else if (e.norm == NORM_RMS) {
