@@ -36,9 +36,16 @@ def _hipcc():
     return h
 
 
+# The GEMM + row-epilogue kernels keep MFMA accumulators in VGPRs: their
+# epilogue is VALU work on the accumulator tile, and accumulators in AGPRs
+# would cost a copy each way for every elementwise step.
+FILE_FLAGS = {f: ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+              for f in ("cf_gemm_inst_v2.hip", "cf_gemm_inst_v1.hip", "cf_gemm_inst_wr.hip", "cf_gemm_inst_split.hip")}
+
+
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [_hipcc(), *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *CFLAGS, *FILE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     errs = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
                      if "packed-fp32-ops" not in l and l.strip())
