@@ -184,7 +184,8 @@ cf_status cf_gemm_subgraph(const cf_subgraph_args* a, void* workspace,
  *   mid = CF_MID_GELU_BIAS : S = GELU(P + b1)                       (FFN)
  *   mid = CF_MID_SOFTMAX   : S = softmax_row(mid_scale * P), computed
  *                            online over blocks of N1 (running row max and
- *                            sum in fp32), so O = S W2 is exact softmax   (attention)
+ *                            sum in fp32), so O = S W2 is exact softmax   (attention);
+ *                            mid_scale must be finite and > 0 (CF_ERR_SHAPE)
  *   out = CF_OUT_STORE     : Y = O (+ b2 if given)
  *   out = CF_OUT_BIAS_RESIDUAL_LN : Y = LN(O + b2 + R) * gamma + beta
  *

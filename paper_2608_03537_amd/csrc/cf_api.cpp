@@ -631,7 +631,8 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, voi
         return fail(CF_ERR_UNSUPPORTED, "attention head dim %lld not compiled (64, 128)", (long long)a->K);
       if (a->out != CF_OUT_STORE || a->b2 || a->R || a->b1)
         return fail(CF_ERR_UNSUPPORTED, "attention supports the plain store of O only");
-      if (!std::isfinite(a->mid_scale)) return fail(CF_ERR_SHAPE, "mid_scale must be finite");
+      if (!std::isfinite(a->mid_scale) || !(a->mid_scale > 0.0f))
+        return fail(CF_ERR_SHAPE, "mid_scale must be finite and > 0");
     }
     const bool empty = a->M == 0 || a->batch == 0;
     const int64_t w1_rows = ffn ? a->N1 : a->N1, w1_cols = a->K;

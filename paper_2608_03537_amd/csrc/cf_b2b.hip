@@ -371,10 +371,17 @@ void b2b_ffn_kernel(B2BParams p) {
 // ===========================================================================
 // Attention: O = softmax(scale * Q K^T) V per (batch*head), online softmax.
 // 4 waves x 32 queries = 128 queries per workgroup; key/value blocks of 64.
-// Q fragments stay in registers for the whole sweep.  Per block:
-//   S^T = K Q^T (K rows from LDS), lane-local row max / sum over its 32
-//   values + the lane pair, P = exp2(S*scale*log2e - m), O = O*corr + P V
+// Q fragments stay in registers for the whole sweep.  Per block j:
+//   S^T = K Q^T (K rows from LDS); lane-local row max / sum over its 32
+//   values + the lane pair; P = exp2(S*scale*log2e - m); O = O*corr + P V
 //   with P fed from registers and V^T rows from LDS.
+// Software pipeline inside each wave (the PingPong of Sec. III-C): the 16
+// MFMAs of block j+1's S^T are issued one per slot, and between them the
+// softmax of block j runs in 16 VALU chunks; then block j's P V MFMAs.
+// The running maximum is raised lazily: O and the row sum are rescaled only
+// when a block's maximum exceeds the one in use by more than 2^8, so
+// exp2(s - m) <= 256 and the common case skips the rescale; the final O / l
+// uses the same maximum throughout, so the result is unchanged.
 // K blocks arrive by wave-wide direct loads; V is transposed on its way into
 // LDS (rows d, 64 keys contiguous) through registers.
 // ===========================================================================
@@ -391,13 +398,22 @@ struct AttnShape {
   static constexpr int BD = D / 32;               // output blocks over d
   static constexpr int KROW = D * 2;              // bytes per K row
   static constexpr int KCH = KROW / 16;           // 16-byte chunks per K row
-  static constexpr int VCH = TN * D / 8 / NT;     // V chunks (8 d of one key) per thread
+  static constexpr int NSA = 2 * DK;              // MFMAs of one S^T block (two 32-key halves)
+  static constexpr int NSB = 4 * BD;              // MFMAs of one P V block
   using Out = TileShape<bf16_t, 1, BD, 4, 1, 128, 0>;
   static_assert(D % 32 == 0 && D <= 128, "head dim");
+  static_assert(16 % NSA == 0 || NSA % 16 == 0, "softmax chunks per slot");
+};
+
+// Softmax state of one block for one lane (query row lane % 32).
+struct SoftmaxStep {
+  float bmax, bsum, corr;
+  bool need;
+  u32x4_t P[2][2];   // bf16 P^T fragments: [32-key half][MFMA step]
 };
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
+__global__ __launch_bounds__(256, 1) void b2b_attention_kernel(B2BParams p) {
   using A = AttnShape<D>;
   __shared__ __attribute__((aligned(16))) char smem[A::LDS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -408,8 +424,9 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   const bf16_t* Q = p.X + (int64_t)bz * p.sx;
   const bf16_t* Kp = p.W1 + (int64_t)bz * p.sw1;
   const bf16_t* Vp = p.W2 + (int64_t)bz * p.sw2;
-  const float sl2 = p.mid_scale * 1.4426950408889634f;   // scale * log2(e)
+  const float sl2 = p.mid_scale * 1.4426950408889634f;   // scale * log2(e), > 0
   const int NB = (Lk + A::TN - 1) / A::TN;
+  constexpr float kLazy = 8.0f;                           // rescale threshold (log2 units)
 
   // Q fragments (B operand of S^T = K Q^T): row m, 8 d per lane per step.
   const int m = m0 + wave * 32 + lr;
@@ -420,49 +437,62 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
 
   // K block rows: swizzled 16-byte chunks inside D*2-byte rows (D/8 chunks;
   // the XOR uses only chunk bits that exist).  Rows past Lk are clamped and
-  // masked to -inf in the scores.
+  // masked out of P in the last block.
   // 256-byte rows (d = 128) all start on bank 0, so 16 consecutive rows need
   // 16 distinct chunk positions: XOR with (row & 15).  128-byte rows (d = 64)
   // pair up within 256 bytes: XOR with ((row >> 1) & 7).
   auto kswz = [](int row) { return A::KCH == 16 ? (row & 15) : ((row >> 1) & 7); };
   auto koff = [&](int row, int c) { return row * A::KROW + ((c ^ kswz(row)) << 4); };
-  u32x4_t vreg[A::VCH];
+  // V^T in LDS: rows d of 64 keys (128 bytes), 16-byte chunk c of row d at
+  // position c ^ vswz(d).  vswz mixes d >> 3 into the row-pair swizzle so the
+  // transposing writes (16 rows d = 8 dc + e at a time) spread over the banks
+  // while 32 consecutive rows still read conflict-free.
+  auto vt_off = [](int d, int c) { return d * 128 + ((c ^ (((d >> 1) ^ (d >> 3)) & 7)) << 4); };
+  // Thread t moves keys 4 kg .. 4 kg + 3 of d chunk dc (8 d): four 16-byte
+  // global loads, an in-register 4 x 8 transpose, eight 8-byte LDS writes.
+  constexpr int DC = D / 8;
+  const int vkg = tid / DC, vdc = tid % DC;
+  const bool vact = tid < (A::TN / 4) * DC;
+  u32x4_t vreg[4];
   auto issue_k = [&](int j) {
     char* dst = smem + (j & 1) * A::STAGE;
     constexpr int LPR = A::KCH;                 // lanes per row in one wave-wide load
     constexpr int RPI = 64 / LPR;               // rows per instruction
-    for (int ins = wave; ins < A::TN / RPI; ins += 4) {
-      const int row = ins * RPI + lane / LPR;
+#pragma unroll
+    for (int ins = 0; ins < A::TN / RPI / 4; ++ins) {
+      const int in = wave + 4 * ins;
+      const int row = in * RPI + lane / LPR;
       const int pos = lane % LPR;
       const int c = pos ^ kswz(row);
       const int key = min(j * A::TN + row, Lk - 1);
-      dma16(reinterpret_cast<const char*>(Kp + (int64_t)key * p.ldw1) + c * 16, dst + ins * 1024);
+      dma16(reinterpret_cast<const char*>(Kp + (int64_t)key * p.ldw1) + c * 16, dst + in * 1024);
     }
   };
   auto load_v = [&](int j) {
+    if (vact) {
 #pragma unroll
-    for (int i = 0; i < A::VCH; ++i) {
-      const int ch = tid + i * A::NT;            // chunk = 8 d of one key
-      const int key = ch / (D / 8), dc = ch % (D / 8);
-      const int kk = min(j * A::TN + key, Lk - 1);
-      vreg[i] = gload16(Vp + (int64_t)kk * p.ldw2 + dc * 8);
+      for (int k = 0; k < 4; ++k) {
+        const int kk = min(j * A::TN + 4 * vkg + k, Lk - 1);
+        vreg[k] = gload16(Vp + (int64_t)kk * p.ldw2 + vdc * 8);
+      }
     }
   };
   auto store_v = [&](int j) {
-    char* vt = smem + (j & 1) * A::STAGE + A::KB;
-#pragma unroll
-    for (int i = 0; i < A::VCH; ++i) {
-      const int ch = tid + i * A::NT;
-      const int key = ch / (D / 8), dc = ch % (D / 8);
-      // V^T row d, key column: 16-byte chunk key/8 of the 128-byte row.
+    if (vact) {
+      char* vt = smem + (j & 1) * A::STAGE + A::KB;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int d = dc * 8 + e;
-        const uint32_t w = vreg[i][e >> 1];
-        *reinterpret_cast<uint16_t*>(vt + swz_off(d, key >> 3) + (key & 7) * 2) =
-            (uint16_t)((e & 1) ? (w >> 16) : (w & 0xFFFFu));
+        // keys 0..3 of d = 8 vdc + e: low (e even) or high halves of word e / 2
+        const unsigned sel = (e & 1) ? 0x07060302u : 0x05040100u;
+        const u32x2_t w = {__builtin_amdgcn_perm(vreg[1][e >> 1], vreg[0][e >> 1], sel),
+                           __builtin_amdgcn_perm(vreg[3][e >> 1], vreg[2][e >> 1], sel)};
+        *reinterpret_cast<u32x2_t*>(vt + vt_off(8 * vdc + e, vkg >> 1) + (vkg & 1) * 8) = w;
       }
     }
+  };
+  auto lds_sync = [] {   // this wave's LDS accesses are done, then a workgroup barrier
+    __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14));
+    lds_barrier();
   };
 
   f32x16_t Oa[A::BD];
@@ -470,71 +500,164 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   for (int b = 0; b < A::BD; ++b)
 #pragma unroll
     for (int i = 0; i < 16; ++i) Oa[b][i] = 0.0f;
-  float mrun = -INFINITY, lrun = 0.0f;
+  float m_used = -INFINITY, lrun = 0.0f;
 
+  // MFMA i of an S^T block (half i / DK, d step i % DK); its K fragment is
+  // read two slots ahead.
+  auto kfrag = [&](const char* kb, int i) {
+    return lds_read16(kb + koff((i / A::DK) * 32 + lr, 2 * (i % A::DK) + lg));
+  };
+  auto mma_s = [&](f32x16_t (&S)[2], int i, u32x4_t kf) {
+    const int b = i / A::DK, ks = i % A::DK;
+    const f32x16_t zero = {};
+    S[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
+                                                   __builtin_bit_cast(bf16x8_t, qf[ks]), ks == 0 ? zero : S[b],
+                                                   0, 0, 0);
+  };
+  // Softmax of block j in 16 chunks (S is this lane's 32 scores, raw).
+  auto sm_chunk = [&](f32x16_t (&S)[2], int c, SoftmaxStep& st, int j, auto mask_t) {
+    constexpr bool MASK = decltype(mask_t)::value;
+    if (c < 4) {   // block maximum of the raw scores (scale > 0)
+      float t = c == 0 ? -INFINITY : st.bmax;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) t = fmaxf(t, S[c >> 1][(c & 1) * 8 + q]);
+      st.bmax = t;
+    } else if (c == 4) {
+      st.bmax = lane_pair_max(st.bmax) * sl2;
+    } else if (c == 5) {
+      const float mnew = fmaxf(m_used, st.bmax);
+      st.need = mnew > m_used + kLazy;
+      const float m_eff = st.need ? mnew : m_used;
+      st.corr = __builtin_amdgcn_exp2f(m_used - m_eff);   // exactly 1 when the maximum in use stays
+      m_used = m_eff;
+      st.bsum = 0.0f;
+    } else if (c < 14) {   // P = exp2(s * scale * log2e - m), 4 values per chunk
+      const float nm = -m_used;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = (c - 6) * 4 + q;
+        float pv = __builtin_amdgcn_exp2f(fmaf(S[e >> 4][e & 15], sl2, nm));
+        if constexpr (MASK) {
+          const int key = j * A::TN + (e >> 4) * 32 + acc_row(e & 15, lane);
+          pv = key < Lk ? pv : 0.0f;
+        }
+        S[e >> 4][e & 15] = pv;
+        st.bsum += pv;
+      }
+    } else if (c == 14) {
+      st.P[0][0] = pack_step(S[0], 0);
+      st.P[0][1] = pack_step(S[0], 1);
+      st.bsum = lane_pair_sum(st.bsum);
+    } else {
+      st.P[1][0] = pack_step(S[1], 0);
+      st.P[1][1] = pack_step(S[1], 1);
+      lrun = lrun * st.corr + st.bsum;
+    }
+  };
+  auto rescale = [&](const SoftmaxStep& st) {
+    if (__any(st.need)) {
+#pragma unroll
+      for (int b = 0; b < A::BD; ++b)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) Oa[b][i] *= st.corr;
+    }
+  };
+  // O^T += V^T P^T for block j (V^T fragments two MFMAs ahead).
+  auto pv_block = [&](int j, const SoftmaxStep& st) {
+    const char* vt = smem + (j & 1) * A::STAGE + A::KB;
+    auto vfrag = [&](int i) {   // i = (bl * 2 + s) * BD + b; permuted k order of pack_step
+      const int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
+      const int row = b * 32 + lr, c0 = 4 * bl + 2 * s;
+      const u32x2_t lo = lds_read8(vt + vt_off(row, c0) + 8 * lg);
+      const u32x2_t hi = lds_read8(vt + vt_off(row, c0 + 1) + 8 * lg);
+      return u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+    };
+    u32x4_t vf[3];
+    vf[0] = vfrag(0);
+    if (A::NSB > 1) vf[1] = vfrag(1);
+#pragma unroll
+    for (int i = 0; i < A::NSB; ++i) {
+      if (i + 2 < A::NSB) vf[(i + 2) % 3] = vfrag(i + 2);
+      const int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
+      Mma<bf16_t>::run(Oa[b], vf[i % 3], st.P[bl][s]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // One pipelined step: S^T of block j+1 (into Sn) under the softmax of block j (Sc).
+  auto s_and_softmax = [&](f32x16_t (&Sn)[2], f32x16_t (&Sc)[2], int j, SoftmaxStep& st, auto mask_t) {
+    const char* kb = smem + ((j + 1) & 1) * A::STAGE;
+    u32x4_t kf[3];
+    kf[0] = kfrag(kb, 0);
+    kf[1] = kfrag(kb, 1);
+    constexpr int CPS = A::NSA >= 16 ? 1 : 16 / A::NSA;   // softmax chunks per MFMA slot
+#pragma unroll
+    for (int i = 0; i < A::NSA; ++i) {
+      if (i + 2 < A::NSA) kf[(i + 2) % 3] = kfrag(kb, i + 2);
+      mma_s(Sn, i, kf[i % 3]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < CPS; ++q)
+        if (i * CPS + q < 16) sm_chunk(Sc, i * CPS + q, st, j, mask_t);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  auto softmax_only = [&](f32x16_t (&Sc)[2], int j, SoftmaxStep& st, auto mask_t) {
+#pragma unroll
+    for (int c = 0; c < 16; ++c) sm_chunk(Sc, c, st, j, mask_t);
+  };
+
+  f32x16_t Sa[2], Sb[2];
+  SoftmaxStep st;
+  // Prologue: K, V of block 0 (V transposed into LDS), K, V of block 1 in
+  // flight, S^T of block 0.
   issue_k(0);
   load_v(0);
+  wait_vmcnt<0>();
   store_v(0);
-  for (int j = 0; j < NB; ++j) {
-    wait_vmcnt<0>();
-    __syncthreads();
-    if (j + 1 < NB) {
-      issue_k(j + 1);
-      load_v(j + 1);
-    }
-    const char* kb = smem + (j & 1) * A::STAGE;
-    const char* vt = kb + A::KB;
-    // S^T block (64 keys x 32 queries) = K Q^T
-    f32x16_t Sb[2];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) Sb[b][i] = 0.0f;
-#pragma unroll
-      for (int ks = 0; ks < A::DK; ++ks)
-        Mma<bf16_t>::run(Sb[b], lds_read16(kb + koff(b * 32 + lr, 2 * ks + lg)), qf[ks]);
-    }
-    // Online softmax for this lane's query row.
-    float bmax = -INFINITY;
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = j * A::TN + b * 32 + acc_row(i, lane);
-        const float sv = key < Lk ? Sb[b][i] * sl2 : -INFINITY;
-        Sb[b][i] = sv;
-        bmax = fmaxf(bmax, sv);
-      }
-    const float mnew = fmaxf(mrun, lane_pair_max(bmax));
-    const float corr = exp2f(mrun - mnew);
-    float bsum = 0.0f;
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float pv = exp2f(Sb[b][i] - mnew);
-        Sb[b][i] = pv;
-        bsum += pv;
-      }
-    lrun = lrun * corr + lane_pair_sum(bsum);
-    mrun = mnew;
-#pragma unroll
-    for (int b = 0; b < A::BD; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) Oa[b][i] *= corr;
-    // O^T += V^T P^T, P from registers in the permuted k order.
-#pragma unroll
-    for (int bl = 0; bl < 2; ++bl)
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const u32x4_t pb = pack_step(Sb[bl], s);
-#pragma unroll
-        for (int b = 0; b < A::BD; ++b) Mma<bf16_t>::run(Oa[b], frag_perm(vt, b * 32 + lr, bl, s, lg), pb);
-      }
-    // Buffer (j+1)&1 was last read in iteration j-1, which every wave left
-    // at this iteration's first barrier; the next barrier publishes it.
-    if (j + 1 < NB) store_v(j + 1);
+  if (NB > 1) {
+    issue_k(1);
+    load_v(1);
   }
+  lds_sync();
+  {
+    const char* kb = smem;
+#pragma unroll
+    for (int i = 0; i < A::NSA; ++i) mma_s(Sa, i, kfrag(kb, i));
+  }
+  // Steady step j (blocks j and j+1 exist): K, V of block j+1 landed; V of
+  // block j+1 goes to LDS; K, V of block j+2 are issued; then the pipelined
+  // S^T(j+1) / softmax(j), the rescale and P V of block j.
+  auto step = [&](int j, f32x16_t (&Sc)[2], f32x16_t (&Sn)[2]) {
+    wait_vmcnt<0>();
+    lds_sync();   // V(j) and K(j+1) visible; buffers of blocks j-1 (V) and j (K) are free
+    store_v(j + 1);
+    if (j + 2 < NB) {
+      issue_k(j + 2);
+      load_v(j + 2);
+    }
+    s_and_softmax(Sn, Sc, j, st, std::false_type{});
+    rescale(st);
+    pv_block(j, st);
+  };
+  // Last block (NB-1): masked softmax, rescale, P V.
+  auto last = [&](f32x16_t (&Sl)[2]) {
+    lds_sync();   // V(NB-1), stored after the previous barrier, is visible
+    softmax_only(Sl, NB - 1, st, std::true_type{});
+    rescale(st);
+    pv_block(NB - 1, st);
+  };
+  int j = 0;
+  for (; j + 2 < NB; j += 2) {
+    step(j, Sa, Sb);
+    step(j + 1, Sb, Sa);
+  }
+  if (j + 1 < NB) {
+    step(j, Sa, Sb);
+    last(Sb);
+  } else {
+    last(Sa);
+  }
+
   __syncthreads();
   const float inv = 1.0f / lrun;
 #pragma unroll
