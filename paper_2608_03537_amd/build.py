@@ -36,11 +36,12 @@ def _hipcc():
     return h
 
 
-# The GEMM + row-epilogue kernels keep MFMA accumulators in VGPRs: their
-# epilogue is VALU work on the accumulator tile, and accumulators in AGPRs
-# would cost a copy each way for every elementwise step.
+# MFMA accumulators stay in VGPRs: every kernel here runs VALU work on its
+# accumulator tiles (the row epilogue, GELU, softmax), and accumulators in
+# AGPRs would cost a copy each way for every such step.
 FILE_FLAGS = {f: ["-mllvm", "-amdgpu-mfma-vgpr-form"]
-              for f in ("cf_gemm_inst_v2.hip", "cf_gemm_inst_v1.hip", "cf_gemm_inst_wr.hip", "cf_gemm_inst_split.hip")}
+              for f in ("cf_gemm_inst_v2.hip", "cf_gemm_inst_v1.hip", "cf_gemm_inst_wr.hip", "cf_gemm_inst_split.hip",
+                        "cf_b2b.hip")}
 
 
 def _compile(src):

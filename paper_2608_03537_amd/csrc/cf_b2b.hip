@@ -418,8 +418,15 @@ __global__ __launch_bounds__(256, 1) void b2b_attention_kernel(B2BParams p) {
   __shared__ __attribute__((aligned(16))) char smem[A::LDS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lg = lane >> 5;
-  const int bz = blockIdx.y;
-  const int m0 = blockIdx.x * A::TM;
+  // XCD-aware order: workgroups go round-robin over the 8 XCDs by linear id,
+  // so linear id L runs on XCD L % 8.  Give each XCD a contiguous range of
+  // (head, query block) pairs: the query blocks of one head then share that
+  // XCD's L2 copy of the head's K and V instead of fetching it on all eight.
+  const int nq = gridDim.x, T = gridDim.x * gridDim.y;
+  const int L = blockIdx.x + nq * blockIdx.y;
+  const int g = (T & 7) == 0 ? (L & 7) * (T >> 3) + (L >> 3) : L;
+  const int bz = g / nq;
+  const int m0 = (g % nq) * A::TM;
   const int Lk = p.N1;
   const bf16_t* Q = p.X + (int64_t)bz * p.sx;
   const bf16_t* Kp = p.W1 + (int64_t)bz * p.sw1;
