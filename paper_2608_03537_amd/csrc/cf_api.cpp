@@ -157,7 +157,13 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
       if (N > kWholeRowMaxN)
         return fail(CF_ERR_UNSUPPORTED, "whole-row path needs N <= %d (N = %lld)", kWholeRowMaxN, (long long)N);
       for (int tn : {128, 256, 384, 512, 768})
-        if (tn >= N) { pl.kidx = find_gemm_kernel(in_f32, 32, tn, 0, 1); break; }
+        if (tn >= N) {
+          // the direct-to-LDS ring where compiled and K fills its prologue
+          const int v2 = loop == 1 ? find_gemm_kernel(in_f32, 32, tn, 1, 1) : -1;
+          if (v2 >= 0 && K / tk >= gemm_kernel(v2).stages - 1) pl.kidx = v2;
+          else pl.kidx = find_gemm_kernel(in_f32, 32, tn, 0, 1);
+          break;
+        }
       pl.mode = ROWS_LOCAL;
     } else if (path == PATH_CLUSTER) {
       pl.kidx = pick_tile(M, N, K, in_f32, loop, 1, true, kClusterMaxPeers);

@@ -76,8 +76,9 @@ struct TileShape {
   // Epilogue operands of the bf16 direct-to-LDS loop (residual tile and the
   // per-column vectors) are loaded by the last main-loop iterations into the
   // two ring slots that free up first (slots 0 and 1): residual rows [0, RA)
-  // and the four 1 KB vector regions in slot 0, rows [RA, TM) in slot 1.
-  static constexpr bool STG = STAGES >= 3 && sizeof(T) == 2;
+  // and the four 1 KB vector regions in slot 0, rows [RA, TM) in slot 1.  A
+  // vector region holds 256 fp32 columns (one 16-byte load per lane).
+  static constexpr bool STG = STAGES >= 3 && sizeof(T) == 2 && TN <= 256;
   static constexpr int STG_VEC = 4096;
   static constexpr int STG_RA0 = STAGES ? (V2_STAGE - STG_VEC) / (TN * 2) / 32 * 32 : 0;
   static constexpr int STG_RA = STG_RA0 < TM ? STG_RA0 : TM;
@@ -371,7 +372,7 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
     // Loads this wave issued after stage kt+1's (the wait below allows them).
     constexpr int AFTER = J < 0 ? PW * (NS - 2)
                                 : PW * (NS - 3 - J) + (!STG ? 0 : J == 0 ? S::STG_IA + 1 : S::STG_IA + 1 + S::STG_IB);
-    static_assert(NL <= (KS - 1) * NMF, "one load per MFMA slot");
+    constexpr int LPS = (NL + (KS - 1) * NMF - 1) / ((KS - 1) * NMF);   // loads per MFMA slot
     const int nxt = kt + NS - 1;
     auto load = [&](int l) {
       if constexpr (J < 0) dma(l, nxt);
@@ -380,7 +381,7 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
     };
     // Steps 0..KS-2; behind each of the first MFMAs one fragment read of the
     // last step (issued after an MFMA so that the MFMA's operands, read during
-    // the previous iteration, need no wait on these) and one load.
+    // the previous iteration, need no wait on these) and LPS loads.
     constexpr int RPF = (NFR + NMF - 1) / NMF;               // last-step reads per MFMA slot
 #pragma unroll
     for (int ks = 0; ks < KS - 1; ++ks)
@@ -394,7 +395,9 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
 #pragma unroll
           for (int r = 0; r < RPF; ++r)
             if (i * RPF + r < NFR) frag1(kt, KS - 1, i * RPF + r);
-          if (i < NL) load(i);
+#pragma unroll
+          for (int r = 0; r < LPS; ++r)
+            if (i * LPS + r < NL) load(i * LPS + r);
           __builtin_amdgcn_sched_barrier(0);
         }
     if constexpr (MORE) {

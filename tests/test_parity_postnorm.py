@@ -60,6 +60,9 @@ SMALL = [  # (M, K, N)
     (33, 784, 768),
     (1, 32, 64),
     (257, 128, 384),
+    (130, 256, 256),   # whole rows on the direct-to-LDS ring (K a multiple of the stage)
+    (70, 192, 128),
+    (65, 320, 320),
 ]
 
 
