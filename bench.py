@@ -44,7 +44,7 @@ F32_PEAK_TFLOPS = 157.3        # dense fp32 MFMA
 # WRITE_SIZE runs (each scaled by a plain-copy calibration: bytes = 2.0 x
 # FETCH_SIZE KiB x 1024 and 1.0 x WRITE_SIZE KiB x 1024), valid only for the
 # kernel sources they were taken on (sha256 over csrc/, see kernel_hash()).
-TRAFFIC = {"kernel_hash": "0a90d07066512843", "bytes": 49383834}
+TRAFFIC = {"kernel_hash": "20e9205137b44b78", "bytes": 49394483}
 
 
 def kernel_hash():
@@ -247,9 +247,13 @@ def workload_attention(torch, cf, I, O, dev):
             cf.gemm(Px, s["V"].view(B * H, Lk, d), b_layout=cf.CF_LAYOUT_KN, out=s["O"].view(B * H, L, d))
         return run
     unfused = time_steps(torch, [unf(s) for s in sets], 8, 2)
+    # context: the vendor attention (torch SDPA on ROCm) on the same inputs
+    sdpa = time_steps(torch, [(lambda s=s: torch.nn.functional.scaled_dot_product_attention(s["Q"], s["K"], s["V"]))
+                              for s in sets], 16, 2)
     flop = 2.0 * B * H * L * Lk * d * 2
     nbytes = 2 * 4 * B * H * L * d
     return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2),
+                     torch_sdpa_us=round(sdpa * 1e3, 2),
                      shape={"B": B, "H": H, "Lq": L, "Lk": Lk, "d": d, "dtype": "bf16"})
 
 
