@@ -129,7 +129,9 @@ cf_status cf_gemm_postnorm(const cf_postnorm_args* a, void* workspace,
  * and must match this grammar (anything else is CF_ERR_UNSUPPORTED):
  *
  *     [SCALE] [BIAS] [RESIDUAL] [LAYERNORM | RMSNORM]
- *     [GELU | GELU_TANH | RELU] STORE [ROWAMAX_QUANT]
+ *     [GELU | GELU_TANH | RELU | SOFTCAP] [SOFTMAX] STORE [ROWAMAX_QUANT]
+ *
+ * (a NORM and SOFTMAX do not appear in one list).
  *
  * SCALE       x *= f0                    (alpha)
  * BIAS        x += v0[n]                 (fp32 [N])
@@ -138,6 +140,10 @@ cf_status cf_gemm_postnorm(const cf_postnorm_args* a, void* workspace,
  * LAYERNORM   x = (x-mean)/sqrt(var+f0) * v0 + v1   (v0/v1 may be NULL)
  * RMSNORM     x = x/sqrt(mean(x^2)+f0) * v0         (v0 may be NULL)
  * GELU        x = x * Phi(x) (erf form); GELU_TANH the tanh approximation
+ * SOFTCAP     x = f0 * tanh(x / f0)       (f0 = cap > 0, finite)
+ * SOFTMAX     x = exp(x - max_row(x)) / sum_row(exp(x - max_row(x)))
+ *             (a scale goes in SCALE; f0 is unused here.  A list holding
+ *             only SOFTMAX is cf_rowop's standalone form below.)
  * STORE       out[m, n] = x  (dtype: F32 or BF16; ld)
  * ROWAMAX_QUANT  s[m] = max_n |x| / f0 (f0 = qmax, 448 for E4M3) into out
  *             (fp32 [M]); out2[m, n] = e4m3(x / s[m]) (ld, may be NULL).
@@ -147,7 +153,7 @@ cf_status cf_gemm_postnorm(const cf_postnorm_args* a, void* workspace,
 typedef enum {
   CF_N_SCALE = 0, CF_N_BIAS = 1, CF_N_RESIDUAL = 2, CF_N_LAYERNORM = 3,
   CF_N_RMSNORM = 4, CF_N_GELU = 5, CF_N_GELU_TANH = 6, CF_N_RELU = 7,
-  CF_N_STORE = 8, CF_N_ROWAMAX_QUANT = 9, CF_N_SOFTMAX = 10
+  CF_N_STORE = 8, CF_N_ROWAMAX_QUANT = 9, CF_N_SOFTMAX = 10, CF_N_SOFTCAP = 11
 } cf_node_kind;
 
 typedef struct {
@@ -159,7 +165,7 @@ typedef struct {
   cf_dtype dtype;     /* STORE output dtype */
   const float* v0;    /* BIAS: bias; LAYERNORM/RMSNORM: gamma */
   const float* v1;    /* LAYERNORM: beta */
-  float f0;           /* SCALE: alpha; *NORM: eps; ROWAMAX_QUANT: qmax */
+  float f0;           /* SCALE: alpha; *NORM: eps; ROWAMAX_QUANT: qmax; SOFTCAP: cap */
 } cf_node;
 
 typedef struct {

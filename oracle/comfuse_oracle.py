@@ -260,6 +260,16 @@ def ln_gelu_amax(X, W_kn, bias=None, R=None, gamma=None, beta=None, eps=1e-5,
     return z, s, q
 
 
+def msts(X, W_kn, alpha=1.0, bias=None, cap=30.0):
+    """MSTS subgraph: row softmax of cap * tanh(x / cap), x = alpha * X.W + bias.
+
+    Scale, tanh softcap and softmax on the GEMM output (the MSTS Stage-Stream
+    workload, Sec. VI); the softcap form is a reading.
+    """
+    x = bias_residual(matmul(X, W_kn), bias, None, alpha)
+    return softmax_rows(tanh_softcap(x, cap))
+
+
 def ffn_b2b(X, W1_kn, b1, W2_kn, b2, gamma=None, beta=None, eps=1e-5):
     """B2BGEMM FFN (Sec. IV, Eq. 2 with F = GELU(. + b1)), followed by a
     residual + LayerNorm epilogue on the second product:

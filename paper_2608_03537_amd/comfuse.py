@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libcomfuse.so")
 CF_F32, CF_BF16, CF_FP8_E4M3 = 0, 1, 2
 CF_LAYOUT_KN, CF_LAYOUT_NK = 0, 1
 (CF_N_SCALE, CF_N_BIAS, CF_N_RESIDUAL, CF_N_LAYERNORM, CF_N_RMSNORM, CF_N_GELU,
- CF_N_GELU_TANH, CF_N_RELU, CF_N_STORE, CF_N_ROWAMAX_QUANT, CF_N_SOFTMAX) = range(11)
+ CF_N_GELU_TANH, CF_N_RELU, CF_N_STORE, CF_N_ROWAMAX_QUANT, CF_N_SOFTMAX, CF_N_SOFTCAP) = range(12)
 CF_MID_GELU_BIAS, CF_MID_SOFTMAX = 0, 1
 CF_OUT_STORE, CF_OUT_BIAS_RESIDUAL_LN = 0, 1
 PATH_AUTO, PATH_WHOLE_ROW, PATH_CLUSTER, PATH_SPLIT = 0, 1, 2, 3

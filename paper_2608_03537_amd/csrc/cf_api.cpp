@@ -226,6 +226,7 @@ cf_status run_rows(const Plan& pl, GemmRowsParams p, void* ws, hipStream_t st) {
     // The GEMM runs stage 1 only and publishes x and partial statistics.
     p.epi.norm = NORM_NONE;
     p.epi.act = ACT_NONE;
+    p.epi.softmax = 0;
     p.epi.Y = nullptr;
     p.epi.quant = 0;
     cf_status s = hip_status(launch_gemm_rows(p, pl.kidx, st), "GEMM launch");
@@ -279,9 +280,10 @@ cf_status parse_nodes(const cf_node* nodes, int n, int64_t M, int64_t N, cf_dtyp
       case CF_N_BIAS: return 1;
       case CF_N_RESIDUAL: return 2;
       case CF_N_LAYERNORM: case CF_N_RMSNORM: return 3;
-      case CF_N_GELU: case CF_N_GELU_TANH: case CF_N_RELU: return 4;
-      case CF_N_STORE: return 5;
-      case CF_N_ROWAMAX_QUANT: return 6;
+      case CF_N_GELU: case CF_N_GELU_TANH: case CF_N_RELU: case CF_N_SOFTCAP: return 4;
+      case CF_N_SOFTMAX: return 5;
+      case CF_N_STORE: return 6;
+      case CF_N_ROWAMAX_QUANT: return 7;
       default: return -1;
     }
   };
@@ -291,8 +293,9 @@ cf_status parse_nodes(const cf_node* nodes, int n, int64_t M, int64_t N, cf_dtyp
     const int r = rank(d.kind);
     if (r < 0) return fail(CF_ERR_UNSUPPORTED, "node %d: kind %d is not in the fused vocabulary", i, (int)d.kind);
     if (r <= last)
-      return fail(CF_ERR_UNSUPPORTED, "node %d: kind %d out of order (grammar: SCALE BIAS RESIDUAL NORM ACT STORE QUANT)",
-                  i, (int)d.kind);
+      return fail(CF_ERR_UNSUPPORTED,
+                  "node %d: kind %d out of order (grammar: SCALE BIAS RESIDUAL NORM ACT SOFTMAX STORE QUANT)", i,
+                  (int)d.kind);
     last = r;
     cf_status s = CF_OK;
     switch (d.kind) {
@@ -322,6 +325,15 @@ cf_status parse_nodes(const cf_node* nodes, int n, int64_t M, int64_t N, cf_dtyp
       case CF_N_GELU: e.act = ACT_GELU; break;
       case CF_N_GELU_TANH: e.act = ACT_GELU_TANH; break;
       case CF_N_RELU: e.act = ACT_RELU; break;
+      case CF_N_SOFTCAP:
+        if (!(d.f0 > 0.0f) || !std::isfinite(d.f0)) return fail(CF_ERR_SHAPE, "SOFTCAP cap must be finite and > 0");
+        e.act = ACT_SOFTCAP;
+        e.softcap = d.f0;
+        break;
+      case CF_N_SOFTMAX:
+        if (e.norm != NORM_NONE) return fail(CF_ERR_UNSUPPORTED, "SOFTMAX after a NORM is not in the fused vocabulary");
+        e.softmax = 1;
+        break;
       case CF_N_STORE:
         if (d.dtype != CF_F32 && d.dtype != CF_BF16) return fail(CF_ERR_DTYPE, "STORE dtype must be F32 or BF16");
         if ((s = check_matrix("STORE", d.out, M, N, d.ld, d.dtype, true)) != CF_OK) return s;
@@ -376,7 +388,7 @@ cf_status rows_common(int64_t M, int64_t N, int64_t K, cf_dtype in, const void* 
   if (wl != CF_LAYOUT_KN && wl != CF_LAYOUT_NK) return fail(CF_ERR_UNSUPPORTED, "unknown weight layout");
   if ((s = check_matrix("X", X, M, K, ldx, in, true)) != CF_OK) return s;
   if ((s = check_matrix("W", W, 1, wl == CF_LAYOUT_NK ? K : N, ldw, in, true)) != CF_OK) return s;
-  const bool need_rows = epi.norm != NORM_NONE || epi.quant;
+  const bool need_rows = epi.norm != NORM_NONE || epi.quant || epi.softmax;
   // The plain epilogue only applies alpha and bias; anything else runs the
   // row-subgraph epilogue.
   const int epi_kind = (need_rows || epi.R || epi.act != ACT_NONE) ? 1 : 0;

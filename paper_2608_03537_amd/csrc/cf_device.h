@@ -177,11 +177,19 @@ __device__ __forceinline__ void load4<float>(const float* p, float (&v)[4]) {
   v[0] = u[0]; v[1] = u[1]; v[2] = u[2]; v[3] = u[3];
 }
 
-__device__ __forceinline__ float apply_act(int act, float x) {
+// tanh(z) = sign(z) (1 - t) / (1 + t), t = exp(-2 |z|): no overflow for any z;
+// near 0 the absolute error stays at the fp32 rounding of 1 - t (~6e-8).
+__device__ __forceinline__ float tanh_exp(float z) {
+  const float t = __builtin_amdgcn_exp2f(-2.8853900817779268f * fabsf(z));   // 2 log2(e)
+  return copysignf((1.0f - t) * __builtin_amdgcn_rcpf(1.0f + t), z);
+}
+
+__device__ __forceinline__ float apply_act(int act, float x, float cap) {
   switch (act) {
     case ACT_GELU: return gelu_erf(x);
     case ACT_GELU_TANH: return gelu_tanh(x);
     case ACT_RELU: return x > 0.0f ? x : 0.0f;
+    case ACT_SOFTCAP: return cap * tanh_exp(x / cap);
     default: return x;
   }
 }

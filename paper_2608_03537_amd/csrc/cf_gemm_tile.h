@@ -508,15 +508,22 @@ __device__ __forceinline__ unsigned long long rec_word(float v, unsigned tag) {
   return ((unsigned long long)tag << 32) | __float_as_uint(v);
 }
 
-// Publishes (a, b) (MAX: a only) of this workgroup's rows, then reads every
-// peer's records of the lane's rows, peer 0 first, until all carry `tag`, and
-// merges them in that order: MAX -> a = max over peers; otherwise (a, b) =
-// (mean, M2) of tiles of TN columns, merged pairwise (Chan, Golub, LeVeque).
-// Every workgroup merges in the same order, so all get bit-identical values.
-template <class S, bool MAX>
+// How cluster_exchange merges the peers' per-row values.
+enum MergeKind {
+  MERGE_CHAN = 0,      // (a, b) = (mean, M2) of TN columns: pairwise update (Chan, Golub, LeVeque)
+  MERGE_MAX = 1,       // a = max over peers
+  MERGE_SOFTMAX = 2    // (a, b) = (max, sum of exp(x - max)): b rescaled to the common max
+};
+
+// Publishes (a, b) (MERGE_MAX: a only) of this workgroup's rows, then reads
+// every peer's records of the lane's rows, peer 0 first, until all carry
+// `tag`, and merges them in that order.  Every workgroup merges in the same
+// order, so all get bit-identical values.
+template <class S, int MERGE>
 __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int stage, int slot, int c, unsigned tag,
                                                  float (&a)[S::BM], float (&b)[S::BM], int lane, int wm, int wn) {
   static_assert(S::TM <= kRecRows, "records hold kRecRows rows per peer");
+  constexpr bool MAX = MERGE == MERGE_MAX;
   constexpr int NV = MAX ? 1 : 2;
   constexpr int PB = 4;   // peers read per batch
   unsigned long long* rec = reinterpret_cast<unsigned long long*>(p.ws_part) + stage * kRecStageWords +
@@ -533,7 +540,10 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
   const int cn = p.cn;
   float n_acc[S::BM], mu[S::BM], sq[S::BM];
 #pragma unroll
-  for (int bm = 0; bm < S::BM; ++bm) n_acc[bm] = mu[bm] = sq[bm] = 0.0f;
+  for (int bm = 0; bm < S::BM; ++bm) {
+    n_acc[bm] = mu[bm] = sq[bm] = 0.0f;
+    if (MERGE == MERGE_SOFTMAX) mu[bm] = -INFINITY;
+  }
   for (int c0 = 0; c0 < cn; c0 += PB) {
     unsigned long long w[S::BM][PB][NV];
     for (int spins = 0;; ++spins) {
@@ -565,6 +575,14 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
         const float va = __uint_as_float((unsigned)w[bm][j][0]);
         if constexpr (MAX) {
           mu[bm] = fmaxf(mu[bm], va);
+        } else if constexpr (MERGE == MERGE_SOFTMAX) {
+          // sum_c s_c exp(m_c - m) with m the running maximum; exp2 of a
+          // non-positive argument (exp2(-inf) = 0 for the first record)
+          const float vb = __uint_as_float((unsigned)w[bm][j][NV - 1]);
+          const float mn = fmaxf(mu[bm], va);
+          sq[bm] = sq[bm] * __builtin_amdgcn_exp2f((mu[bm] - mn) * 1.4426950408889634f) +
+                   vb * __builtin_amdgcn_exp2f((va - mn) * 1.4426950408889634f);
+          mu[bm] = mn;
         } else {
           const float vb = __uint_as_float((unsigned)w[bm][j][NV - 1]);
           const float nb = (float)S::TN, nn = n_acc[bm] + nb;
@@ -902,7 +920,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     }
 
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
-      cluster_exchange<S, false>(p, 0, slot, c, tag, mean, m2, lane, wm, wn);
+      cluster_exchange<S, MERGE_CHAN>(p, 0, slot, c, tag, mean, m2, lane, wm, wn);
       exchanged = true;
     }
 
@@ -964,7 +982,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
       float z[S::BM];
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) z[bm] = 0.0f;
-      cluster_exchange<S, false>(p, 0, slot, c, tag, z, s, lane, wm, wn);
+      cluster_exchange<S, MERGE_CHAN>(p, 0, slot, c, tag, z, s, lane, wm, wn);
       exchanged = true;
     }
     const float invN = 1.0f / (float)N;
@@ -991,7 +1009,67 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
 #pragma unroll
       for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) x[bm][bn][i] = apply_act(e.act, x[bm][bn][i]);
+        for (int i = 0; i < 16; ++i) x[bm][bn][i] = apply_act(e.act, x[bm][bn][i], e.softcap);
+  }
+  // ---- stage 3b: row softmax.  Local row maximum, e = exp(x - max_local) and
+  // its sum; across workgroups the (max, sum) pairs merge with the sums
+  // rescaled to the common maximum (one exchange); then x = e * exp(max_local
+  // - max) / sum.  Padding columns of a ragged tile take no part.
+  if (e.softmax) {
+    const bool full_n = n0 + S::TN <= N;
+    float mx[S::BM], sm[S::BM];
+#pragma unroll
+    for (int bm = 0; bm < S::BM; ++bm) {
+      float t = -INFINITY;
+#pragma unroll
+      for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          if (full_n || ncol(bn, g) < N)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) t = fmaxf(t, x[bm][bn][4 * g + q]);
+      mx[bm] = t;
+    }
+    wg_row_reduce<S, true>(mx, red, lane, wm, wn);
+#pragma unroll
+    for (int bm = 0; bm < S::BM; ++bm) {
+      const float nl = -mx[bm] * 1.4426950408889634f;
+      float t = 0.0f;
+#pragma unroll
+      for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const bool v = full_n || ncol(bn, g) < N;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float ev = v ? __builtin_amdgcn_exp2f(fmaf(x[bm][bn][4 * g + q], 1.4426950408889634f, nl)) : 0.0f;
+            x[bm][bn][4 * g + q] = ev;
+            t += ev;
+          }
+        }
+      sm[bm] = t;
+    }
+    wg_row_reduce<S, false>(sm, red, lane, wm, wn);
+    float f[S::BM];
+    if (p.mode == ROWS_CLUSTER && p.cn > 1) {
+      float mg[S::BM];
+#pragma unroll
+      for (int bm = 0; bm < S::BM; ++bm) mg[bm] = mx[bm];
+      cluster_exchange<S, MERGE_SOFTMAX>(p, 0, slot, c, tag, mg, sm, lane, wm, wn);
+      exchanged = true;
+#pragma unroll
+      for (int bm = 0; bm < S::BM; ++bm)
+        f[bm] = __builtin_amdgcn_exp2f((mx[bm] - mg[bm]) * 1.4426950408889634f) / sm[bm];
+    } else {
+#pragma unroll
+      for (int bm = 0; bm < S::BM; ++bm) f[bm] = 1.0f / sm[bm];
+    }
+#pragma unroll
+    for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+      for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) x[bm][bn][i] *= f[bm];
   }
   if (e.Y) {
     char* Yb = reinterpret_cast<char*>(e.Y) + (int64_t)bz * e.sy * (e.y_f32 ? 4 : 2);
@@ -1016,7 +1094,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     }
     wg_row_reduce<S, true>(a, red, lane, wm, wn);
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
-      cluster_exchange<S, true>(p, exchanged ? 1 : 0, slot, c, tag, a, a, lane, wm, wn);
+      cluster_exchange<S, MERGE_MAX>(p, exchanged ? 1 : 0, slot, c, tag, a, a, lane, wm, wn);
       exchanged = true;
     }
 #pragma unroll

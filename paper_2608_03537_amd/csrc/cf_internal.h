@@ -7,14 +7,15 @@
 namespace cf {
 
 enum NormKind { NORM_NONE = 0, NORM_LAYER = 1, NORM_RMS = 2 };
-enum ActKind { ACT_NONE = 0, ACT_GELU = 1, ACT_GELU_TANH = 2, ACT_RELU = 3 };
+enum ActKind { ACT_NONE = 0, ACT_GELU = 1, ACT_GELU_TANH = 2, ACT_RELU = 3, ACT_SOFTCAP = 4 };
 
 // Epilogue "program": the stage chain of the Stage-Stream model in a fixed
 // order.  Every field is uniform across the launch, so the kernel branches on
 // it with scalar branches.
 //   stage 1: x = alpha * acc + bias[n] + R[m, n]
 //   stage 2: optional row reduction (LayerNorm / RMSNorm) and its PostOp
-//   stage 3: optional activation
+//   stage 3: optional activation, then optional row softmax (a reduction:
+//            row max and the sum of exp(x - max))
 //   store  : Y[m, n] = x (bf16 or fp32)
 //   stage 4: optional row amax -> s[m] = amax / qmax, Q[m, n] = e4m3(x / s)
 struct RowEpi {
@@ -24,7 +25,8 @@ struct RowEpi {
   int r_f32;                                // row kernel: residual is fp32
   int norm;
   const float* gamma; const float* beta; float eps;
-  int act;
+  int act; float softcap;                   // ACT_SOFTCAP: cap
+  int softmax;
   void* Y; int64_t ldy; int64_t sy; int y_f32;
   int quant; float qmax; float* s_out; uint8_t* q_out; int64_t ldq;
 };

@@ -26,8 +26,10 @@ __device__ __forceinline__ float wave_max(float v) {
 
 // VPL = groups of 4 consecutive columns per lane; a row of up to 256*VPL.
 // Lane l holds columns 256*j + 4*l + (0..3), j < VPL: each j is one fully
-// coalesced 1 KB (fp32) or 512 B (bf16) access by the wave.
-template <int VPL>
+// coalesced 1 KB (fp32) or 512 B (bf16) access by the wave.  SM: the node
+// list has a SOFTMAX stage (compiled separately: its exp chain would raise
+// the register use of every other list).
+template <int VPL, bool SM>
 __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
   const int lane = threadIdx.x & 63;
   const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -172,7 +174,31 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
 #pragma unroll
     for (int j = 0; j < VPL; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[j][q] = apply_act(e.act, v[j][q]);
+      for (int q = 0; q < 4; ++q) v[j][q] = apply_act(e.act, v[j][q], e.softcap);
+  }
+  if (SM) {   // row softmax of the (activated) values
+    float mx = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < VPL; ++j)
+      if (val[j])
+#pragma unroll
+        for (int q = 0; q < 4; ++q) mx = fmaxf(mx, v[j][q]);
+    mx = wave_max(mx);
+    const float nl = -mx * 1.4426950408889634f;
+    float s = 0.0f;
+#pragma unroll
+    for (int j = 0; j < VPL; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float t = val[j] ? __builtin_amdgcn_exp2f(fmaf(v[j][q], 1.4426950408889634f, nl)) : 0.0f;
+        v[j][q] = t;
+        s += t;
+      }
+    const float inv = 1.0f / wave_sum(s);
+#pragma unroll
+    for (int j = 0; j < VPL; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[j][q] *= inv;
   }
   if (e.Y) {
 #pragma unroll
@@ -208,13 +234,20 @@ hipError_t launch_row_kernel(const RowKernelParams& p, hipStream_t st) {
   if (p.M <= 0) return hipSuccess;
   const dim3 grid((unsigned)((p.M + 3) / 4)), block(256);
   const int vpl = (p.N + 255) / 256;
-  if (vpl <= 1) hipLaunchKernelGGL(row_kernel<1>, grid, block, 0, st, p);
-  else if (vpl <= 2) hipLaunchKernelGGL(row_kernel<2>, grid, block, 0, st, p);
-  else if (vpl <= 4) hipLaunchKernelGGL(row_kernel<4>, grid, block, 0, st, p);
-  else if (vpl <= 8) hipLaunchKernelGGL(row_kernel<8>, grid, block, 0, st, p);
-  else if (vpl <= 16) hipLaunchKernelGGL(row_kernel<16>, grid, block, 0, st, p);
-  else if (vpl <= 32) hipLaunchKernelGGL(row_kernel<32>, grid, block, 0, st, p);
+  const bool sm = p.epi.softmax != 0;
+#define CF_ROW_LAUNCH(V)                                                                    \
+  do {                                                                                      \
+    if (sm) hipLaunchKernelGGL((row_kernel<V, true>), grid, block, 0, st, p);               \
+    else hipLaunchKernelGGL((row_kernel<V, false>), grid, block, 0, st, p);                 \
+  } while (0)
+  if (vpl <= 1) CF_ROW_LAUNCH(1);
+  else if (vpl <= 2) CF_ROW_LAUNCH(2);
+  else if (vpl <= 4) CF_ROW_LAUNCH(4);
+  else if (vpl <= 8) CF_ROW_LAUNCH(8);
+  else if (vpl <= 16) CF_ROW_LAUNCH(16);
+  else if (vpl <= 32) CF_ROW_LAUNCH(32);
   else return hipErrorInvalidValue;
+#undef CF_ROW_LAUNCH
   return hipGetLastError();
 }
 

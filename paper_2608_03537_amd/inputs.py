@@ -32,6 +32,7 @@ WL_BERT_POSTNORM = 2
 WL_LN_GELU_AMAX = 3
 WL_FFN_B2B = 4
 WL_ATTENTION = 5
+WL_MSTS = 6
 WL_CUSTOM = 99
 
 
@@ -144,6 +145,15 @@ def ln_gelu_amax_inputs(seed=0, M=16384, K=4096, N=4096) -> PostnormInputs:
     W ~ N(0, 1/K); b ~ N(0, 0.02^2); gamma = 1, beta = 0 (not passed)."""
     return postnorm_inputs(M, K, N, "bf16", seed, WL_LN_GELU_AMAX,
                            with_affine=False)
+
+
+def msts_inputs(seed=0, M=16384, K=768, N=1024, dtype="bf16", alpha=8.0, cap=10.0) -> PostnormInputs:
+    """Scale -> tanh softcap -> softmax on a GEMM output: X ~ N(0,1);
+    W ~ N(0, 1/K); b ~ N(0, 0.02^2); alpha = 8 spreads the logits to about
+    +-30 so that the softcap (cap 10) saturates part of them."""
+    inp = postnorm_inputs(M, K, N, dtype, seed, WL_MSTS, with_residual=False, with_affine=False, alpha=alpha)
+    inp.meta["cap"] = cap
+    return inp
 
 
 @dataclass

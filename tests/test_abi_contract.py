@@ -146,6 +146,21 @@ def test_subgraph_grammar():
     assert cf.STATUS[cf.cf_gemm_subgraph(a, None, 0, None)] == "CF_ERR_ALIGN"
 
 
+def test_subgraph_grammar_softcap_softmax():
+    store = dict(kind=cf.CF_N_STORE, out=Y, ld=256, dtype=cf.CF_BF16)
+    msts = [dict(kind=cf.CF_N_SCALE, f0=0.5), dict(kind=cf.CF_N_SOFTCAP, f0=30.0), dict(kind=cf.CF_N_SOFTMAX), store]
+    a, keep = _sg(msts, M=0)
+    assert cf.cf_gemm_subgraph(a, None, 0, None) == 0
+    for cap in (0.0, -1.0, float("inf"), float("nan")):
+        a, keep = _sg([dict(kind=cf.CF_N_SOFTCAP, f0=cap), store])
+        assert cf.STATUS[cf.cf_gemm_subgraph(a, None, 0, None)] == "CF_ERR_SHAPE", cap
+    for bad in ([dict(kind=cf.CF_N_LAYERNORM, f0=1e-5), dict(kind=cf.CF_N_SOFTMAX), store],
+                [dict(kind=cf.CF_N_SOFTMAX), dict(kind=cf.CF_N_GELU), store],
+                [dict(kind=cf.CF_N_SOFTCAP, f0=30.0), dict(kind=cf.CF_N_GELU), store]):
+        a, keep = _sg(bad)
+        assert cf.STATUS[cf.cf_gemm_subgraph(a, None, 0, None)] == "CF_ERR_UNSUPPORTED"
+
+
 def test_gemm_and_rowop_validation():
     st = cf.STATUS
     assert cf.cf_gemm(1, 0, 256, 128, cf.CF_BF16, cf.CF_BF16, A, 128, 0, B, 128, 0, cf.CF_LAYOUT_NK,

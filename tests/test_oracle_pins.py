@@ -239,6 +239,45 @@ def test_softmax_rows_sum_and_shift():
     np.testing.assert_allclose(O.softmax_rows(s + 123.25), p, rtol=1e-12, atol=1e-300)
 
 
+# ---------------------------------------------------------------- softcap / MSTS
+def test_tanh_softcap_closed_forms():
+    cap = 7.5
+    # tanh(atanh(1/2)) = 1/2 (math.atanh, not the oracle's np.tanh)
+    np.testing.assert_allclose(O.tanh_softcap(np.array([cap * math.atanh(0.5)]), cap), [cap / 2], rtol=1e-15)
+    # tanh(1) = (e^2 - 1) / (e^2 + 1)
+    e2 = math.exp(2.0)
+    np.testing.assert_allclose(O.tanh_softcap(np.array([cap]), cap), [cap * (e2 - 1) / (e2 + 1)], rtol=1e-15)
+    x = np.random.default_rng(21).standard_normal(1000) * 40
+    y = O.tanh_softcap(x, cap)
+    np.testing.assert_array_equal(O.tanh_softcap(-x, cap), -y)                   # odd
+    assert np.all(np.abs(y) <= cap) and np.all(np.abs(y) <= np.abs(x))            # bounded, contracting
+    z = x * 1e-3 / cap                                                            # |x| << cap: tanh series
+    series = z - z ** 3 / 3 + 2 * z ** 5 / 15 - 17 * z ** 7 / 315 + 62 * z ** 9 / 2835
+    np.testing.assert_allclose(O.tanh_softcap(z * cap, cap), cap * series, rtol=5e-14, atol=1e-300)
+
+
+def test_msts_by_hand_and_limits():
+    # 2 x 3 logits by hand: x = alpha X.W + b, y = cap tanh(x / cap), softmax of each row
+    X = np.array([[1.0, -2.0], [0.5, 0.25]])
+    W = np.array([[1.0, 0.0, 2.0], [0.5, -1.0, 0.0]])
+    b = np.array([0.1, -0.2, 0.3])
+    alpha, cap = 3.0, 2.5
+    want = []
+    for i in range(2):
+        logits = [alpha * (X[i, 0] * W[0, j] + X[i, 1] * W[1, j]) + b[j] for j in range(3)]
+        y = [cap * math.tanh(v / cap) for v in logits]
+        m = max(y)
+        e = [math.exp(v - m) for v in y]
+        want.append([v / math.fsum(e) for v in e])
+    np.testing.assert_allclose(O.msts(X, W, alpha, b, cap), np.array(want), rtol=1e-14)
+    # rows sum to 1; a very large cap leaves the plain softmax of the logits
+    rng = np.random.default_rng(22)
+    X, W = rng.standard_normal((8, 16)), rng.standard_normal((16, 40)) / 4
+    p = O.msts(X, W, 2.0, None, 1e6)
+    np.testing.assert_allclose(p.sum(axis=1), 1.0, atol=1e-14)
+    np.testing.assert_allclose(p, O.softmax_rows(2.0 * (X @ W)), rtol=1e-9)
+
+
 def _attn_mp(Q, K, V, scale):
     Lq, Lk, dv = Q.shape[0], K.shape[0], V.shape[1]
     out = np.zeros((Lq, dv))

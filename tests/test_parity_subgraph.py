@@ -193,3 +193,67 @@ def test_subgraph_without_reduction(act, dtype):
     x = O.bias_residual(O.matmul(inp.X, inp.W), inp.bias, inp.R, alpha=0.5)
     ref = {"none": x, "gelu": O.gelu_erf(x), "relu": O.relu(x)}[act]
     assert_close_f32(host(Y), ref, f"no-reduction {act} {dtype}")
+
+
+# ---------------------------------------------------------------- MSTS: scale -> softcap -> softmax
+def run_msts(inp, path=0, out_f32=False, layout="nk"):
+    X = dev(inp.X, inp.dtype)
+    W = dev(I.lay_out_weight(inp.W, layout), inp.dtype)
+    Y = torch.empty((inp.M, inp.N), dtype=torch.float32 if out_f32 else torch.bfloat16, device="cuda")
+    spec = [dict(kind=cf.CF_N_SCALE, f0=inp.alpha)]
+    if inp.bias is not None:
+        spec.append(dict(kind=cf.CF_N_BIAS, v0=dev(inp.bias, "f32")))
+    spec += [dict(kind=cf.CF_N_SOFTCAP, f0=inp.meta["cap"]), dict(kind=cf.CF_N_SOFTMAX),
+             dict(kind=cf.CF_N_STORE, out=Y, ld=inp.N, dtype=cf.CF_F32 if out_f32 else cf.CF_BF16)]
+    cf.gemm_subgraph(X, W, spec, w_layout=cf.CF_LAYOUT_NK if layout == "nk" else cf.CF_LAYOUT_KN, path=path)
+    torch.cuda.synchronize()
+    return host(Y)
+
+
+def msts_ref(inp):
+    return O.msts(inp.X, inp.W, inp.alpha, inp.bias, inp.meta["cap"])
+
+
+@pytest.mark.parametrize("path", [1, 2, 3])
+@pytest.mark.parametrize("M,K,N", [(200, 128, 512), (77, 192, 384), (130, 64, 320), (64, 256, 1024)])
+def test_msts_small(M, K, N, path):
+    inp = I.msts_inputs(seed=12, M=M, K=K, N=N)
+    if path == 1 and N > 768:
+        pytest.skip("whole-row path covers N <= 768")
+    if path == 2 and not any(N % t == 0 for t in (256, 192, 128)):
+        with pytest.raises(cf.CfError, match="UNSUPPORTED"):
+            run_msts(inp, path)
+        return
+    ref = msts_ref(inp)
+    got = run_msts(inp, path)
+    assert_close_bf16(got, ref, f"MSTS {M}x{K}x{N} path {path}")
+    np.testing.assert_allclose(got.astype(np.float64).sum(axis=1), 1.0, atol=0.02)
+
+
+@pytest.mark.parametrize("path", [0, 3])
+def test_msts_fp32_out_and_kn_layout(path):
+    inp = I.msts_inputs(seed=13, M=150, K=128, N=512, dtype="f32")
+    ref = msts_ref(inp)
+    assert_close_f32(run_msts(inp, path, out_f32=True, layout="kn"), ref, f"MSTS fp32 kn path {path}")
+
+
+def test_msts_full_size_sampled_rows():
+    inp = I.msts_inputs()
+    got = run_msts(inp)
+    rows = np.unique(np.concatenate([[0, 1, 127, 128, inp.M - 1],
+                                     np.random.default_rng(1).choice(inp.M, 27, replace=False)]))
+    ref = O.msts(inp.X[rows], inp.W, inp.alpha, inp.bias, inp.meta["cap"])
+    assert_close_bf16(got[rows], ref, "MSTS full size")
+
+
+def test_rowop_msts_grammar():
+    # the unfused row operator runs the same node list on a materialised P
+    inp = I.msts_inputs(seed=14, M=96, K=128, N=640, dtype="f32")
+    P = dev(O.matmul(inp.X, inp.W), "f32")
+    Y = torch.empty((inp.M, inp.N), dtype=torch.float32, device="cuda")
+    spec = [dict(kind=cf.CF_N_SCALE, f0=inp.alpha), dict(kind=cf.CF_N_BIAS, v0=dev(inp.bias, "f32")),
+            dict(kind=cf.CF_N_SOFTCAP, f0=inp.meta["cap"]), dict(kind=cf.CF_N_SOFTMAX),
+            dict(kind=cf.CF_N_STORE, out=Y, ld=inp.N, dtype=cf.CF_F32)]
+    cf.rowop(P, spec)
+    torch.cuda.synchronize()
+    assert_close_f32(host(Y), msts_ref(inp), "rowop MSTS")
