@@ -257,6 +257,56 @@ def workload_attention(torch, cf, I, O, dev):
                      shape={"B": B, "H": H, "Lq": L, "Lk": Lk, "d": d, "dtype": "bf16"})
 
 
+def stage_stream_sweep(torch, cf, I, O, dev):
+    """The paper's other Stage-Stream workloads over a batch sweep (K = N = 1024,
+    bf16): MBR (RMSNorm), MBLR (bias + LayerNorm + ReLU) and MSTS (scale, tanh
+    softcap 10, softmax), fused vs cf_gemm + cf_rowop on the same node list."""
+    K = N = 1024
+    bf = torch.bfloat16
+    out = {}
+    for M in (2048, 8192, 32768):
+        inp = I.msts_inputs(seed=0, M=M, K=K, N=N)
+        X = tensor(torch, inp.X, bf, dev)
+        W = tensor(torch, I.lay_out_weight(inp.W, "nk"), bf, dev)
+        b = tensor(torch, inp.bias, torch.float32, dev)
+        gam = tensor(torch, 1.0 + 0.02 * np.random.default_rng(3).standard_normal(N), torch.float32, dev)
+        Y = torch.empty((M, N), dtype=bf, device=dev)
+        P = torch.empty((M, N), dtype=bf, device=dev)
+        store = dict(kind=cf.CF_N_STORE, out=Y, ld=N, dtype=cf.CF_BF16)
+        lists = {
+            "MBR": [dict(kind=cf.CF_N_RMSNORM, v0=gam, f0=1e-5), store],
+            "MBLR": [dict(kind=cf.CF_N_BIAS, v0=b), dict(kind=cf.CF_N_LAYERNORM, f0=1e-5),
+                     dict(kind=cf.CF_N_RELU), store],
+            "MSTS": [dict(kind=cf.CF_N_SCALE, f0=inp.alpha), dict(kind=cf.CF_N_SOFTCAP, f0=inp.meta["cap"]),
+                     dict(kind=cf.CF_N_SOFTMAX), store],
+        }
+        for name, spec in lists.items():
+            fused = time_steps(torch, [lambda spec=spec: cf.gemm_subgraph(X, W, spec)], 20, 3)
+            if M == 8192:   # spot check of the fused output on three rows
+                rows = np.array([0, 4097, M - 1])
+                xw = O.matmul(inp.X[rows], inp.W)
+                g64 = gam.cpu().numpy().astype(np.float64)
+                if name == "MBR":
+                    ref = O.rmsnorm(xw, g64, 1e-5)
+                elif name == "MBLR":
+                    ref = O.relu(O.layernorm(O.bias_residual(xw, inp.bias), eps=1e-5))
+                else:
+                    ref = O.msts(inp.X[rows], inp.W, inp.alpha, None, inp.meta["cap"])
+                got = Y[torch.from_numpy(rows).to(dev)].float().cpu().numpy()
+                out[f"{name}_parity"] = verdict(float(np.max(np.abs(got - ref))), 2e-2)
+
+            def unf(spec=spec):
+                cf.gemm(X, W, out=P)
+                cf.rowop(P, spec)
+            unfused = time_steps(torch, [unf], 20, 3)
+            out[f"{name}_M{M}"] = {"fused_us": round(fused * 1e3, 2), "unfused_us": round(unfused * 1e3, 2),
+                                   "speedup_vs_unfused": round(unfused / fused, 3),
+                                   "tflops": round(2.0 * M * N * K / (fused * 1e-3) / 1e12, 1)}
+        del X, W, Y, P
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -365,7 +415,8 @@ def main():
     if not args.only_main:
         wl = {}
         for name, fn in [("postnorm_tiny_fp32", workload_tiny), ("ln_gelu_amax_fp8", workload_chain),
-                         ("ffn_b2b", workload_ffn), ("attention_b2b", workload_attention)]:
+                         ("ffn_b2b", workload_ffn), ("attention_b2b", workload_attention),
+                         ("stage_stream_sweep", stage_stream_sweep)]:
             wl[name] = fn(torch, cf, I, O, dev)
             torch.cuda.empty_cache()
         out["workloads"] = wl

@@ -1003,13 +1003,28 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
   }
 
   // ---- stage 3: activation and store
-  if (e.act != ACT_NONE) {
+  // One straight loop per activation kind (the kind is uniform): a per-element
+  // switch would put every kind's code on the path of every element.
+  auto act_all = [&](auto f) {   // one 16-value block at a time (bounds the live temporaries)
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-      for (int bn = 0; bn < S::BN; ++bn)
+      for (int bn = 0; bn < S::BN; ++bn) {
 #pragma unroll
-        for (int i = 0; i < 16; ++i) x[bm][bn][i] = apply_act(e.act, x[bm][bn][i], e.softcap);
+        for (int i = 0; i < 16; ++i) x[bm][bn][i] = f(x[bm][bn][i]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+  };
+  switch (e.act) {
+    case ACT_GELU: act_all([](float v) { return gelu_erf(v); }); break;
+    case ACT_GELU_TANH: act_all([](float v) { return gelu_tanh(v); }); break;
+    case ACT_RELU: act_all([](float v) { return v > 0.0f ? v : 0.0f; }); break;
+    case ACT_SOFTCAP: {
+      const float cap = e.softcap, inv = 1.0f / cap;
+      act_all([=](float v) { return cap * tanh_exp(v * inv); });
+      break;
+    }
+    default: break;
   }
   // ---- stage 3b: row softmax.  Local row maximum, e = exp(x - max_local) and
   // its sum; across workgroups the (max, sum) pairs merge with the sums
