@@ -1,21 +1,22 @@
-// Back-to-back GEMM kernels for gfx950 (Sec. IV, Eq. 2: P = X W1, S = F(P),
-// O = S W2) with the intermediate S kept in registers.
+// Back-to-back attention kernel for gfx950 (Sec. IV, Eq. 2 with F = scaled
+// softmax: P = softmax(scale Q K^T), O = P V) with the intermediate P kept in
+// registers.
 //
-// Register hand-off between the two products.  GEMM 1 is computed in the
-// transposed form P^T = W1^T X^T, so in each 32x32 accumulator block a lane
-// holds one row m of P and 16 of its columns n1: rows 8*(i/4) + 4*g + i%4
-// of the block for element i, g = lane/32.  GEMM 2 (O^T = W2^T S^T) consumes
-// S^T as its B operand, where lane group g supplies 8 values of the
-// contraction index per MFMA step.  The k order inside a step is free as long
-// as both operands use the same one, so step s of block b is DEFINED to use
+// Register hand-off between the two products.  The first product is computed
+// in the transposed form S^T = K Q^T, so in each 32x32 accumulator block a
+// lane holds one query row m and 16 of its key columns: rows
+// 8*(i/4) + 4*g + i%4 of the block for element i, g = lane/32.  The second
+// product (O^T = V^T P^T) consumes P^T as its B operand, where lane group g
+// supplies 8 values of the contraction index per MFMA step; step s takes
+// accumulator elements 8s .. 8s+7 of the lane, so P never leaves the
+// registers of the wave that produced it (the register-resident S_tile of
+// Sec. IV-A).  The k order inside a step is free as long as both operands use
+// the same one: step s of block b is DEFINED to use
 //     n1(s, g, j) = 32 b + 16 s + 8 (j/4) + 4 g + j%4,   j = 0..7,
-// which is exactly accumulator elements 8s .. 8s+7 of the lane.  S therefore
-// never leaves the registers of the wave that produced it (the register-
-// resident S_tile of Sec. IV-A); only the W2 operand is read from LDS, as two
-// 8-byte pieces per lane in that same order.
+// and the V operand is read from LDS as two 8-byte pieces per lane in that
+// same order.
 //
-// Each wave owns 32 complete rows (all N1 columns of P, all N2 columns of O),
-// so the FFN's LayerNorm and the attention's softmax statistics need only
+// Each wave owns 32 complete query rows, so the softmax statistics need only
 // the lane pair (l, l^32) — no cross-wave or cross-workgroup exchange.
 #include "cf_gemm_tile.h"
 #include "comfuse.h"
@@ -45,328 +46,6 @@ __device__ __forceinline__ u32x4_t pack_step(const f32x16_t& v, int s) {
 
 __device__ __forceinline__ float lane_pair_sum(float v) { return v + __shfl_xor(v, 32); }
 __device__ __forceinline__ float lane_pair_max(float v) { return fmaxf(v, __shfl_xor(v, 32)); }
-
-// ===========================================================================
-// FFN:  O = GELU(X W1 + b1) W2 (+ b2 + R, LayerNorm), K = N2 = D.
-// 4 waves x 32 rows = 128 rows per workgroup.  The hidden dimension is swept
-// in chunks of HC = 32 columns; for chunk k a wave computes its 32 x 32 block
-// of P^T = W1^T X^T (the X^T fragments of its rows stay in registers for the
-// whole sweep), adds b1, applies GELU, packs S as the second product's B
-// fragment and accumulates O^T += W2^T S^T (the partial-sum identity
-// O = sum_k S^(k) W2^(k) of Sec. IV-A, accumulated in registers).  S never
-// leaves the registers of the wave that produced it.
-// Three-stage software pipeline (the PingPong of Sec. III-C inside one wave):
-// iteration c issues the MFMAs of chunk c+1's first product and of chunk
-// c-1's second product, and between consecutive MFMAs one stage of chunk c's
-// GELU for four independent elements (gelu_stage), so the matrix pipe and the
-// vector ALU work together without dependency stalls.  W1^T chunks (32 rows,
-// all K) and W2^T chunks (D rows, 32 hidden) stream through two two-slot LDS
-// rings (Sec. IV-B) one chunk ahead.  The residual, when it is X itself, is
-// taken from the X fragments through the lane pair.
-// ===========================================================================
-template <int N1, int D>
-struct FfnShape {
-  static constexpr int TM = 128, NT = 256, HC = 32;
-  static constexpr int NC = N1 / HC;                 // hidden chunks
-  static constexpr int KS1 = D / 16;                 // MFMA steps of GEMM 1 (= X fragments)
-  static constexpr int B2 = D / 32;                  // output blocks
-  static constexpr int RB1 = D * 2;                  // bytes of one W1^T row (all of K)
-  static constexpr int CPR1 = RB1 / 16;              // 16-byte chunks per W1^T row
-  static constexpr int W1C = HC * RB1, W2C = D * HC * 2;
-  static constexpr int RING1 = 2 * W1C, RING = RING1 + 2 * W2C;
-  static constexpr int VEC = (N1 + 3 * D) * 4;       // b1, b2, gamma, beta
-  static constexpr int LDS_STORE = TM * (D * 2 + 8);
-  static constexpr int LDS = (RING > LDS_STORE ? RING : LDS_STORE) + VEC;
-  static constexpr int I1 = W1C / 4096, I2 = W2C / 4096;   // wave-wide loads per wave per chunk
-  static constexpr int NM1 = KS1, NM2 = 2 * B2;      // MFMAs per chunk of GEMM 1 / GEMM 2
-  static constexpr int GSLOTS = 32;                  // GELU work: 4 groups x 8 stages
-  static_assert(N1 % HC == 0 && D % 64 == 0 && W1C % 4096 == 0 && W2C % 4096 == 0, "shape");
-  static_assert(LDS <= 160 * 1024, "LDS budget");
-  using Out = TileShape<bf16_t, 1, B2, 4, 1, 128, 0>;   // for the staged store (128 x D)
-};
-
-// Position of 16-byte chunk c of W1^T row r inside its LDS row: 16 consecutive
-// rows read one chunk column, so the position is XOR-swizzled by the row
-// (by (r >> 1) & 7 for 128-byte rows, as the GEMM stages).
-template <int CPR>
-__device__ __forceinline__ int w1_pos(int r, int c) {
-  if constexpr (CPR == 8) return c ^ ((r >> 1) & 7);
-  else return c ^ (r & 15);
-}
-// W2^T chunk rows are 64 bytes (32 hidden): chunk c of row r sits at
-// position c ^ ((r >> 2) & 3), which spreads 16 consecutive rows over all
-// 64 banks.
-__device__ __forceinline__ int w2_pos(int r, int c) { return c ^ ((r >> 2) & 3); }
-
-// GEMM-2 A fragment of W2^T row `row` for step s, in the permuted k order of
-// pack_step (hidden 16 s + 4 lg + 0..3, then 16 s + 8 + 4 lg + 0..3).
-__device__ __forceinline__ u32x4_t frag_perm64(const char* base, int row, int s, int lg) {
-  const char* r = base + row * 64 + 8 * lg;
-  const u32x2_t lo = lds_read8(r + (w2_pos(row, 2 * s) << 4));
-  const u32x2_t hi = lds_read8(r + (w2_pos(row, 2 * s + 1) << 4));
-  return u32x4_t{lo[0], lo[1], hi[0], hi[1]};
-}
-
-// GELU(x) = x/2 (1 + erf(x / sqrt 2)) with the erf of erf_as (Abramowitz and
-// Stegun 7.1.26), split into 8 stages of about two operations so that four
-// independent elements can advance one stage between two MFMAs.
-struct GeluPipe {
-  float h[4], u[4], t[4], y[4], e[4];
-};
-__device__ __forceinline__ void gelu_stage(GeluPipe& g, float* x, int st) {
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    switch (st) {
-      case 0: g.h[j] = 0.5f * x[j]; g.u[j] = x[j] * 0.70710678118654752f;
-              g.t[j] = fmaf(0.3275911f, fabsf(g.u[j]), 1.0f); break;
-      case 1: g.t[j] = __builtin_amdgcn_rcpf(g.t[j]); g.e[j] = -(g.u[j] * g.u[j]) * 1.4426950408889634f; break;
-      case 2: g.y[j] = fmaf(1.061405429f, g.t[j], -1.453152027f); g.e[j] = __builtin_amdgcn_exp2f(g.e[j]); break;
-      case 3: g.y[j] = fmaf(g.y[j], g.t[j], 1.421413741f); break;
-      case 4: g.y[j] = fmaf(g.y[j], g.t[j], -0.284496736f); break;
-      case 5: g.y[j] = fmaf(g.y[j], g.t[j], 0.254829592f) * g.t[j]; break;
-      case 6: g.y[j] = copysignf(fmaf(-g.y[j], g.e[j], 1.0f), g.u[j]); break;
-      default: x[j] = fmaf(g.h[j], g.y[j], g.h[j]); break;
-    }
-  }
-}
-
-template <int N1, int D>
-__global__ __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void b2b_ffn_kernel(B2BParams p) {
-  using F = FfnShape<N1, D>;
-  __shared__ __attribute__((aligned(16))) char smem[F::LDS];
-  float* vec = reinterpret_cast<float*>(smem + F::LDS - F::VEC);   // b1[N1] b2[D] gamma[D] beta[D]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int lr = lane & 31, lg = lane >> 5;
-  const int bz = blockIdx.y;
-  const int m0 = blockIdx.x * F::TM;
-  const bf16_t* X = p.X + (int64_t)bz * p.sx;
-  const bf16_t* W1 = p.W1 + (int64_t)bz * p.sw1;
-  const bf16_t* W2 = p.W2 + (int64_t)bz * p.sw2;
-
-  // Per-column vectors into LDS (absent ones as 0 / 1 / 0).
-  for (int i = tid; i < N1 + 3 * D; i += F::NT) {
-    float v;
-    if (i < N1) v = p.b1 ? p.b1[i] : 0.0f;
-    else if (i < N1 + D) v = p.b2 ? p.b2[i - N1] : 0.0f;
-    else if (i < N1 + 2 * D) v = p.gamma ? p.gamma[i - N1 - D] : 1.0f;
-    else v = p.beta ? p.beta[i - N1 - 2 * D] : 0.0f;
-    vec[i] = v;
-  }
-
-  // Wave-wide loads of hidden chunk k: W1^T rows 32k .. +31 (all K) into
-  // ring-1 slot k & 1; W2^T rows 0 .. D-1, hidden 32k .. +31, into ring 2.
-  auto issue1 = [&](int k) {
-    char* slot = smem + (k & 1) * F::W1C;
-#pragma unroll
-    for (int j = 0; j < F::I1; ++j) {
-      const int q = (wave * F::I1 + j) * 64 + lane;
-      const int r = q / F::CPR1, c = w1_pos<F::CPR1>(r, q % F::CPR1);
-      dma16(W1 + (int64_t)(k * F::HC + r) * p.ldw1 + c * 8, slot + (wave * F::I1 + j) * 1024);
-    }
-  };
-  auto issue2 = [&](int k) {
-    char* slot = smem + F::RING1 + (k & 1) * F::W2C;
-#pragma unroll
-    for (int j = 0; j < F::I2; ++j) {
-      const int q = (wave * F::I2 + j) * 64 + lane;
-      const int r = q >> 2, c = w2_pos(r, q & 3);
-      dma16(W2 + (int64_t)r * p.ldw2 + k * F::HC + c * 8, slot + (wave * F::I2 + j) * 1024);
-    }
-  };
-  issue1(0);
-
-  // X^T fragments of this wave's 32 rows: xf[ks] = X[m][16 ks + 8 lg .. +8].
-  const int m = m0 + wave * 32 + lr;
-  const bf16_t* xrow = X + (int64_t)min(m, p.M - 1) * p.ldx + 8 * lg;
-  u32x4_t xf[F::KS1];
-#pragma unroll
-  for (int ks = 0; ks < F::KS1; ++ks) xf[ks] = gload16(xrow + 16 * ks);
-
-  f32x16_t Oa[F::B2];
-#pragma unroll
-  for (int b = 0; b < F::B2; ++b)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) Oa[b][i] = 0.0f;
-
-  // One pipeline iteration c: GEMM 1 of chunk c+1 (into Pn, if ONE), GEMM 2
-  // of chunk c-1 (with Sp, if TWO) and the GELU of chunk c (on Pc, if GEL).
-  // Slot i issues MFMA i (if any), the A-fragment read for MFMA i+2, and GELU
-  // stage i % 8 of elements 4 (i / 8) .. +3; the order is pinned.
-  f32x16_t Pc, Pn;
-  u32x4_t Sp[2];
-  auto iter = [&](int c, auto one_t, auto two_t, auto gel_t) {
-    constexpr bool ONE = decltype(one_t)::value, TWO = decltype(two_t)::value, GEL = decltype(gel_t)::value;
-    constexpr int NM = (ONE ? F::NM1 : 0) + (TWO ? F::NM2 : 0);
-    constexpr int NS = GEL ? (NM > F::GSLOTS ? NM : F::GSLOTS) : NM;   // slots
-    static_assert(!GEL || NS == F::GSLOTS, "one GELU stage per slot");
-    const char* s1 = smem + ((c + 1) & 1) * F::W1C;
-    const char* s2 = smem + F::RING1 + ((c - 1) & 1) * F::W2C;
-    auto afrag = [&](int i) -> u32x4_t {
-      if (ONE && i < F::NM1) return lds_read16(s1 + lr * F::RB1 + (w1_pos<F::CPR1>(lr, 2 * i + lg) << 4));
-      const int j = i - (ONE ? F::NM1 : 0);
-      return frag_perm64(s2, (j % F::B2) * 32 + lr, j / F::B2, lg);
-    };
-    if constexpr (ONE) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) Pn[i] = 0.0f;
-    }
-    u32x4_t fr[3];
-    GeluPipe gp;
-    if constexpr (NM > 0) fr[0] = afrag(0);
-    if constexpr (NM > 1) fr[1] = afrag(1);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = 0; i < NS; ++i) {
-      if (i < NM) {
-        if (ONE && i < F::NM1) {
-          Mma<bf16_t>::run(Pn, fr[i % 3], xf[i]);
-        } else {
-          const int j = i - (ONE ? F::NM1 : 0);
-          Mma<bf16_t>::run(Oa[j % F::B2], fr[i % 3], Sp[j / F::B2]);
-        }
-        if (i + 2 < NM) fr[(i + 2) % 3] = afrag(i + 2);
-      }
-      if constexpr (GEL) {
-        const int gi = i;   // GELU stage gi & 7 of elements 4 (gi >> 3) .. +3
-        {
-          float x4[4] = {Pc[(gi >> 3) * 4], Pc[(gi >> 3) * 4 + 1], Pc[(gi >> 3) * 4 + 2], Pc[(gi >> 3) * 4 + 3]};
-          gelu_stage(gp, x4, gi & 7);
-          if ((gi & 7) == 7) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) Pc[(gi >> 3) * 4 + q] = x4[q];
-          }
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
-  // P += b1 of chunk k (right after its GEMM 1; the GELU work then touches registers only).
-  auto add_b1 = [&](int k, f32x16_t& P) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const f32x4_t bb = *reinterpret_cast<const f32x4_t*>(vec + k * F::HC + 8 * g + 4 * lg);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) P[4 * g + q] += bb[q];
-    }
-  };
-  using T_ = std::true_type;
-  using F_ = std::false_type;
-  // Iteration c: W1^T(c+1) and W2^T(c-1) have landed; every wave is done with
-  // the slots the next loads overwrite (W1^T(c), W2^T(c-2)).
-  auto top = [&](int c) {
-    wait_vmcnt<0>();
-    __syncthreads();
-    if (c + 2 < F::NC) issue1(c + 2);
-    if (c < F::NC) issue2(c);
-  };
-  auto rotate = [&](int c) {   // after iteration c: S of chunk c, P of chunk c+1
-    Sp[0] = pack_step(Pc, 0);
-    Sp[1] = pack_step(Pc, 1);
-    if (c + 1 < F::NC) {
-      add_b1(c + 1, Pn);
-      Pc = Pn;
-    }
-  };
-
-  // Prologue: GEMM 1 of chunk 0, then iteration 0 (no GEMM 2 yet).
-  wait_vmcnt<0>();
-  __syncthreads();
-  if (F::NC > 1) issue1(1);
-  iter(-1, T_{}, F_{}, F_{});
-  add_b1(0, Pn);
-  Pc = Pn;
-  top(0);
-  if constexpr (F::NC > 1) iter(0, T_{}, F_{}, T_{});
-  else iter(0, F_{}, F_{}, T_{});
-  rotate(0);
-  // Steady state: one body, so every accumulator keeps its registers.
-  for (int c = 1; c + 1 < F::NC; ++c) {
-    top(c);
-    iter(c, T_{}, T_{}, T_{});
-    rotate(c);
-  }
-  if constexpr (F::NC > 1) {
-    top(F::NC - 1);
-    iter(F::NC - 1, F_{}, T_{}, T_{});
-    rotate(F::NC - 1);
-  }
-  top(F::NC);
-  iter(F::NC, F_{}, T_{}, F_{});
-  __syncthreads();
-
-  // Epi2: x = O + b2 + R, LayerNorm over the row (the lane pair holds it all).
-  const bool mv = m < p.M;
-  const bool r_is_x = p.R == p.X && p.ldr == p.ldx && (p.batch == 1 || p.sr == p.sx);
-#pragma unroll
-  for (int b = 0; b < F::B2; ++b)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int n = b * 32 + 8 * g + 4 * lg;
-      const f32x4_t bb = *reinterpret_cast<const f32x4_t*>(vec + N1 + n);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) Oa[b][4 * g + q] += bb[q];
-    }
-  if (p.R && r_is_x) {
-    // X[m][32 b + 8 g + 4 lg + q] lives in xf[2 b + g / 2] of lane half g % 2:
-    // each lane keeps one half of a fragment and takes the other from its pair.
-#pragma unroll
-    for (int ks = 0; ks < F::KS1; ++ks) {
-      const uint32_t s0 = lg ? xf[ks][0] : xf[ks][2], s1 = lg ? xf[ks][1] : xf[ks][3];
-      const uint32_t r0 = __shfl_xor(s0, 32), r1 = __shfl_xor(s1, 32);
-      const uint32_t e0 = lg ? r0 : xf[ks][0], e1 = lg ? r1 : xf[ks][1];   // columns of g even
-      const uint32_t o0 = lg ? xf[ks][2] : r0, o1 = lg ? xf[ks][3] : r1;   // columns of g odd
-      const int b = ks >> 1, ge = 2 * (ks & 1);
-      Oa[b][4 * ge + 0] += bf16_to_f32(e0 & 0xFFFFu);
-      Oa[b][4 * ge + 1] += bf16_to_f32(e0 >> 16);
-      Oa[b][4 * ge + 2] += bf16_to_f32(e1 & 0xFFFFu);
-      Oa[b][4 * ge + 3] += bf16_to_f32(e1 >> 16);
-      Oa[b][4 * ge + 4] += bf16_to_f32(o0 & 0xFFFFu);
-      Oa[b][4 * ge + 5] += bf16_to_f32(o0 >> 16);
-      Oa[b][4 * ge + 6] += bf16_to_f32(o1 & 0xFFFFu);
-      Oa[b][4 * ge + 7] += bf16_to_f32(o1 >> 16);
-    }
-  } else if (p.R && mv) {
-#pragma unroll
-    for (int b = 0; b < F::B2; ++b)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        float r[4];
-        load4<bf16_t>(p.R + (int64_t)bz * p.sr + (int64_t)m * p.ldr + b * 32 + 8 * g + 4 * lg, r);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) Oa[b][4 * g + q] += r[q];
-      }
-  }
-  if (p.out_ln) {
-    float s4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int b = 0; b < F::B2; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) s4[i & 3] += Oa[b][i];
-    const float mean = lane_pair_sum((s4[0] + s4[1]) + (s4[2] + s4[3])) * (1.0f / D);
-    float q4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int b = 0; b < F::B2; ++b)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float d = Oa[b][i] - mean;
-        q4[i & 3] += d * d;
-      }
-    const float rstd = rsqrtf(lane_pair_sum((q4[0] + q4[1]) + (q4[2] + q4[3])) * (1.0f / D) + p.eps);
-#pragma unroll
-    for (int b = 0; b < F::B2; ++b)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = b * 32 + 8 * g + 4 * lg;
-        const f32x4_t ga = *reinterpret_cast<const f32x4_t*>(vec + N1 + D + n);
-        const f32x4_t be = *reinterpret_cast<const f32x4_t*>(vec + N1 + 2 * D + n);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) Oa[b][4 * g + q] = (Oa[b][4 * g + q] - mean) * rstd * ga[q] + be[q];
-      }
-  }
-  store_tile_staged<typename F::Out>(reinterpret_cast<f32x16_t(&)[1][F::B2]>(Oa), p.O + (int64_t)bz * p.so, p.ldo, 0,
-                                     p.M, D, m0, 0, smem, tid, lane, wave, 0);
-}
 
 // ===========================================================================
 // Attention: O = softmax(scale * Q K^T) V per (batch*head), online softmax.
@@ -676,21 +355,7 @@ __global__ __launch_bounds__(256, 1) void b2b_attention_kernel(B2BParams p) {
 }
 
 // ---------------------------------------------------------------------------
-bool b2b_ffn_supported(int N1, int N2) {
-  return (N1 == 512 && N2 == 256) || (N1 == 256 && N2 == 128) || (N1 == 128 && N2 == 64) ||
-         (N1 == 256 && N2 == 256);
-}
 bool b2b_attention_supported(int d) { return d == 64 || d == 128; }
-
-hipError_t launch_b2b_ffn(const B2BParams& p, hipStream_t st) {
-  const dim3 grid((unsigned)((p.M + 127) / 128), (unsigned)p.batch), block(256);
-  if (p.N1 == 512 && p.N2 == 256) hipLaunchKernelGGL((b2b_ffn_kernel<512, 256>), grid, block, 0, st, p);
-  else if (p.N1 == 256 && p.N2 == 256) hipLaunchKernelGGL((b2b_ffn_kernel<256, 256>), grid, block, 0, st, p);
-  else if (p.N1 == 256 && p.N2 == 128) hipLaunchKernelGGL((b2b_ffn_kernel<256, 128>), grid, block, 0, st, p);
-  else if (p.N1 == 128 && p.N2 == 64) hipLaunchKernelGGL((b2b_ffn_kernel<128, 64>), grid, block, 0, st, p);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
-}
 
 hipError_t launch_b2b_attention(const B2BParams& p, hipStream_t st) {
   const dim3 grid((unsigned)((p.M + 127) / 128), (unsigned)p.batch), block(256);

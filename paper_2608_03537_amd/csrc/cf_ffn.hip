@@ -1,0 +1,420 @@
+// Back-to-back FFN for gfx950 (Sec. IV, Eq. 2 with F = +b1, GELU; Sec. IV-A):
+//   O = GELU(X W1 + b1) W2 (+ b2 + R, LayerNorm),   K = N2 = D,
+// with the intermediate S kept on chip.
+//
+// Work split.  A workgroup owns 128 rows and runs 8 waves, two per SIMD: a
+// single wave issues vector instructions at about half the SIMD's rate, and
+// the GELU between the two products is vector work.  Waves w and w + 4 form
+// a pair that shares 32 rows (row group pr = w & 3); half h = w >> 2 of the
+// pair owns output columns [h D/2, (h+1) D/2) and the hidden chunks c with
+// c % 2 == h (chunks are HC = 32 hidden units).  Round t covers chunks 2t and
+// 2t+1: each half computes the first product and the GELU of its own chunk,
+// hands the bf16 S of that chunk to its partner through LDS, and accumulates
+// the second product of both chunks into its own half of O (the partial-sum
+// identity O = sum_k S^(k) W2^(k) of Sec. IV-A).
+//
+// Register hand-off.  The first product is computed transposed,
+// P^T = W1^T X^T, so in a 32x32 accumulator block lane (lr, g = lane / 32)
+// holds row m = lr of P and element i sits in block row 8 (i/4) + 4 g + i%4.
+// The rows of each W1^T chunk are loaded in a permuted order
+// (ffn_hidden_row), so that accumulator elements 8 s .. 8 s + 7 hold hidden
+// units 16 s + 8 g + 0..7.  Packed to bf16 they are exactly the B operand of
+// step s of the second product O^T = W2^T S^T, whose A operand is then one
+// contiguous 16-byte piece of a W2^T row.
+//
+// LDS operands are stored in MFMA fragment order: wave-wide direct loads
+// (global_load_lds) place lane l's 16 bytes of fragment f at f * 1024 + 16 l,
+// so every fragment read is one conflict-free 1 KB read at an immediate
+// offset.  Layout (bytes):
+//   ring 1: 2 stages x {W1^T chunk 2t, W1^T chunk 2t+1}, KS1 fragments each
+//   ring 2: 2 stages x {W2^T chunk 2t, W2^T chunk 2t+1}, 2 B2 fragments each
+//   S exchange: 2 stages x [row group 4][half 2][lane 64][32 B]
+#include "cf_gemm_tile.h"
+#include "comfuse.h"
+
+namespace cf {
+
+template <int N1, int D>
+struct FfnShape {
+  static constexpr int TM = 128, NW = 8, NT = 64 * NW, HC = 32;
+  static constexpr int NC = N1 / HC;            // hidden chunks
+  static constexpr int NR = NC / 2;             // rounds (one chunk per half)
+  static constexpr int KS1 = D / 16;            // MFMA steps of the first product (= X fragments)
+  static constexpr int B2 = D / 32, B2H = B2 / 2;   // output blocks: all, per half
+  static constexpr int NM1 = KS1;               // first-product MFMAs per round (own chunk)
+  static constexpr int NM2 = 2 * 2 * B2H;       // second-product MFMAs per round (2 chunks x B2H x 2 steps)
+  static constexpr int W1C = KS1 * 1024;        // one W1^T chunk (32 x D bf16)
+  static constexpr int W2C = 2 * B2 * 1024;     // one W2^T chunk (D x 32 bf16)
+  static constexpr int W1S = 2 * W1C, W2S = 2 * W2C;
+  static constexpr int OFF_W2 = 2 * W1S;
+  static constexpr int OFF_X = OFF_W2 + 2 * W2S;
+  static constexpr int XCH = 4 * 2 * 64 * 32;   // one exchange stage
+  static constexpr int LDS = OFF_X + 2 * XCH;
+  static constexpr int LDS_STORE = TM * (D * 2 + 8);
+  static constexpr int DMA_W = (2 * KS1 + 2 * 2 * B2) / NW;   // wave-wide loads per wave per round
+  static constexpr int GSLOTS = 32;             // GELU work per round: 4 groups x 8 stages
+  static constexpr int FG = 4;                  // A-fragment reads per group
+  static_assert(N1 % (2 * HC) == 0 && D % 64 == 0, "shape");
+  static_assert(NM1 == NM2, "the two products alternate MFMA by MFMA");
+  static_assert((2 * KS1 + 4 * B2) % NW == 0, "loads per wave");
+  static_assert(LDS <= 160 * 1024 && LDS_STORE <= OFF_X, "LDS budget");
+  using Out = TileShape<bf16_t, 1, B2H, 4, 2, 128, 0>;   // staged store: 128 x D, wave tile 32 x D/2
+};
+
+// Hidden unit (within its chunk) held by row r of a W1^T chunk in LDS: bits
+// 2 and 3 of r swapped (see the register hand-off above).
+__device__ __forceinline__ int ffn_hidden_row(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
+
+// Accumulator elements 8 s .. 8 s + 7 as 8 packed bf16 (B operand of step s).
+__device__ __forceinline__ u32x4_t ffn_pack_step(const f32x16_t& v, int s) {
+  return u32x4_t{pack_bf16x2(v[8 * s + 0], v[8 * s + 1]), pack_bf16x2(v[8 * s + 2], v[8 * s + 3]),
+                 pack_bf16x2(v[8 * s + 4], v[8 * s + 5]), pack_bf16x2(v[8 * s + 6], v[8 * s + 7])};
+}
+
+// GELU(x) = x/2 (1 + erf(x / sqrt 2)) with the erf of Abramowitz and Stegun
+// 7.1.26 (as erf_as), split into 8 stages of about two operations so that
+// four independent elements advance one stage between two MFMAs.  The input
+// x stays in place until the last stage (it carries the sign and x/2).
+struct GeluPipe {
+  float t[4], y[4], e[4];
+};
+__device__ __forceinline__ void gelu_stage(GeluPipe& g, const float* x, float* out, int st) {
+  constexpr float kRs2 = 0.70710678118654752f;            // 1 / sqrt 2
+  constexpr float kHalfLog2e = 0.72134752044448170f;      // log2(e) / 2: exp(-x^2 / 2) = exp2(-x^2 kHalfLog2e)
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    switch (st) {
+      case 0: g.t[j] = fmaf(0.3275911f * kRs2, fabsf(x[j]), 1.0f); break;
+      case 1: g.t[j] = __builtin_amdgcn_rcpf(g.t[j]); g.e[j] = -(x[j] * x[j]) * kHalfLog2e; break;
+      case 2: g.y[j] = fmaf(1.061405429f, g.t[j], -1.453152027f); g.e[j] = __builtin_amdgcn_exp2f(g.e[j]); break;
+      case 3: g.y[j] = fmaf(g.y[j], g.t[j], 1.421413741f); break;
+      case 4: g.y[j] = fmaf(g.y[j], g.t[j], -0.284496736f); break;
+      case 5: g.y[j] = fmaf(g.y[j], g.t[j], 0.254829592f) * g.t[j]; break;
+      case 6: g.y[j] = copysignf(fmaf(-g.y[j], g.e[j], 1.0f), x[j]); break;
+      default: { const float hx = 0.5f * x[j]; out[j] = fmaf(hx, g.y[j], hx); } break;
+    }
+  }
+}
+
+template <int N1, int D>
+__global__ __launch_bounds__(512, 1) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void b2b_ffn_kernel(B2BParams p) {
+  using F = FfnShape<N1, D>;
+  __shared__ __attribute__((aligned(16))) char smem[F::LDS];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
+  const int lr = lane & 31, lg = lane >> 5;
+  const int pr = wave & 3, h = wave >> 2;       // row group, half
+  const int bz = blockIdx.y;
+  const int m0 = blockIdx.x * F::TM;
+  const int m = m0 + pr * 32 + lr;
+  const bf16_t* X = p.X + (int64_t)bz * p.sx;
+  const bf16_t* W1 = p.W1 + (int64_t)bz * p.sw1;
+  const bf16_t* W2 = p.W2 + (int64_t)bz * p.sw2;
+  const int nb0 = h * F::B2H;                   // first output block of this half
+
+  // Wave-wide loads.  Waves 0-3 load the two W1^T chunks of a round: load
+  // q = DMA_W wave + j in [0, 2 KS1) is fragment q % KS1 of chunk 2 r + q / KS1
+  // (32 hidden rows in ffn_hidden_row order, k step 16 (q % KS1)).  Waves 4-7
+  // load the two W2^T chunks: load q in [0, 4 B2) is fragment (b, s) of chunk
+  // 2 r + e (rows 32 b .. +31, hidden 32 (2 r + e) + 16 s ..), q = 2 B2 e + 2 b + s.
+  // Addresses are a wave-uniform base plus a 32-bit lane offset.
+  const bool w1part = wave < 4;
+  const char* gbase = w1part ? reinterpret_cast<const char*>(W1) : reinterpret_cast<const char*>(W2);
+  const uint32_t loff = w1part ? (uint32_t)(ffn_hidden_row(lr) * p.ldw1 * 2 + 16 * lg)
+                               : (uint32_t)(lr * p.ldw2 * 2 + 16 * lg);
+  auto issue = [&](int r1, bool do1, int r2, bool do2) {
+    if (w1part ? !do1 : !do2) return;
+    const int r = w1part ? r1 : r2;
+#pragma unroll
+    for (int j = 0; j < F::DMA_W; ++j) {
+      const int q = (wave & 3) * F::DMA_W + j;
+      int64_t goff;
+      int soff;
+      if (w1part) {
+        const int e = q / F::KS1, f = q % F::KS1;
+        goff = (int64_t)((2 * r + e) * F::HC) * p.ldw1 * 2 + 32 * f;
+        soff = (r & 1) * F::W1S + q * 1024;
+      } else {
+        const int e = q / (2 * F::B2), f = q % (2 * F::B2), b = f >> 1, sb = f & 1;
+        goff = (int64_t)(32 * b) * p.ldw2 * 2 + ((2 * r + e) * F::HC + 16 * sb) * 2;
+        soff = F::OFF_W2 + (r & 1) * F::W2S + q * 1024;
+      }
+      dma16(gbase + goff + (uint64_t)loff, smem + soff);
+    }
+  };
+
+  // X^T fragments of this pair's 32 rows: xf[ks] = X[m][16 ks + 8 lg .. +8].
+  const bf16_t* xrow = X + (int64_t)min(m, p.M - 1) * p.ldx + 8 * lg;
+  u32x4_t xf[F::KS1];
+#pragma unroll
+  for (int ks = 0; ks < F::KS1; ++ks) xf[ks] = gload16(xrow + 16 * ks);
+
+  // O accumulators start at b2 (element i of block b: column 32 b + 8 (i/4) + 4 lg + i%4).
+  f32x16_t Oa[F::B2H];
+  if (p.b2) {
+    const float* b2l = p.b2 + nb0 * 32 + 4 * lg;
+#pragma unroll
+    for (int b = 0; b < F::B2H; ++b)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4_t bb = *reinterpret_cast<const f32x4_t*>(b2l + b * 32 + 8 * g);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) Oa[b][4 * g + q] = bb[q];
+      }
+  } else {
+#pragma unroll
+    for (int b = 0; b < F::B2H; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) Oa[b][i] = 0.0f;
+  }
+  // b1 of hidden chunk c in the accumulator order: element 4 g + q holds hidden
+  // unit 16 (g / 2) + 8 lg + 4 (g % 2) + q of the chunk.
+  auto load_b1 = [&](int c, f32x4_t (&v)[4]) {
+    if (p.b1) {
+      const float* b1l = p.b1 + c * F::HC + 8 * lg;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) v[g] = *reinterpret_cast<const f32x4_t*>(b1l + 16 * (g >> 1) + 4 * (g & 1));
+    } else {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) v[g] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+  };
+  auto add_b1 = [&](f32x16_t& P, const f32x4_t (&v)[4]) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) P[4 * g + q] += v[g][q];
+  };
+
+  issue(0, true, 0, false);
+
+  // Residual R = X: O^T += I X^T, one MFMA per (block, k step) with an
+  // identity fragment as A (exact: the products are x * 1 and x * 0).
+  const bool r_is_x = p.R == p.X && p.ldr == p.ldx && (p.batch == 1 || p.sr == p.sx);
+  if (p.R && r_is_x) {
+    u32x4_t id[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int j = lr - 16 * e - 8 * lg;   // position of the 1 in this lane's 8 k values
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        id[e][w] = (j == 2 * w ? 0x3F80u : 0u) | (j == 2 * w + 1 ? 0x3F800000u : 0u);
+    }
+#pragma unroll
+    for (int b = 0; b < F::B2H; ++b) {   // block nb0 + b takes X fragments 2 (nb0 + b) and 2 (nb0 + b) + 1
+      Mma<bf16_t>::run(Oa[b], id[0], h ? xf[2 * (F::B2H + b)] : xf[2 * b]);
+      Mma<bf16_t>::run(Oa[b], id[1], h ? xf[2 * (F::B2H + b) + 1] : xf[2 * b + 1]);
+    }
+  }
+
+  // One pipeline round t: the first product of this half's chunk of round
+  // t+1 (into Pn, if ONE), the second product of both chunks of round t-1
+  // (own S from Sp, the partner's from Sx, if TWO) and the GELU of this
+  // half's chunk of round t (on Pc, if GEL).  MFMAs of the two products
+  // alternate; slot i issues MFMA i (if any) and GELU stage i % 8 of
+  // elements 4 (i / 8) .. +3.  A fragments are read in groups of FG, each
+  // group right after the first MFMA of the previous group.
+  f32x16_t Pc, Pn;
+  u32x4_t Sp[2], Sx[2];
+  auto iter = [&](int t, auto one_t, auto two_t, auto gel_t) {
+    constexpr bool ONE = decltype(one_t)::value, TWO = decltype(two_t)::value, GEL = decltype(gel_t)::value;
+    constexpr int NM = (ONE ? F::NM1 : 0) + (TWO ? F::NM2 : 0);
+    constexpr int NS = GEL ? (NM > F::GSLOTS ? NM : F::GSLOTS) : NM;
+    constexpr int FG = F::FG;
+    static_assert(!GEL || NS == F::GSLOTS, "one GELU stage per slot");
+    const char* a1 = smem + ((t + 1) & 1) * F::W1S + h * F::W1C + lane * 16;
+    const char* a2o = smem + F::OFF_W2 + ((t - 1) & 1) * F::W2S + h * F::W2C + lane * 16;   // own chunk
+    const char* a2p = smem + F::OFF_W2 + ((t - 1) & 1) * F::W2S + (1 - h) * F::W2C + lane * 16;   // partner's
+    auto is1 = [&](int i) { return ONE && (TWO ? (i & 1) == 0 : true); };
+    auto idx = [&](int i) { return ONE && TWO ? i >> 1 : i; };
+    // second-product op j: block nb0 + j % B2H, step j / (2 B2H), with this
+    // half's chunk of round t-1 (S in Sp) if (j / B2H) is even, else the
+    // partner's chunk (S in Sx)
+    auto afrag = [&](int i) -> u32x4_t {
+      const int j = idx(i);
+      if (is1(i)) return lds_read16(a1 + j * 1024);
+      const int b = j % F::B2H, own = ((j / F::B2H) & 1) == 0, s = j / (2 * F::B2H);
+      return lds_read16((own ? a2o : a2p) + (2 * (nb0 + b) + s) * 1024);
+    };
+    if constexpr (ONE) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) Pn[i] = 0.0f;
+    }
+    u32x4_t fr[2][FG];
+    GeluPipe gp;
+#pragma unroll
+    for (int k = 0; k < FG; ++k)
+      if (k < NM) fr[0][k] = afrag(k);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      if (i < NM) {
+        const u32x4_t& a = fr[(i / FG) & 1][i % FG];
+        const int j = idx(i);
+        if (is1(i)) {
+          Mma<bf16_t>::run(Pn, a, xf[j]);
+        } else {
+          const bool own = ((j / F::B2H) & 1) == 0;
+          const int s = j / (2 * F::B2H);
+          Mma<bf16_t>::run(Oa[j % F::B2H], a, own ? Sp[s] : Sx[s]);
+        }
+        if (i % FG == 0) {
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int k = 0; k < FG; ++k) {
+            const int nx = (i / FG + 1) * FG + k;
+            if (nx < NM) fr[(i / FG + 1) & 1][k] = afrag(nx);
+          }
+        }
+      }
+      if constexpr (GEL) {
+        const float x4[4] = {Pc[(i >> 3) * 4], Pc[(i >> 3) * 4 + 1], Pc[(i >> 3) * 4 + 2], Pc[(i >> 3) * 4 + 3]};
+        float o4[4];
+        gelu_stage(gp, x4, o4, i & 7);
+        if ((i & 7) == 7) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) Pc[(i >> 3) * 4 + q] = o4[q];
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  char* xch_own = smem + F::OFF_X + ((pr * 2 + h) * 64 + lane) * 32;
+  char* xch_par = smem + F::OFF_X + ((pr * 2 + (1 - h)) * 64 + lane) * 32;
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+  // Top of round t: W1^T of round t+1 and W2^T of round t-1 have landed and
+  // every wave is done with the slots the next loads overwrite (W1^T of
+  // round t, W2^T of round t-2); the partner's S of round t-1 is visible.
+  auto top = [&](int t) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    issue(t + 2, t + 2 < F::NR, t, t < F::NR);
+    if (t >= 1) {
+      const char* src = xch_par + ((t - 1) & 1) * F::XCH;
+      Sx[0] = lds_read16(src);
+      Sx[1] = lds_read16(src + 16);
+    }
+  };
+  // After round t: S of round t to registers and to the exchange; P of round t+1.
+  auto rotate = [&](int t) {
+    Sp[0] = ffn_pack_step(Pc, 0);
+    Sp[1] = ffn_pack_step(Pc, 1);
+    char* dst = xch_own + (t & 1) * F::XCH;
+    lds_write16(dst, Sp[0]);
+    lds_write16(dst + 16, Sp[1]);
+    if (t + 1 < F::NR) {
+      f32x4_t b1v[4];
+      load_b1(2 * (t + 1) + h, b1v);
+      add_b1(Pn, b1v);
+      Pc = Pn;
+    }
+  };
+
+  // Prologue: the first product of round 0, then round 0 (no second product yet).
+  wait_vmcnt<0>();
+  __syncthreads();
+  if (F::NR > 1) issue(1, true, 0, false);
+  iter(-1, T_{}, F_{}, F_{});
+  {
+    f32x4_t b1v[4];
+    load_b1(h, b1v);
+    add_b1(Pn, b1v);
+  }
+  Pc = Pn;
+  top(0);
+  if constexpr (F::NR > 1) iter(0, T_{}, F_{}, T_{});
+  else iter(0, F_{}, F_{}, T_{});
+  rotate(0);
+#pragma unroll 1
+  for (int t = 1; t + 1 < F::NR; ++t) {
+    top(t);
+    iter(t, T_{}, T_{}, T_{});
+    rotate(t);
+  }
+  if constexpr (F::NR > 1) {
+    top(F::NR - 1);
+    iter(F::NR - 1, F_{}, T_{}, T_{});
+    rotate(F::NR - 1);
+  }
+  top(F::NR);
+  iter(F::NR, F_{}, T_{}, F_{});
+  __syncthreads();
+
+  // Epi2: residual (general R), then LayerNorm over the row, whose D values
+  // sit in lanes (lr, lr + 32) of both halves of the pair.
+  const bool mv = m < p.M;
+  if (p.R && !r_is_x && mv) {
+#pragma unroll
+    for (int b = 0; b < F::B2H; ++b)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float r[4];
+        load4<bf16_t>(p.R + (int64_t)bz * p.sr + (int64_t)m * p.ldr + (nb0 + b) * 32 + 8 * g + 4 * lg, r);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) Oa[b][4 * g + q] += r[q];
+      }
+  }
+  if (p.out_ln) {
+    float* red = reinterpret_cast<float*>(smem + F::OFF_X);   // [stat 2][row group 4][half 2][row 32]
+    auto pair_total = [&](float v, int stat) {
+      v += __shfl_xor(v, 32);
+      if (lg == 0) red[((stat * 4 + pr) * 2 + h) * 32 + lr] = v;
+      __syncthreads();
+      return red[((stat * 4 + pr) * 2 + 0) * 32 + lr] + red[((stat * 4 + pr) * 2 + 1) * 32 + lr];
+    };
+    float s4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int b = 0; b < F::B2H; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s4[i & 3] += Oa[b][i];
+    const float mean = pair_total((s4[0] + s4[1]) + (s4[2] + s4[3]), 0) * (1.0f / D);
+    float q4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int b = 0; b < F::B2H; ++b)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        Oa[b][i] -= mean;
+        q4[i & 3] = fmaf(Oa[b][i], Oa[b][i], q4[i & 3]);
+      }
+    const float rstd = rsqrtf(pair_total((q4[0] + q4[1]) + (q4[2] + q4[3]), 1) * (1.0f / D) + p.eps);
+#pragma unroll
+    for (int b = 0; b < F::B2H; ++b)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = (nb0 + b) * 32 + 8 * g + 4 * lg;
+        f32x4_t ga = {1.0f, 1.0f, 1.0f, 1.0f}, be = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (p.gamma) ga = *reinterpret_cast<const f32x4_t*>(p.gamma + n);
+        if (p.beta) be = *reinterpret_cast<const f32x4_t*>(p.beta + n);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) Oa[b][4 * g + q] = fmaf(Oa[b][4 * g + q] * rstd, ga[q], be[q]);
+      }
+  }
+  store_tile_staged<typename F::Out>(reinterpret_cast<f32x16_t(&)[1][F::B2H]>(Oa), p.O + (int64_t)bz * p.so, p.ldo, 0,
+                                     p.M, D, m0, 0, smem, tid, lane, pr, h);
+}
+
+bool b2b_ffn_supported(int N1, int N2) {
+  return (N1 == 512 && N2 == 256) || (N1 == 256 && N2 == 128) || (N1 == 128 && N2 == 64) ||
+         (N1 == 256 && N2 == 256);
+}
+
+template <int N1, int D>
+static hipError_t launch_ffn(const B2BParams& p, hipStream_t st) {
+  using F = FfnShape<N1, D>;
+  const dim3 grid((unsigned)((p.M + F::TM - 1) / F::TM), (unsigned)p.batch), block(F::NT);
+  hipLaunchKernelGGL((b2b_ffn_kernel<N1, D>), grid, block, 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_b2b_ffn(const B2BParams& p, hipStream_t st) {
+  if (p.N1 == 512 && p.N2 == 256) return launch_ffn<512, 256>(p, st);
+  if (p.N1 == 256 && p.N2 == 256) return launch_ffn<256, 256>(p, st);
+  if (p.N1 == 256 && p.N2 == 128) return launch_ffn<256, 128>(p, st);
+  if (p.N1 == 128 && p.N2 == 64) return launch_ffn<128, 64>(p, st);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace cf

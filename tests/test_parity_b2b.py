@@ -50,6 +50,23 @@ def test_ffn_without_layernorm():
     assert rel_rms(got, ref) < 5e-3 and max_abs(got, ref) < 2e-2
 
 
+@pytest.mark.parametrize("M,d,N1", [(190, 128, 256), (257, 256, 512)])
+def test_ffn_other_residual_gamma_beta(M, d, N1):
+    """Residual R != X (read from memory) and a LayerNorm with gamma/beta."""
+    inp = I.ffn_inputs(seed=5, M=M, d=d, N1=N1)
+    rng = np.random.default_rng(7)
+    R = I.round_to_bf16(rng.standard_normal((M, d)).astype(np.float32))
+    gamma = (1.0 + 0.1 * rng.standard_normal(d)).astype(np.float32)
+    beta = (0.1 * rng.standard_normal(d)).astype(np.float32)
+    X = dev(inp.X)
+    Y = cf.b2b_ffn(X, dev(I.lay_out_weight(inp.W1, "nk")), dev(inp.b1, "f32"), dev(I.lay_out_weight(inp.W2, "nk")),
+                   dev(inp.b2, "f32"), dev(R), dev(gamma, "f32"), dev(beta, "f32"), eps=inp.eps)
+    torch.cuda.synchronize()
+    S = O.gelu_erf(O.bias_residual(O.matmul(inp.X, inp.W1), inp.b1))
+    ref = O.layernorm(O.bias_residual(O.matmul(S, inp.W2), inp.b2, R), gamma, beta, inp.eps)
+    assert_close_bf16(host(Y), ref, f"FFN R != X {M}x{d}x{N1}")
+
+
 def test_ffn_zero_second_weight_is_layernorm_of_input():
     inp = I.ffn_inputs(seed=4, M=256, d=256, N1=512)
     inp.W2[:] = 0.0
