@@ -33,6 +33,8 @@ WL_LN_GELU_AMAX = 3
 WL_FFN_B2B = 4
 WL_ATTENTION = 5
 WL_MSTS = 6
+WL_SELF_ATTN_T2 = 7
+WL_TARGET_ATTN_T2 = 8
 WL_CUSTOM = 99
 
 
@@ -201,3 +203,16 @@ def attention_inputs(seed=0, B=4, H=16, Lq=2048, Lk=2048, d=128,
     K = _normal(seed, workload, 1, (B, H, Lk, d), 1.0, "bf16")
     V = _normal(seed, workload, 2, (B, H, Lk, d), 1.0, "bf16")
     return AttentionInputs(B, H, Lq, Lk, d, Q, K, V)
+
+
+def self_attention_table2(seed=0, B=16, H=16) -> AttentionInputs:
+    """Self-Attention of Table 2: sequence length 512, head dimension 128.
+    The paper gives no batch or head count; B = H = 16 gives 1024 workgroups."""
+    return attention_inputs(seed, B, H, 512, 512, 128, WL_SELF_ATTN_T2)
+
+
+def target_attention_table2(seed=0, B=4, H=16, d=128) -> AttentionInputs:
+    """Target-Attention of Table 2: 4096 target (query) rows against 256 source
+    (key/value) rows.  The paper gives no head dimension, batch or head count;
+    d = 128 as in its Self-Attention row, B = 4, H = 16 (2048 workgroups)."""
+    return attention_inputs(seed, B, H, 4096, 256, d, WL_TARGET_ATTN_T2)

@@ -97,6 +97,17 @@ def test_attention_small(B, H, Lq, Lk, d):
     assert max_abs(got, ref) < 2e-2
 
 
+@pytest.mark.parametrize("which", ["self", "target"])
+def test_attention_table2_shapes(which):
+    """Table 2 shapes (one batch, two heads), every element against the oracle:
+    Self-Attention (512 x 512, d 128) and Target-Attention (4096 target rows,
+    256 source rows, d 128)."""
+    a = I.self_attention_table2(seed=3, B=1, H=2) if which == "self" else I.target_attention_table2(seed=3, B=1, H=2)
+    got = run_attn(a.Q, a.K, a.V)
+    ref = O.attention(a.Q, a.K, a.V)
+    assert rel_rms(got, ref) < 5e-3 and max_abs(got, ref) < 2e-2, (rel_rms(got, ref), max_abs(got, ref))
+
+
 def test_attention_invariants():
     a = I.attention_inputs(seed=6, B=1, H=2, Lq=128, Lk=200, d=128)
     ones = run_attn(a.Q, a.K, np.ones_like(a.V))
