@@ -54,9 +54,10 @@ __device__ __forceinline__ float lane_pair_max(float v) { return fmaxf(v, __shfl
 //   S^T = K Q^T (K rows from LDS); lane-local row max / sum over its 32
 //   values + the lane pair; P = exp2(S*scale*log2e - m); O = O*corr + P V
 //   with P fed from registers and V^T rows from LDS.
-// Software pipeline inside each wave (the PingPong of Sec. III-C): the 16
-// MFMAs of block j+1's S^T are issued one per slot, and between them the
-// softmax of block j runs in 16 VALU chunks; then block j's P V MFMAs.
+// Two workgroups share a CU (at most 256 VGPRs per wave), so each SIMD runs
+// two waves of different workgroups, which no barrier holds in step: one
+// wave's softmax overlaps the other's MFMAs (the PingPong of Sec. III-C across
+// waves rather than inside one).
 // The running maximum is raised lazily: O and the row sum are rescaled only
 // when a block's maximum exceeds the one in use by more than 2^8, so
 // exp2(s - m) <= 256 and the common case skips the rescale; the final O / l
@@ -92,7 +93,7 @@ struct SoftmaxStep {
 };
 
 template <int D>
-__global__ __launch_bounds__(256, 1) void b2b_attention_kernel(B2BParams p) {
+__global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   using A = AttnShape<D>;
   __shared__ __attribute__((aligned(16))) char smem[A::LDS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -248,7 +249,7 @@ __global__ __launch_bounds__(256, 1) void b2b_attention_kernel(B2BParams p) {
         for (int i = 0; i < 16; ++i) Oa[b][i] *= st.corr;
     }
   };
-  // O^T += V^T P^T for block j (V^T fragments two MFMAs ahead).
+  // O^T += V^T P^T for block j (V^T fragments one MFMA ahead).
   auto pv_block = [&](int j, const SoftmaxStep& st) {
     const char* vt = smem + (j & 1) * A::STAGE + A::KB;
     auto vfrag = [&](int i) {   // i = (bl * 2 + s) * BD + b; permuted k order of pack_step
@@ -258,90 +259,60 @@ __global__ __launch_bounds__(256, 1) void b2b_attention_kernel(B2BParams p) {
       const u32x2_t hi = lds_read8(vt + vt_off(row, c0 + 1) + 8 * lg);
       return u32x4_t{lo[0], lo[1], hi[0], hi[1]};
     };
-    u32x4_t vf[3];
+    u32x4_t vf[2];
     vf[0] = vfrag(0);
-    if (A::NSB > 1) vf[1] = vfrag(1);
 #pragma unroll
     for (int i = 0; i < A::NSB; ++i) {
-      if (i + 2 < A::NSB) vf[(i + 2) % 3] = vfrag(i + 2);
+      if (i + 1 < A::NSB) vf[(i + 1) & 1] = vfrag(i + 1);
       const int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
-      Mma<bf16_t>::run(Oa[b], vf[i % 3], st.P[bl][s]);
+      Mma<bf16_t>::run(Oa[b], vf[i & 1], st.P[bl][s]);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // One pipelined step: S^T of block j+1 (into Sn) under the softmax of block j (Sc).
-  auto s_and_softmax = [&](f32x16_t (&Sn)[2], f32x16_t (&Sc)[2], int j, SoftmaxStep& st, auto mask_t) {
-    const char* kb = smem + ((j + 1) & 1) * A::STAGE;
-    u32x4_t kf[3];
+  // S^T of block j from its K rows in LDS (K fragments one MFMA ahead).
+  auto s_block = [&](f32x16_t (&S)[2], int j) {
+    const char* kb = smem + (j & 1) * A::STAGE;
+    u32x4_t kf[2];
     kf[0] = kfrag(kb, 0);
-    kf[1] = kfrag(kb, 1);
-    constexpr int CPS = A::NSA >= 16 ? 1 : 16 / A::NSA;   // softmax chunks per MFMA slot
 #pragma unroll
     for (int i = 0; i < A::NSA; ++i) {
-      if (i + 2 < A::NSA) kf[(i + 2) % 3] = kfrag(kb, i + 2);
-      mma_s(Sn, i, kf[i % 3]);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int q = 0; q < CPS; ++q)
-        if (i * CPS + q < 16) sm_chunk(Sc, i * CPS + q, st, j, mask_t);
-      __builtin_amdgcn_sched_barrier(0);
+      if (i + 1 < A::NSA) kf[(i + 1) & 1] = kfrag(kb, i + 1);
+      mma_s(S, i, kf[i & 1]);
     }
   };
-  auto softmax_only = [&](f32x16_t (&Sc)[2], int j, SoftmaxStep& st, auto mask_t) {
+  auto softmax_all = [&](f32x16_t (&Sc)[2], int j, SoftmaxStep& st, auto mask_t) {
 #pragma unroll
     for (int c = 0; c < 16; ++c) sm_chunk(Sc, c, st, j, mask_t);
   };
 
-  f32x16_t Sa[2], Sb[2];
+  f32x16_t S[2];
   SoftmaxStep st;
-  // Prologue: K, V of block 0 (V transposed into LDS), K, V of block 1 in
-  // flight, S^T of block 0.
+  // Prologue: K, V of block 0 in LDS (V transposed); V of block 1 in registers.
   issue_k(0);
   load_v(0);
   wait_vmcnt<0>();
   store_v(0);
-  if (NB > 1) {
-    issue_k(1);
-    load_v(1);
-  }
-  lds_sync();
-  {
-    const char* kb = smem;
-#pragma unroll
-    for (int i = 0; i < A::NSA; ++i) mma_s(Sa, i, kfrag(kb, i));
-  }
-  // Steady step j (blocks j and j+1 exist): K, V of block j+1 landed; V of
-  // block j+1 goes to LDS; K, V of block j+2 are issued; then the pipelined
-  // S^T(j+1) / softmax(j), the rescale and P V of block j.
-  auto step = [&](int j, f32x16_t (&Sc)[2], f32x16_t (&Sn)[2]) {
+  if (NB > 1) load_v(1);
+  // Step j: K(j) and V(j) are in stage j & 1 once every wave has passed the
+  // barrier, and every wave is then done with block j-1, so stage (j+1) & 1
+  // takes K(j+1) (direct load) and V(j+1) (from registers).  Then S^T(j),
+  // softmax and rescale; V(j+2) is loaded into registers (which the score
+  // block no longer needs) before the P V of block j.  Two workgroups share a
+  // CU, so while one wave of a SIMD runs the softmax the other (from the other
+  // workgroup) can issue MFMAs.
+  for (int j = 0; j < NB; ++j) {
     wait_vmcnt<0>();
-    lds_sync();   // V(j) and K(j+1) visible; buffers of blocks j-1 (V) and j (K) are free
-    store_v(j + 1);
-    if (j + 2 < NB) {
-      issue_k(j + 2);
-      load_v(j + 2);
+    lds_sync();
+    if (j + 1 < NB) {
+      store_v(j + 1);
+      issue_k(j + 1);
     }
-    s_and_softmax(Sn, Sc, j, st, std::false_type{});
+    s_block(S, j);
+    if (j + 1 < NB) softmax_all(S, j, st, std::false_type{});
+    else softmax_all(S, j, st, std::true_type{});
     rescale(st);
+    if (j + 2 < NB) load_v(j + 2);
     pv_block(j, st);
-  };
-  // Last block (NB-1): masked softmax, rescale, P V.
-  auto last = [&](f32x16_t (&Sl)[2]) {
-    lds_sync();   // V(NB-1), stored after the previous barrier, is visible
-    softmax_only(Sl, NB - 1, st, std::true_type{});
-    rescale(st);
-    pv_block(NB - 1, st);
-  };
-  int j = 0;
-  for (; j + 2 < NB; j += 2) {
-    step(j, Sa, Sb);
-    step(j + 1, Sb, Sa);
-  }
-  if (j + 1 < NB) {
-    step(j, Sa, Sb);
-    last(Sb);
-  } else {
-    last(Sa);
   }
 
   __syncthreads();
