@@ -141,8 +141,8 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   const int vkg = tid / DC, vdc = tid % DC;
   const bool vact = tid < (A::TN / 4) * DC;
   u32x4_t vreg[4];
-  auto issue_k = [&](int j) {
-    char* dst = smem + (j & 1) * A::STAGE;
+  auto issue_k = [&](int j, auto stage_t) {
+    char* dst = smem + decltype(stage_t)::value * A::STAGE;
     constexpr int LPR = A::KCH;                 // lanes per row in one wave-wide load
     constexpr int RPI = 64 / LPR;               // rows per instruction
 #pragma unroll
@@ -164,9 +164,9 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
       }
     }
   };
-  auto store_v = [&](int j) {
+  auto store_v = [&](auto stage_t) {
     if (vact) {
-      char* vt = smem + (j & 1) * A::STAGE + A::KB;
+      char* vt = smem + decltype(stage_t)::value * A::STAGE + A::KB;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         // keys 0..3 of d = 8 vdc + e: low (e even) or high halves of word e / 2
@@ -250,8 +250,8 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
     }
   };
   // O^T += V^T P^T for block j (V^T fragments one MFMA ahead).
-  auto pv_block = [&](int j, const SoftmaxStep& st) {
-    const char* vt = smem + (j & 1) * A::STAGE + A::KB;
+  auto pv_block = [&](auto stage_t, const SoftmaxStep& st) {
+    const char* vt = smem + decltype(stage_t)::value * A::STAGE + A::KB;
     auto vfrag = [&](int i) {   // i = (bl * 2 + s) * BD + b; permuted k order of pack_step
       const int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
       const int row = b * 32 + lr, c0 = 4 * bl + 2 * s;
@@ -270,8 +270,8 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
     }
   };
   // S^T of block j from its K rows in LDS (K fragments one MFMA ahead).
-  auto s_block = [&](f32x16_t (&S)[2], int j) {
-    const char* kb = smem + (j & 1) * A::STAGE;
+  auto s_block = [&](f32x16_t (&S)[2], auto stage_t) {
+    const char* kb = smem + decltype(stage_t)::value * A::STAGE;
     u32x4_t kf[2];
     kf[0] = kfrag(kb, 0);
 #pragma unroll
@@ -288,10 +288,12 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   f32x16_t S[2];
   SoftmaxStep st;
   // Prologue: K, V of block 0 in LDS (V transposed); V of block 1 in registers.
-  issue_k(0);
+  using S0_ = std::integral_constant<int, 0>;
+  using S1_ = std::integral_constant<int, 1>;
+  issue_k(0, S0_{});
   load_v(0);
   wait_vmcnt<0>();
-  store_v(0);
+  store_v(S0_{});
   if (NB > 1) load_v(1);
   // Step j: K(j) and V(j) are in stage j & 1 once every wave has passed the
   // barrier, and every wave is then done with block j-1, so stage (j+1) & 1
@@ -299,20 +301,25 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   // softmax and rescale; V(j+2) is loaded into registers (which the score
   // block no longer needs) before the P V of block j.  Two workgroups share a
   // CU, so while one wave of a SIMD runs the softmax the other (from the other
-  // workgroup) can issue MFMAs.
-  for (int j = 0; j < NB; ++j) {
+  // workgroup) can issue MFMAs.  The loop runs two blocks per trip so that the
+  // stage, and with it every LDS offset, is a compile-time constant.
+  auto step = [&](int j, auto stage_t, auto next_t) {
     wait_vmcnt<0>();
     lds_sync();
     if (j + 1 < NB) {
-      store_v(j + 1);
-      issue_k(j + 1);
+      store_v(next_t);
+      issue_k(j + 1, next_t);
     }
-    s_block(S, j);
+    s_block(S, stage_t);
     if (j + 1 < NB) softmax_all(S, j, st, std::false_type{});
     else softmax_all(S, j, st, std::true_type{});
     rescale(st);
     if (j + 2 < NB) load_v(j + 2);
-    pv_block(j, st);
+    pv_block(stage_t, st);
+  };
+  for (int j = 0; j < NB; j += 2) {
+    step(j, S0_{}, S1_{});
+    if (j + 1 < NB) step(j + 1, S1_{}, S0_{});
   }
 
   __syncthreads();
