@@ -62,14 +62,14 @@ __device__ __forceinline__ float lane_pair_max(float v) { return fmaxf(v, __shfl
 // when a block's maximum exceeds the one in use by more than 2^8, so
 // exp2(s - m) <= 256 and the common case skips the rescale; the final O / l
 // uses the same maximum throughout, so the result is unchanged.
-// K blocks arrive by wave-wide direct loads; V is transposed on its way into
-// LDS (rows d, 64 keys contiguous) through registers.
+// K and V blocks arrive by wave-wide direct loads, both key-major; the
+// second product reads V^T fragments with transposing LDS reads.
 // ===========================================================================
 template <int D>
 struct AttnShape {
   static constexpr int TM = 128, TN = 64, NT = 256;
   static constexpr int KB = TN * D * 2;           // K block bytes (TN rows of D*2 bytes)
-  static constexpr int VB = D * TN * 2;           // V^T block bytes (D rows of 128 bytes)
+  static constexpr int VB = TN * D * 2;           // V block bytes (TN rows of D*2 bytes)
   static constexpr int STAGE = KB + VB;
   static constexpr int LDS_RING = 2 * STAGE;
   static constexpr int LDS_STORE = TM * (D * 2 + 8);
@@ -130,52 +130,34 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   // pair up within 256 bytes: XOR with ((row >> 1) & 7).
   auto kswz = [](int row) { return A::KCH == 16 ? (row & 15) : ((row >> 1) & 7); };
   auto koff = [&](int row, int c) { return row * A::KROW + ((c ^ kswz(row)) << 4); };
-  // V^T in LDS: rows d of 64 keys (128 bytes), 16-byte chunk c of row d at
-  // position c ^ vswz(d).  vswz mixes d >> 3 into the row-pair swizzle so the
-  // transposing writes (16 rows d = 8 dc + e at a time) spread over the banks
-  // while 32 consecutive rows still read conflict-free.
-  auto vt_off = [](int d, int c) { return d * 128 + ((c ^ (((d >> 1) ^ (d >> 3)) & 7)) << 4); };
-  // Thread t moves keys 4 kg .. 4 kg + 3 of d chunk dc (8 d): four 16-byte
-  // global loads, an in-register 4 x 8 transpose, eight 8-byte LDS writes.
-  constexpr int DC = D / 8;
-  const int vkg = tid / DC, vdc = tid % DC;
-  const bool vact = tid < (A::TN / 4) * DC;
-  u32x4_t vreg[4];
-  auto issue_k = [&](int j, auto stage_t) {
-    char* dst = smem + decltype(stage_t)::value * A::STAGE;
-    constexpr int LPR = A::KCH;                 // lanes per row in one wave-wide load
-    constexpr int RPI = 64 / LPR;               // rows per instruction
+  // V rows in LDS as they are in memory (key-major, D*2 bytes), 16-byte chunk
+  // c of key row k at position c ^ vswz(k).  The second product reads V^T
+  // fragments with transposing LDS reads (see vfrag), and this swizzle keeps
+  // each 32-lane half of such a read on distinct banks.
+  auto vswz = [](int k) { return A::KCH == 16 ? 4 * (k & 3) : 4 * ((k >> 1) & 1); };
+  constexpr int LPR = A::KCH;                   // lanes per row in one wave-wide load
+  constexpr int RPI = 64 / LPR;                 // rows per instruction
+  // Wave-wide direct loads of key block j (K, or V when v_t is true) into a
+  // ring stage; rows past Lk are clamped (and masked out of P in the last
+  // block).
+  auto issue_rows = [&](int j, auto stage_t, auto v_t) {
+    constexpr bool VS = decltype(v_t)::value;
+    char* dst = smem + decltype(stage_t)::value * A::STAGE + (VS ? A::KB : 0);
+    const bf16_t* src = VS ? Vp : Kp;
+    const int64_t ld = VS ? p.ldw2 : p.ldw1;
 #pragma unroll
     for (int ins = 0; ins < A::TN / RPI / 4; ++ins) {
       const int in = wave + 4 * ins;
       const int row = in * RPI + lane / LPR;
       const int pos = lane % LPR;
-      const int c = pos ^ kswz(row);
+      const int c = pos ^ (VS ? vswz(row) : kswz(row));
       const int key = min(j * A::TN + row, Lk - 1);
-      dma16(reinterpret_cast<const char*>(Kp + (int64_t)key * p.ldw1) + c * 16, dst + in * 1024);
+      dma16(reinterpret_cast<const char*>(src + (int64_t)key * ld) + c * 16, dst + in * 1024);
     }
   };
-  auto load_v = [&](int j) {
-    if (vact) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int kk = min(j * A::TN + 4 * vkg + k, Lk - 1);
-        vreg[k] = gload16(Vp + (int64_t)kk * p.ldw2 + vdc * 8);
-      }
-    }
-  };
-  auto store_v = [&](auto stage_t) {
-    if (vact) {
-      char* vt = smem + decltype(stage_t)::value * A::STAGE + A::KB;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        // keys 0..3 of d = 8 vdc + e: low (e even) or high halves of word e / 2
-        const unsigned sel = (e & 1) ? 0x07060302u : 0x05040100u;
-        const u32x2_t w = {__builtin_amdgcn_perm(vreg[1][e >> 1], vreg[0][e >> 1], sel),
-                           __builtin_amdgcn_perm(vreg[3][e >> 1], vreg[2][e >> 1], sel)};
-        *reinterpret_cast<u32x2_t*>(vt + vt_off(8 * vdc + e, vkg >> 1) + (vkg & 1) * 8) = w;
-      }
-    }
+  auto issue_kv = [&](int j, auto stage_t) {
+    issue_rows(j, stage_t, std::false_type{});
+    issue_rows(j, stage_t, std::true_type{});
   };
   auto lds_sync = [] {   // this wave's LDS accesses are done, then a workgroup barrier
     __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14));
@@ -249,35 +231,52 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
         for (int i = 0; i < 16; ++i) Oa[b][i] *= st.corr;
     }
   };
-  // O^T += V^T P^T for block j (V^T fragments one MFMA ahead).
+  // O^T += V^T P^T for block j (V^T fragments two MFMAs ahead).  Fragment
+  // (b, s, bl) gives lane (lr, lg) V[k0 + 0..3][32 b + lr] and
+  // V[k0 + 8 + 0..3][32 b + lr], k0 = 32 bl + 16 s + 4 lg: the permuted k order
+  // of pack_step.  Each half comes from one ds_read_b64_tr_b16: in a group of
+  // 16 lanes, lane r names 4 consecutive d of key k0 + r / 4 (d offset
+  // 4 (r % 4)), and lane i receives the 4 keys of d offset i.
   auto pv_block = [&](auto stage_t, const SoftmaxStep& st) {
     const char* vt = smem + decltype(stage_t)::value * A::STAGE + A::KB;
-    auto vfrag = [&](int i) {   // i = (bl * 2 + s) * BD + b; permuted k order of pack_step
+    const int r = lane & 15;
+    const int dcol = (lane & 16) + 4 * (r & 3);       // d within the 32-block named by this lane
+    const int hb = 8 * (r & 1);
+    auto tr_read = [&](int key, int d) {
+      typedef short v4i16 __attribute__((ext_vector_type(4)));
+      const char* a = vt + key * A::KROW + (((d >> 3) ^ vswz(key)) << 4) + hb;
+      const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) v4i16*)(a));
+      return __builtin_bit_cast(u32x2_t, v);
+    };
+    auto vfrag = [&](int i) {   // i = (bl * 2 + s) * BD + b
       const int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
-      const int row = b * 32 + lr, c0 = 4 * bl + 2 * s;
-      const u32x2_t lo = lds_read8(vt + vt_off(row, c0) + 8 * lg);
-      const u32x2_t hi = lds_read8(vt + vt_off(row, c0 + 1) + 8 * lg);
+      const int k0 = 32 * bl + 16 * s + 4 * lg + (r >> 2);
+      const u32x2_t lo = tr_read(k0, 32 * b + dcol);
+      const u32x2_t hi = tr_read(k0 + 8, 32 * b + dcol);
       return u32x4_t{lo[0], lo[1], hi[0], hi[1]};
     };
-    u32x4_t vf[2];
+    u32x4_t vf[3];
     vf[0] = vfrag(0);
+    vf[1] = vfrag(1);
 #pragma unroll
     for (int i = 0; i < A::NSB; ++i) {
-      if (i + 1 < A::NSB) vf[(i + 1) & 1] = vfrag(i + 1);
+      if (i + 2 < A::NSB) vf[(i + 2) % 3] = vfrag(i + 2);
       const int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
-      Mma<bf16_t>::run(Oa[b], vf[i & 1], st.P[bl][s]);
+      Mma<bf16_t>::run(Oa[b], vf[i % 3], st.P[bl][s]);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // S^T of block j from its K rows in LDS (K fragments one MFMA ahead).
+  // S^T of block j from its K rows in LDS (K fragments two MFMAs ahead).
   auto s_block = [&](f32x16_t (&S)[2], auto stage_t) {
     const char* kb = smem + decltype(stage_t)::value * A::STAGE;
-    u32x4_t kf[2];
+    u32x4_t kf[3];
     kf[0] = kfrag(kb, 0);
+    kf[1] = kfrag(kb, 1);
 #pragma unroll
     for (int i = 0; i < A::NSA; ++i) {
-      if (i + 1 < A::NSA) kf[(i + 1) & 1] = kfrag(kb, i + 1);
-      mma_s(S, i, kf[i & 1]);
+      if (i + 2 < A::NSA) kf[(i + 2) % 3] = kfrag(kb, i + 2);
+      mma_s(S, i, kf[i % 3]);
     }
   };
   auto softmax_all = [&](f32x16_t (&Sc)[2], int j, SoftmaxStep& st, auto mask_t) {
@@ -287,34 +286,25 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
 
   f32x16_t S[2];
   SoftmaxStep st;
-  // Prologue: K, V of block 0 in LDS (V transposed); V of block 1 in registers.
+  // Prologue: K and V of block 0 on their way into LDS stage 0.
   using S0_ = std::integral_constant<int, 0>;
   using S1_ = std::integral_constant<int, 1>;
-  issue_k(0, S0_{});
-  load_v(0);
-  wait_vmcnt<0>();
-  store_v(S0_{});
-  if (NB > 1) load_v(1);
+  issue_kv(0, S0_{});
   // Step j: K(j) and V(j) are in stage j & 1 once every wave has passed the
   // barrier, and every wave is then done with block j-1, so stage (j+1) & 1
-  // takes K(j+1) (direct load) and V(j+1) (from registers).  Then S^T(j),
-  // softmax and rescale; V(j+2) is loaded into registers (which the score
-  // block no longer needs) before the P V of block j.  Two workgroups share a
+  // takes K(j+1) and V(j+1) (direct loads).  Then S^T(j), softmax, rescale
+  // and the P V of block j.  Two workgroups share a
   // CU, so while one wave of a SIMD runs the softmax the other (from the other
   // workgroup) can issue MFMAs.  The loop runs two blocks per trip so that the
   // stage, and with it every LDS offset, is a compile-time constant.
   auto step = [&](int j, auto stage_t, auto next_t) {
     wait_vmcnt<0>();
     lds_sync();
-    if (j + 1 < NB) {
-      store_v(next_t);
-      issue_k(j + 1, next_t);
-    }
+    if (j + 1 < NB) issue_kv(j + 1, next_t);
     s_block(S, stage_t);
     if (j + 1 < NB) softmax_all(S, j, st, std::false_type{});
     else softmax_all(S, j, st, std::true_type{});
     rescale(st);
-    if (j + 2 < NB) load_v(j + 2);
     pv_block(stage_t, st);
   };
   for (int j = 0; j < NB; j += 2) {
