@@ -87,7 +87,7 @@ struct AttnShape {
 
 // Softmax state of one block for one lane (query row lane % 32).
 struct SoftmaxStep {
-  float bmax, bsum, corr;
+  float bmax, corr;
   bool need;
   u32x4_t P[2][2];   // bf16 P^T fragments: [32-key half][MFMA step]
 };
@@ -96,7 +96,8 @@ template <int D>
 __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   using A = AttnShape<D>;
   __shared__ __attribute__((aligned(16))) char smem[A::LDS];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int lr = lane & 31, lg = lane >> 5;
   // XCD-aware order: workgroups go round-robin over the 8 XCDs by linear id,
   // so linear id L runs on XCD L % 8.  Give each XCD a contiguous range of
@@ -138,21 +139,36 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   constexpr int LPR = A::KCH;                   // lanes per row in one wave-wide load
   constexpr int RPI = 64 / LPR;                 // rows per instruction
   // Wave-wide direct loads of key block j (K, or V when v_t is true) into a
-  // ring stage; rows past Lk are clamped (and masked out of P in the last
-  // block).
+  // ring stage.  Load ins of a wave covers rows in * RPI .. + RPI - 1, in =
+  // wave + 4 ins; both swizzles depend on the row only through
+  // (row & 15) = (4 wave + lane / LPR) & 15 (d = 128) or the row pair
+  // ((row >> 1) & 7, d = 64), which does not change with ins, so the lane's
+  // byte offset inside its rows is fixed and the rest is wave-uniform.  Rows
+  // past Lk (the last block only) are clamped, and masked out of P.
+  const int row0 = wave * RPI + lane / LPR;     // this lane's row in load 0
+  const uint32_t kl_off = (uint32_t)((lane / LPR) * p.ldw1 * 2 + (((lane % LPR) ^ kswz(row0)) << 4));
+  const uint32_t vl_off = (uint32_t)((lane / LPR) * p.ldw2 * 2 + (((lane % LPR) ^ vswz(row0)) << 4));
   auto issue_rows = [&](int j, auto stage_t, auto v_t) {
     constexpr bool VS = decltype(v_t)::value;
     char* dst = smem + decltype(stage_t)::value * A::STAGE + (VS ? A::KB : 0);
     const bf16_t* src = VS ? Vp : Kp;
     const int64_t ld = VS ? p.ldw2 : p.ldw1;
+    if ((j + 1) * A::TN <= Lk) {
 #pragma unroll
-    for (int ins = 0; ins < A::TN / RPI / 4; ++ins) {
-      const int in = wave + 4 * ins;
-      const int row = in * RPI + lane / LPR;
-      const int pos = lane % LPR;
-      const int c = pos ^ (VS ? vswz(row) : kswz(row));
-      const int key = min(j * A::TN + row, Lk - 1);
-      dma16(reinterpret_cast<const char*>(src + (int64_t)key * ld) + c * 16, dst + in * 1024);
+      for (int ins = 0; ins < A::TN / RPI / 4; ++ins) {
+        const int in = wave + 4 * ins;
+        const char* base = reinterpret_cast<const char*>(src + (int64_t)(j * A::TN + in * RPI) * ld);
+        dma16(base + (VS ? vl_off : kl_off), dst + in * 1024);
+      }
+    } else {
+#pragma unroll
+      for (int ins = 0; ins < A::TN / RPI / 4; ++ins) {
+        const int in = wave + 4 * ins;
+        const int row = in * RPI + lane / LPR;
+        const int c = (lane % LPR) ^ (VS ? vswz(row) : kswz(row));
+        const int key = min(j * A::TN + row, Lk - 1);
+        dma16(reinterpret_cast<const char*>(src + (int64_t)key * ld) + c * 16, dst + in * 1024);
+      }
     }
   };
   auto issue_kv = [&](int j, auto stage_t) {
@@ -169,7 +185,10 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   for (int b = 0; b < A::BD; ++b)
 #pragma unroll
     for (int i = 0; i < 16; ++i) Oa[b][i] = 0.0f;
-  float m_used = -INFINITY, lrun = 0.0f;
+  float m_used = -INFINITY;
+  // Row sums l of P, accumulated by MFMAs with an all-ones A operand (every
+  // row of the block holds l of query lr), from the same bf16 P as O.
+  f32x16_t Lacc = {};
 
   // MFMA i of an S^T block (half i / DK, d step i % DK); its K fragment is
   // read two slots ahead.
@@ -199,7 +218,6 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
       const float m_eff = st.need ? mnew : m_used;
       st.corr = __builtin_amdgcn_exp2f(m_used - m_eff);   // exactly 1 when the maximum in use stays
       m_used = m_eff;
-      st.bsum = 0.0f;
     } else if (c < 14) {   // P = exp2(s * scale * log2e - m), 4 values per chunk
       const float nm = -m_used;
 #pragma unroll
@@ -211,16 +229,13 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
           pv = key < Lk ? pv : 0.0f;
         }
         S[e >> 4][e & 15] = pv;
-        st.bsum += pv;
       }
     } else if (c == 14) {
       st.P[0][0] = pack_step(S[0], 0);
       st.P[0][1] = pack_step(S[0], 1);
-      st.bsum = lane_pair_sum(st.bsum);
     } else {
       st.P[1][0] = pack_step(S[1], 0);
       st.P[1][1] = pack_step(S[1], 1);
-      lrun = lrun * st.corr + st.bsum;
     }
   };
   auto rescale = [&](const SoftmaxStep& st) {
@@ -229,6 +244,8 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
       for (int b = 0; b < A::BD; ++b)
 #pragma unroll
         for (int i = 0; i < 16; ++i) Oa[b][i] *= st.corr;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) Lacc[i] *= st.corr;
     }
   };
   // O^T += V^T P^T for block j (V^T fragments two MFMAs ahead).  Fragment
@@ -266,6 +283,9 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
       Mma<bf16_t>::run(Oa[b], vf[i % 3], st.P[bl][s]);
       __builtin_amdgcn_sched_barrier(0);
     }
+    const u32x4_t ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};   // bf16 1.0 x 8
+#pragma unroll
+    for (int q = 0; q < 4; ++q) Mma<bf16_t>::run(Lacc, ones, st.P[q >> 1][q & 1]);
   };
   // S^T of block j from its K rows in LDS (K fragments two MFMAs ahead).
   auto s_block = [&](f32x16_t (&S)[2], auto stage_t) {
@@ -313,7 +333,7 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   }
 
   __syncthreads();
-  const float inv = 1.0f / lrun;
+  const float inv = 1.0f / Lacc[0];
 #pragma unroll
   for (int b = 0; b < A::BD; ++b)
 #pragma unroll
