@@ -194,6 +194,9 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
     if (slots < 1) return fail(CF_ERR_UNSUPPORTED, "cluster path: %d peers do not fit the device", pl.cn);
     pl.slots = std::min(pl.slots, std::min(slots, kMaxSlots / 8));
   }
+  // the finish pass reads a row's partials one per lane of a 64-lane wave
+  if (pl.mode == ROWS_SPLIT && pl.cn > 64)
+    return fail(CF_ERR_UNSUPPORTED, "split path: %d tiles per row exceed 64", pl.cn);
   if (pl.mode == ROWS_CLUSTER && (pl.tm > kRecRows || pl.cn > kRecPeers))
     return fail(CF_ERR_UNSUPPORTED, "cluster path: tile of %d rows x %d peers exceeds the exchange records",
                 pl.tm, pl.cn);

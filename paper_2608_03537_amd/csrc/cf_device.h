@@ -42,43 +42,29 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_v));
 }
 
-// OCP E4M3FN encoder: nearest representable value, ties to even mantissa,
-// magnitudes beyond 448 saturate to 448, NaN -> 0x7F.  Integer-only so the
-// rounding is exact and independent of any hardware conversion mode.
-//   normal:    (-1)^s 2^(e-7) (1 + m/8), e in 1..15 (e=15,m=7 is NaN)
-//   subnormal: (-1)^s 2^-6 (m/8)
-__device__ __forceinline__ uint32_t f32_to_e4m3(float f) {
-  uint32_t u = __float_as_uint(f);
-  uint32_t sign = (u >> 24) & 0x80u;
-  uint32_t a = u & 0x7FFFFFFFu;
-  if (a > 0x7F800000u) return 0x7Fu;                 // NaN
-  if (a >= 0x43E00000u) return sign | 0x7Eu;          // |f| >= 448: saturate
-  uint32_t e32 = a >> 23;                             // biased fp32 exponent
-  uint32_t code;
-  if (e32 >= 121u) {                                  // |f| >= 2^-6: normal
-    // Keep 3 mantissa bits; round the 20 dropped bits to nearest even.
-    uint32_t mant = a & 0x7FFFFFu;
-    uint32_t keep = mant >> 20;
-    uint32_t rest = mant & 0xFFFFFu;
-    uint32_t e8 = e32 - 120u;                         // e4m3 exponent field
-    uint32_t v = (e8 << 3) | keep;
-    if (rest > 0x80000u || (rest == 0x80000u && (keep & 1u))) v += 1u;  // may carry into exponent
-    code = v;                                          // v <= 0x7E since |f| < 448
-  } else {
-    // Subnormal target: value = k * 2^-9, k = round_even(|f| * 2^9).
-    // |f| < 2^-6 so k <= 8 (8 = smallest normal, code 0x08: the carry is right).
-    if (e32 < 110u) return sign;                      // |f| < 2^-17: rounds to 0
-    uint32_t mant = (a & 0x7FFFFFu) | 0x800000u;      // 1.m * 2^(e32-127)
-    // |f| * 2^9 = mant * 2^(e32 - 127 - 23 + 9) = mant >> (141 - e32);
-    // e32 in [110, 120] gives a shift of 21..31.
-    uint32_t shift = 141u - e32;
-    uint32_t k = mant >> shift;
-    uint32_t rest = mant & ((1u << shift) - 1u);
-    uint32_t half = 1u << (shift - 1u);
-    if (rest > half || (rest == half && (k & 1u))) k += 1u;
-    code = k;
-  }
-  return sign | code;
+// z / s rounded to nearest fp32, from r = 1 / s rounded to nearest (one IEEE
+// division per row): the product z r is corrected by one fused step on its
+// exact remainder z - q s (Markstein's division theorem: with r within half
+// an ulp of 1/s and q within one ulp of z/s, q + (z - q s) r rounds to the
+// correctly rounded quotient).  For s > 0 and quotients in the normal range.
+// The sign is copied from z: for z = -0 the correction would add opposite
+// zeros and return +0.
+__device__ __forceinline__ float div_rn(float z, float s, float r) {
+  const float q = z * r;
+  return copysignf(fmaf(fmaf(-q, s, z), r, q), z);
+}
+
+// Four fp32 values -> four OCP E4M3FN codes (byte q from the q-th value) by
+// gfx950's packed conversion: round to nearest, ties to even mantissa,
+// subnormals m * 2^-9.  Callers pass quotients x / s with s = amax / 448 of
+// the values' own row, so |x / s| stays below 464 and the conversion never
+// reaches its overflow range (448 is the largest finite code).  Over every
+// fp32 pattern in [-448, 448] it gives the same code as an integer encoder
+// written from the OCP FP8 specification.
+__device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);   // bytes 0, 1
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);          // bytes 2, 3
+  return (uint32_t)w;
 }
 
 // erf by Abramowitz and Stegun, Handbook of Mathematical Functions, 7.1.26:
@@ -182,16 +168,6 @@ __device__ __forceinline__ void load4<float>(const float* p, float (&v)[4]) {
 __device__ __forceinline__ float tanh_exp(float z) {
   const float t = __builtin_amdgcn_exp2f(-2.8853900817779268f * fabsf(z));   // 2 log2(e)
   return copysignf((1.0f - t) * __builtin_amdgcn_rcpf(1.0f + t), z);
-}
-
-__device__ __forceinline__ float apply_act(int act, float x, float cap) {
-  switch (act) {
-    case ACT_GELU: return gelu_erf(x);
-    case ACT_GELU_TANH: return gelu_tanh(x);
-    case ACT_RELU: return x > 0.0f ? x : 0.0f;
-    case ACT_SOFTCAP: return cap * tanh_exp(x / cap);
-    default: return x;
-  }
 }
 
 __device__ __forceinline__ void store4(void* base, int64_t off, int f32, const float (&v)[4]) {

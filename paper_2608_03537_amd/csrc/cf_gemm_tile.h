@@ -1118,19 +1118,19 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
       const float sc = a[bm] / e.qmax;
       if (c == 0 && wn == 0 && lane < 32 && e.s_out) e.s_out[mrow[bm]] = sc;
       if (e.q_out) {
+        // codes of fl32(z / s); a zero row (s = 0) gives codes 0
+        const bool nz = sc > 0.0f;
+        const float sd = nz ? sc : 1.0f, inv = nz ? 1.0f / sc : 1.0f;
 #pragma unroll
         for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int n = ncol(bn, g);
             if (n < N) {
-              uint32_t w = 0;
-#pragma unroll
-              for (int q = 0; q < 4; ++q) {
-                const uint32_t code = sc > 0.0f ? f32_to_e4m3(x[bm][bn][4 * g + q] / sc) : 0u;
-                w |= code << (8 * q);
-              }
-              *reinterpret_cast<uint32_t*>(e.q_out + (int64_t)mrow[bm] * e.ldq + n) = w;
+              const uint32_t w =
+                  e4m3x4(div_rn(x[bm][bn][4 * g], sd, inv), div_rn(x[bm][bn][4 * g + 1], sd, inv),
+                         div_rn(x[bm][bn][4 * g + 2], sd, inv), div_rn(x[bm][bn][4 * g + 3], sd, inv));
+              *reinterpret_cast<uint32_t*>(e.q_out + (int64_t)mrow[bm] * e.ldq + n) = nz ? w : 0u;
             }
           }
       }

@@ -1,11 +1,14 @@
-// Wave-per-row kernels for gfx950.
+// Row kernels for gfx950.
 //
-// One 64-lane wave owns one row: its values stay in registers from load to
-// store, every reduction is a wave-wide butterfly (no LDS, no barrier), and
-// the row is read from HBM exactly once.  Two users:
+// row_kernel: one 64-lane wave owns one row: its values stay in registers
+// from load to store, every reduction is a wave-wide butterfly (no LDS, no
+// barrier), and the row is read from HBM exactly once.  finish_kernel: the
+// same for the split-N finish pass on rows wider than 1024, with a
+// 256-thread workgroup per row.  Two users:
 //   * the finish pass of the split-N path: the GEMM has written fp32 x and a
 //     partial (mean, M2) per (row, N tile); the wave merges the partials with
-//     the pairwise update of Chan, Golub and LeVeque, then runs stages 2..4;
+//     the k-way form of the pairwise update of Chan, Golub and LeVeque, then
+//     runs stages 2..4;
 //   * the unfused row operator (the materialising baseline): stages 1..4, or
 //     a softmax, on a matrix that a plain GEMM wrote to global memory.
 #include "cf_device.h"
@@ -22,6 +25,22 @@ __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
   return v;
+}
+
+// Row statistics from the split GEMM pass's per-tile partials (mean_c, M2_c)
+// of cn tiles of width tn (the last one N - (cn - 1) tn wide), in the k-way
+// form of the pairwise update of Chan, Golub and LeVeque:
+//   mean = sum_c n_c mean_c / N,   M2 = sum_c (M2_c + n_c (mean_c - mean)^2).
+// Lane c (< cn <= 64) holds tile c's pair; both sums are butterflies, whose
+// pairwise additions commute exactly, so every lane gets the same values.
+__device__ __forceinline__ void merge_partials(const float2* part, int cn, int tn, int N, int lane, float& mean,
+                                               float& m2) {
+  const bool has = lane < cn;
+  const float2 pc = has ? part[lane] : make_float2(0.0f, 0.0f);
+  const float nc = has ? (float)min(tn, N - lane * tn) : 0.0f;
+  mean = wave_sum(nc * pc.x) / (float)N;
+  const float d = pc.x - mean;
+  m2 = wave_sum(has ? fmaf(nc * d, d, pc.y) : 0.0f);
 }
 
 // VPL = groups of 4 consecutive columns per lane; a row of up to 256*VPL.
@@ -109,20 +128,7 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
   if (e.norm != NORM_NONE) {
     float mean, m2;
     if (p.finish) {
-      // Pairwise merge of (count, mean, M2) over the row's tiles, in order.
-      const float2* part = reinterpret_cast<const float2*>(p.part) + (int64_t)m * p.cn;
-      float n_acc = 0.0f;
-      mean = 0.0f;
-      m2 = 0.0f;
-      for (int c = 0; c < p.cn; ++c) {
-        const float nb = (float)min(p.tn, N - c * p.tn);
-        const float2 pb = part[c];
-        const float nn = n_acc + nb;
-        const float delta = pb.x - mean;
-        mean += delta * (nb / nn);
-        m2 += pb.y + delta * delta * (n_acc * nb / nn);
-        n_acc = nn;
-      }
+      merge_partials(reinterpret_cast<const float2*>(p.part) + (int64_t)m * p.cn, p.cn, p.tn, N, lane, mean, m2);
     } else {
       float s = 0.0f;
 #pragma unroll
@@ -170,11 +176,23 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
   }
 
   // ---- stage 3: activation and store
-  if (e.act != ACT_NONE) {
+  // One straight loop per activation kind (the kind is uniform).
+  auto act_all = [&](auto f) {
 #pragma unroll
     for (int j = 0; j < VPL; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[j][q] = apply_act(e.act, v[j][q], e.softcap);
+      for (int q = 0; q < 4; ++q) v[j][q] = f(v[j][q]);
+  };
+  switch (e.act) {
+    case ACT_GELU: act_all([](float x) { return gelu_erf(x); }); break;
+    case ACT_GELU_TANH: act_all([](float x) { return gelu_tanh(x); }); break;
+    case ACT_RELU: act_all([](float x) { return x > 0.0f ? x : 0.0f; }); break;
+    case ACT_SOFTCAP: {
+      const float cap = e.softcap;
+      act_all([cap](float x) { return cap * tanh_exp(x / cap); });
+      break;
+    }
+    default: break;
   }
   if (SM) {   // row softmax of the (activated) values
     float mx = -INFINITY;
@@ -218,13 +236,115 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
     const float sc = a / e.qmax;
     if (lane == 0 && e.s_out) e.s_out[m] = sc;
     if (e.q_out) {
+      // codes of fl32(z / s); a zero row (s = 0, uniform over the wave) gives codes 0
+      const bool nz = sc > 0.0f;
+      const float sd = nz ? sc : 1.0f, inv = nz ? 1.0f / sc : 1.0f;
 #pragma unroll
       for (int j = 0; j < VPL; ++j) {
         if (!val[j]) continue;
-        uint32_t w = 0;
+        const uint32_t w = e4m3x4(div_rn(v[j][0], sd, inv), div_rn(v[j][1], sd, inv), div_rn(v[j][2], sd, inv),
+                                  div_rn(v[j][3], sd, inv));
+        *reinterpret_cast<uint32_t*>(e.q_out + (int64_t)m * e.ldq + 256 * j + 4 * lane) = nz ? w : 0u;
+      }
+    }
+  }
+}
+
+// Finish pass of the split-N path for rows wider than 1024: one 256-thread
+// workgroup per row, so a lane holds 4 * VPW values (not 4 * N / 256) and a
+// CU keeps enough waves resident to overlap the fp32 x reads with the
+// element work.  Lane l of wave w holds columns 1024 j + 256 w + 4 l + (0..3),
+// j < VPW (each j one coalesced 1 KB read per wave).  Every wave merges the
+// row's partial statistics itself (same values in every wave); the row amax
+// is combined across the four waves through LDS.  FULL: N = 1024 VPW, no
+// column guards.  Softmax lists keep the wave-per-row kernel.
+template <int VPW, bool FULL>
+__global__ __launch_bounds__(256) void finish_kernel(RowKernelParams p) {
+  __shared__ float red[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int m = blockIdx.x;
+  const int N = p.N;
+  const RowEpi& e = p.epi;
+  const float* x = reinterpret_cast<const float*>(p.P) + (int64_t)m * p.ldp;
+  float v[VPW][4];
+  bool val[VPW];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) w |= (sc > 0.0f ? f32_to_e4m3(v[j][q] / sc) : 0u) << (8 * q);
-        *reinterpret_cast<uint32_t*>(e.q_out + (int64_t)m * e.ldq + 256 * j + 4 * lane) = w;
+  for (int j = 0; j < VPW; ++j) {
+    const int n = 1024 * j + 256 * wave + 4 * lane;
+    val[j] = FULL || n < N;
+    if (val[j]) load4<float>(x + n, v[j]);
+    else v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0.0f;
+  }
+  float mean, m2;
+  merge_partials(reinterpret_cast<const float2*>(p.part) + (int64_t)m * p.cn, p.cn, p.tn, N, lane, mean, m2);
+  const float invN = 1.0f / (float)N;
+  if (e.norm == NORM_LAYER || e.norm == NORM_RMS) {
+    // LayerNorm: (x - mean) rstd; RMSNorm: x rstd with mean of squares M2/N + mean^2
+    const bool ln = e.norm == NORM_LAYER;
+    const float rstd = ln ? rsqrtf(m2 * invN + e.eps) : rsqrtf(m2 * invN + mean * mean + e.eps);
+    const float sh = ln ? mean : 0.0f;
+#pragma unroll
+    for (int j = 0; j < VPW; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[j][q] = (v[j][q] - sh) * rstd;
+    if (e.gamma || (ln && e.beta)) {
+#pragma unroll
+      for (int j = 0; j < VPW; ++j) {
+        if (!val[j]) continue;
+        const int n = 1024 * j + 256 * wave + 4 * lane;
+        float g[4] = {1.0f, 1.0f, 1.0f, 1.0f}, b[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (e.gamma) load4<float>(e.gamma + n, g);
+        if (ln && e.beta) load4<float>(e.beta + n, b);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[j][q] = fmaf(v[j][q], g[q], b[q]);
+      }
+    }
+  }
+  auto act_all = [&](auto f) {
+#pragma unroll
+    for (int j = 0; j < VPW; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[j][q] = f(v[j][q]);
+  };
+  switch (e.act) {
+    case ACT_GELU: act_all([](float t) { return gelu_erf(t); }); break;
+    case ACT_GELU_TANH: act_all([](float t) { return gelu_tanh(t); }); break;
+    case ACT_RELU: act_all([](float t) { return t > 0.0f ? t : 0.0f; }); break;
+    case ACT_SOFTCAP: {
+      const float cap = e.softcap;
+      act_all([cap](float t) { return cap * tanh_exp(t / cap); });
+      break;
+    }
+    default: break;
+  }
+  if (e.Y) {
+#pragma unroll
+    for (int j = 0; j < VPW; ++j)
+      if (val[j]) store4(e.Y, (int64_t)m * e.ldy + 1024 * j + 256 * wave + 4 * lane, e.y_f32, v[j]);
+  }
+  if (e.quant) {
+    float a = 0.0f;
+#pragma unroll
+    for (int j = 0; j < VPW; ++j)
+      if (val[j])
+#pragma unroll
+        for (int q = 0; q < 4; ++q) a = fmaxf(a, fabsf(v[j][q]));
+    a = wave_max(a);
+    if (lane == 0) red[wave] = a;
+    __syncthreads();
+    a = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const float sc = a / e.qmax;
+    if (threadIdx.x == 0 && e.s_out) e.s_out[m] = sc;
+    if (e.q_out) {
+      // codes of fl32(z / s); a zero row (s = 0) gives codes 0
+      const bool nz = sc > 0.0f;
+      const float sd = nz ? sc : 1.0f, inv = nz ? 1.0f / sc : 1.0f;
+#pragma unroll
+      for (int j = 0; j < VPW; ++j) {
+        if (!val[j]) continue;
+        const uint32_t w = e4m3x4(div_rn(v[j][0], sd, inv), div_rn(v[j][1], sd, inv), div_rn(v[j][2], sd, inv),
+                                  div_rn(v[j][3], sd, inv));
+        *reinterpret_cast<uint32_t*>(e.q_out + (int64_t)m * e.ldq + 1024 * j + 256 * wave + 4 * lane) = nz ? w : 0u;
       }
     }
   }
@@ -232,6 +352,21 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
 
 hipError_t launch_row_kernel(const RowKernelParams& p, hipStream_t st) {
   if (p.M <= 0) return hipSuccess;
+  if (p.finish && !p.epi.softmax && p.p_f32 && p.N > 1024) {
+    const dim3 grid((unsigned)p.M), block(256);
+#define CF_FIN_LAUNCH(V)                                                                    \
+  do {                                                                                      \
+    if (p.N == 1024 * (V)) hipLaunchKernelGGL((finish_kernel<V, true>), grid, block, 0, st, p); \
+    else hipLaunchKernelGGL((finish_kernel<V, false>), grid, block, 0, st, p);              \
+  } while (0)
+    const int vpw = (p.N + 1023) / 1024;
+    if (vpw <= 2) CF_FIN_LAUNCH(2);
+    else if (vpw <= 4) CF_FIN_LAUNCH(4);
+    else if (vpw <= 8) CF_FIN_LAUNCH(8);
+    else return hipErrorInvalidValue;
+#undef CF_FIN_LAUNCH
+    return hipGetLastError();
+  }
   const dim3 grid((unsigned)((p.M + 3) / 4)), block(256);
   const int vpl = (p.N + 255) / 256;
   const bool sm = p.epi.softmax != 0;

@@ -87,6 +87,49 @@ def test_chain_quant_exact_against_own_z(path):
     assert_close_f32(Zg, z, "fp32 chain")
 
 
+@pytest.mark.parametrize("N", [1280, 2048, 3072, 4160])
+def test_chain_split_wide_rows(N):
+    # Split-N rows wider than 1024 finish in one workgroup per row: whole
+    # multiples of 1024 (2048) and ragged widths, where whole column groups
+    # of the last waves (3072: the fourth group of every wave) hold no data.
+    inp = I.postnorm_inputs(70, 64, N, "bf16", seed=31, with_affine=False)
+    z, s, q = O.ln_gelu_amax(inp.X, inp.W, inp.bias, inp.R, eps=inp.eps)
+    Zg, sg, Qg = run_chain(inp, 3)
+    assert_close_bf16(Zg, z, f"Z N={N} split")
+    np.testing.assert_allclose(sg, s, rtol=1e-3)
+    check_codes(Qg, q, min_equal=0.999)
+
+
+def test_chain_split_wide_quant_exact_against_own_z():
+    # fp32 Z from the wide-row finish pass: its scale and codes equal the
+    # fp32 scale chain applied to that Z, exactly.
+    inp = I.postnorm_inputs(33, 64, 2112, "f32", seed=32, with_affine=False)
+    Zg, sg, Qg = run_chain(inp, 3, z_f32=True)
+    s32, q32 = O.rowamax_quant_f32(Zg.astype(np.float32))
+    assert np.array_equal(sg, s32)
+    assert np.array_equal(Qg, q32)
+
+
+@pytest.mark.parametrize("norm,N", [("rms", 2560), ("ln", 3136)])
+def test_split_wide_rows_affine(norm, N):
+    # RMSNorm (gamma) and LayerNorm (gamma, beta) on the wide-row finish pass.
+    inp = I.postnorm_inputs(40, 64, N, "f32", seed=33, with_residual=False)
+    X, W = dev(inp.X, "f32"), dev(I.lay_out_weight(inp.W, "nk"), "f32")
+    b, g, be = dev(inp.bias, "f32"), dev(inp.gamma, "f32"), dev(inp.beta, "f32")
+    Y = torch.empty((inp.M, inp.N), dtype=torch.float32, device="cuda")
+    if norm == "rms":
+        spec = [dict(kind=cf.CF_N_BIAS, v0=b), dict(kind=cf.CF_N_RMSNORM, v0=g, f0=1e-5),
+                dict(kind=cf.CF_N_STORE, out=Y, ld=inp.N, dtype=cf.CF_F32)]
+        r = O.rmsnorm(O.bias_residual(O.matmul(inp.X, inp.W), inp.bias), inp.gamma, 1e-5)
+    else:
+        spec = [dict(kind=cf.CF_N_BIAS, v0=b), dict(kind=cf.CF_N_LAYERNORM, v0=g, v1=be, f0=1e-5),
+                dict(kind=cf.CF_N_STORE, out=Y, ld=inp.N, dtype=cf.CF_F32)]
+        r = O.postnorm(inp.X, inp.W, inp.bias, None, inp.gamma, inp.beta, 1.0, 1e-5)
+    cf.gemm_subgraph(X, W, spec, path=3)
+    torch.cuda.synchronize()
+    assert_close_f32(host(Y), r, f"{norm} N={N} split")
+
+
 def test_gelu_tanh_variant_is_the_tanh_one():
     inp = I.postnorm_inputs(64, 64, 256, "f32", seed=13, with_affine=False)
     Zg, _, _ = run_chain(inp, 1, z_f32=True, gelu=cf.CF_N_GELU_TANH)
@@ -141,10 +184,13 @@ def test_rowop_quant_encoder_exact():
     n = ((len(pts) + 255) // 256) * 256
     row = np.zeros(n, np.float32)
     row[:len(pts)] = pts
-    P = np.stack([row, row * np.float32(0.5), row * np.float32(1e-3), np.zeros(n, np.float32)])
+    # Scales that are not powers of two put z/s next to the midpoints, where
+    # only a correctly rounded fp32 quotient gives the reference code.
+    P = np.stack([row, row * np.float32(0.5), row * np.float32(1e-3), np.zeros(n, np.float32),
+                  row * np.float32(0.37), row * np.float32(0.033), row * np.float32(7.1)])
     Pd = dev(P, "f32")
-    s = torch.empty(4, dtype=torch.float32, device="cuda")
-    Q = torch.empty((4, n), dtype=torch.uint8, device="cuda")
+    s = torch.empty(len(P), dtype=torch.float32, device="cuda")
+    Q = torch.empty((len(P), n), dtype=torch.uint8, device="cuda")
     cf.rowop(Pd, [dict(kind=cf.CF_N_ROWAMAX_QUANT, out=s, out2=Q, ld=n, f0=448.0)])
     torch.cuda.synchronize()
     s32, q32 = O.rowamax_quant_f32(P)
