@@ -2,9 +2,9 @@
 //
 // row_kernel: one 64-lane wave owns one row: its values stay in registers
 // from load to store, every reduction is a wave-wide butterfly (no LDS, no
-// barrier), and the row is read from HBM exactly once.  finish_kernel: the
-// same for the split-N finish pass on rows wider than 1024, with a
-// 256-thread workgroup per row.  Two users:
+// barrier), and the row is read from HBM exactly once.  wide_row_kernel:
+// the same for rows wider than 1024, with a 256-thread workgroup per row.
+// Two users:
 //   * the finish pass of the split-N path: the GEMM has written fp32 x and a
 //     partial (mean, M2) per (row, N tile); the wave merges the partials with
 //     the k-way form of the pairwise update of Chan, Golub and LeVeque, then
@@ -176,23 +176,23 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
   }
 
   // ---- stage 3: activation and store
-  // One straight loop per activation kind (the kind is uniform).
-  auto act_all = [&](auto f) {
+  // The kind is switched per element here: one loop per kind would keep
+  // every kind's temporaries of all 4 * VPL values live at once (74 against
+  // 48 VGPRs for VPL = 4, and two fewer resident waves per SIMD).
+  if (e.act != ACT_NONE) {
 #pragma unroll
     for (int j = 0; j < VPL; ++j)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[j][q] = f(v[j][q]);
-  };
-  switch (e.act) {
-    case ACT_GELU: act_all([](float x) { return gelu_erf(x); }); break;
-    case ACT_GELU_TANH: act_all([](float x) { return gelu_tanh(x); }); break;
-    case ACT_RELU: act_all([](float x) { return x > 0.0f ? x : 0.0f; }); break;
-    case ACT_SOFTCAP: {
-      const float cap = e.softcap;
-      act_all([cap](float x) { return cap * tanh_exp(x / cap); });
-      break;
-    }
-    default: break;
+      for (int q = 0; q < 4; ++q) {
+        const float x = v[j][q];
+        switch (e.act) {
+          case ACT_GELU: v[j][q] = gelu_erf(x); break;
+          case ACT_GELU_TANH: v[j][q] = gelu_tanh(x); break;
+          case ACT_RELU: v[j][q] = x > 0.0f ? x : 0.0f; break;
+          case ACT_SOFTCAP: v[j][q] = e.softcap * tanh_exp(x / e.softcap); break;
+          default: break;
+        }
+      }
   }
   if (SM) {   // row softmax of the (activated) values
     float mx = -INFINITY;
@@ -250,35 +250,88 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
   }
 }
 
-// Finish pass of the split-N path for rows wider than 1024: one 256-thread
-// workgroup per row, so a lane holds 4 * VPW values (not 4 * N / 256) and a
-// CU keeps enough waves resident to overlap the fp32 x reads with the
-// element work.  Lane l of wave w holds columns 1024 j + 256 w + 4 l + (0..3),
-// j < VPW (each j one coalesced 1 KB read per wave).  Every wave merges the
-// row's partial statistics itself (same values in every wave); the row amax
-// is combined across the four waves through LDS.  FULL: N = 1024 VPW, no
-// column guards.  Softmax lists keep the wave-per-row kernel.
+// Rows wider than 1024 (split-N finish pass and the unfused row operator,
+// softmax lists excepted): one 256-thread workgroup per row, so a lane holds
+// 4 * VPW values (not 4 * N / 256) and a CU keeps enough waves resident to
+// overlap the row reads with the element work.  Lane l of wave w holds
+// columns 1024 j + 256 w + 4 l + (0..3), j < VPW (each j one coalesced read
+// per wave).  Row sums and the amax are combined across the four waves
+// through LDS in a fixed order, so every wave gets the same values; the
+// finish pass merges the partial statistics in every wave.  FULL: N = 1024
+// VPW, no column guards.
 template <int VPW, bool FULL>
-__global__ __launch_bounds__(256) void finish_kernel(RowKernelParams p) {
-  __shared__ float red[4];
+__global__ __launch_bounds__(256) void wide_row_kernel(RowKernelParams p) {
+  __shared__ float red[3][4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int m = blockIdx.x;
   const int N = p.N;
   const RowEpi& e = p.epi;
-  const float* x = reinterpret_cast<const float*>(p.P) + (int64_t)m * p.ldp;
+  auto col = [&](int j) { return 1024 * j + 256 * wave + 4 * lane; };
+  // sum over the workgroup of one value per lane (reduction slot r)
+  auto block_sum = [&](float t, int r) {
+    t = wave_sum(t);
+    if (lane == 0) red[r][wave] = t;
+    __syncthreads();
+    return (red[r][0] + red[r][1]) + (red[r][2] + red[r][3]);
+  };
   float v[VPW][4];
   bool val[VPW];
 #pragma unroll
   for (int j = 0; j < VPW; ++j) {
-    const int n = 1024 * j + 256 * wave + 4 * lane;
-    val[j] = FULL || n < N;
-    if (val[j]) load4<float>(x + n, v[j]);
-    else v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0.0f;
+    val[j] = FULL || col(j) < N;
+    if (val[j]) {
+      if (p.p_f32) load4<float>(reinterpret_cast<const float*>(p.P) + (int64_t)m * p.ldp + col(j), v[j]);
+      else load4<bf16_t>(reinterpret_cast<const bf16_t*>(p.P) + (int64_t)m * p.ldp + col(j), v[j]);
+    } else {
+      v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0.0f;
+    }
   }
-  float mean, m2;
-  merge_partials(reinterpret_cast<const float2*>(p.part) + (int64_t)m * p.cn, p.cn, p.tn, N, lane, mean, m2);
-  const float invN = 1.0f / (float)N;
+  if (!p.finish) {
+    // stage 1; only the terms that are given are added (x + 0 would turn -0 into +0)
+#pragma unroll
+    for (int j = 0; j < VPW; ++j) {
+      if (!val[j]) continue;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[j][q] *= e.alpha;
+      if (e.bias) {
+        float b[4];
+        load4<float>(e.bias + col(j), b);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[j][q] += b[q];
+      }
+      if (e.R) {
+        float r[4];
+        if (e.r_f32) load4<float>(reinterpret_cast<const float*>(e.R) + (int64_t)m * e.ldr + col(j), r);
+        else load4<bf16_t>(reinterpret_cast<const bf16_t*>(e.R) + (int64_t)m * e.ldr + col(j), r);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[j][q] += r[q];
+      }
+    }
+  }
   if (e.norm == NORM_LAYER || e.norm == NORM_RMS) {
+    float mean, m2;
+    if (p.finish) {
+      merge_partials(reinterpret_cast<const float2*>(p.part) + (int64_t)m * p.cn, p.cn, p.tn, N, lane, mean, m2);
+    } else {
+      // two passes: mean, then the sum of squared deviations (padding columns skipped)
+      float t = 0.0f;
+#pragma unroll
+      for (int j = 0; j < VPW; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) t += v[j][q];
+      mean = block_sum(t, 0) / (float)N;
+      t = 0.0f;
+#pragma unroll
+      for (int j = 0; j < VPW; ++j)
+        if (val[j])
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float d = v[j][q] - mean;
+            t = fmaf(d, d, t);
+          }
+      m2 = block_sum(t, 1);
+    }
+    const float invN = 1.0f / (float)N;
     // LayerNorm: (x - mean) rstd; RMSNorm: x rstd with mean of squares M2/N + mean^2
     const bool ln = e.norm == NORM_LAYER;
     const float rstd = ln ? rsqrtf(m2 * invN + e.eps) : rsqrtf(m2 * invN + mean * mean + e.eps);
@@ -291,10 +344,9 @@ __global__ __launch_bounds__(256) void finish_kernel(RowKernelParams p) {
 #pragma unroll
       for (int j = 0; j < VPW; ++j) {
         if (!val[j]) continue;
-        const int n = 1024 * j + 256 * wave + 4 * lane;
         float g[4] = {1.0f, 1.0f, 1.0f, 1.0f}, b[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (e.gamma) load4<float>(e.gamma + n, g);
-        if (ln && e.beta) load4<float>(e.beta + n, b);
+        if (e.gamma) load4<float>(e.gamma + col(j), g);
+        if (ln && e.beta) load4<float>(e.beta + col(j), b);
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[j][q] = fmaf(v[j][q], g[q], b[q]);
       }
@@ -320,7 +372,7 @@ __global__ __launch_bounds__(256) void finish_kernel(RowKernelParams p) {
   if (e.Y) {
 #pragma unroll
     for (int j = 0; j < VPW; ++j)
-      if (val[j]) store4(e.Y, (int64_t)m * e.ldy + 1024 * j + 256 * wave + 4 * lane, e.y_f32, v[j]);
+      if (val[j]) store4(e.Y, (int64_t)m * e.ldy + col(j), e.y_f32, v[j]);
   }
   if (e.quant) {
     float a = 0.0f;
@@ -330,9 +382,9 @@ __global__ __launch_bounds__(256) void finish_kernel(RowKernelParams p) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) a = fmaxf(a, fabsf(v[j][q]));
     a = wave_max(a);
-    if (lane == 0) red[wave] = a;
+    if (lane == 0) red[2][wave] = a;
     __syncthreads();
-    a = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    a = fmaxf(fmaxf(red[2][0], red[2][1]), fmaxf(red[2][2], red[2][3]));
     const float sc = a / e.qmax;
     if (threadIdx.x == 0 && e.s_out) e.s_out[m] = sc;
     if (e.q_out) {
@@ -344,7 +396,7 @@ __global__ __launch_bounds__(256) void finish_kernel(RowKernelParams p) {
         if (!val[j]) continue;
         const uint32_t w = e4m3x4(div_rn(v[j][0], sd, inv), div_rn(v[j][1], sd, inv), div_rn(v[j][2], sd, inv),
                                   div_rn(v[j][3], sd, inv));
-        *reinterpret_cast<uint32_t*>(e.q_out + (int64_t)m * e.ldq + 1024 * j + 256 * wave + 4 * lane) = nz ? w : 0u;
+        *reinterpret_cast<uint32_t*>(e.q_out + (int64_t)m * e.ldq + col(j)) = nz ? w : 0u;
       }
     }
   }
@@ -352,12 +404,12 @@ __global__ __launch_bounds__(256) void finish_kernel(RowKernelParams p) {
 
 hipError_t launch_row_kernel(const RowKernelParams& p, hipStream_t st) {
   if (p.M <= 0) return hipSuccess;
-  if (p.finish && !p.epi.softmax && p.p_f32 && p.N > 1024) {
+  if (!p.epi.softmax && !p.softmax && p.N > 1024) {
     const dim3 grid((unsigned)p.M), block(256);
 #define CF_FIN_LAUNCH(V)                                                                    \
   do {                                                                                      \
-    if (p.N == 1024 * (V)) hipLaunchKernelGGL((finish_kernel<V, true>), grid, block, 0, st, p); \
-    else hipLaunchKernelGGL((finish_kernel<V, false>), grid, block, 0, st, p);              \
+    if (p.N == 1024 * (V)) hipLaunchKernelGGL((wide_row_kernel<V, true>), grid, block, 0, st, p); \
+    else hipLaunchKernelGGL((wide_row_kernel<V, false>), grid, block, 0, st, p);            \
   } while (0)
     const int vpw = (p.N + 1023) / 1024;
     if (vpw <= 2) CF_FIN_LAUNCH(2);

@@ -200,6 +200,48 @@ def test_rowop_quant_encoder_exact():
     assert len(bad) == 0, [(int(i), int(j), float(P[i, j]), hex(qg[i, j]), hex(q32[i, j])) for i, j in bad[:8]]
 
 
+@pytest.mark.parametrize("N,p_dtype", [(3072, torch.bfloat16), (4160, torch.float32)])
+def test_rowop_wide_rows_chain(N, p_dtype):
+    # The unfused row operator on rows wider than 1024 (one workgroup per
+    # row): bias, residual, LayerNorm, GELU, store, row amax and E4M3 codes
+    # over a materialised product (bf16 or fp32), against the oracle.
+    inp = I.postnorm_inputs(45, 64, N, "bf16", seed=34, with_affine=False)
+    X, W = dev(inp.X), dev(I.lay_out_weight(inp.W, "nk"))
+    b, R = dev(inp.bias, "f32"), dev(inp.R)
+    P = cf.gemm(X, W, out_dtype=p_dtype)
+    Z = torch.empty((inp.M, N), dtype=torch.bfloat16, device="cuda")
+    s = torch.empty(inp.M, dtype=torch.float32, device="cuda")
+    Q = torch.empty((inp.M, N), dtype=torch.uint8, device="cuda")
+    cf.rowop(P, [dict(kind=cf.CF_N_BIAS, v0=b), dict(kind=cf.CF_N_RESIDUAL, **{"in": R}, ld=N, dtype=cf.CF_BF16),
+                 dict(kind=cf.CF_N_LAYERNORM, f0=1e-5), dict(kind=cf.CF_N_GELU),
+                 dict(kind=cf.CF_N_STORE, out=Z, ld=N, dtype=cf.CF_BF16),
+                 dict(kind=cf.CF_N_ROWAMAX_QUANT, out=s, out2=Q, ld=N, f0=448.0)])
+    torch.cuda.synchronize()
+    if p_dtype == torch.bfloat16:
+        # the oracle runs on the same bf16-rounded product the row pass reads
+        Pr = host(P).astype(np.float64)
+        z = O.gelu_erf(O.layernorm(O.bias_residual(Pr, inp.bias, inp.R), eps=1e-5))
+        sr, q = O.rowamax_quant(z)
+    else:
+        z, sr, q = O.ln_gelu_amax(inp.X, inp.W, inp.bias, inp.R, eps=1e-5)
+    assert_close_bf16(host(Z), z, f"unfused wide chain N={N}")
+    np.testing.assert_allclose(s.cpu().numpy(), sr, rtol=1e-3)
+    check_codes(Q.cpu().numpy(), q, min_equal=0.999)
+
+
+def test_rowop_wide_rows_rms():
+    inp = I.postnorm_inputs(37, 64, 2560, "f32", seed=35, with_residual=False)
+    X, W = dev(inp.X, "f32"), dev(I.lay_out_weight(inp.W, "nk"), "f32")
+    b, g = dev(inp.bias, "f32"), dev(inp.gamma, "f32")
+    P = cf.gemm(X, W, out_dtype=torch.float32)
+    Y = torch.empty((inp.M, inp.N), dtype=torch.float32, device="cuda")
+    cf.rowop(P, [dict(kind=cf.CF_N_BIAS, v0=b), dict(kind=cf.CF_N_RMSNORM, v0=g, f0=1e-5),
+                 dict(kind=cf.CF_N_STORE, out=Y, ld=inp.N, dtype=cf.CF_F32)])
+    torch.cuda.synchronize()
+    r = O.rmsnorm(O.bias_residual(O.matmul(inp.X, inp.W), inp.bias), inp.gamma, 1e-5)
+    assert_close_f32(host(Y), r, "unfused wide RMSNorm")
+
+
 def test_rowop_matches_fused_chain():
     inp = I.postnorm_inputs(70, 64, 384, "bf16", seed=15, with_affine=False)
     X, W = dev(inp.X), dev(I.lay_out_weight(inp.W, "nk"))
