@@ -128,6 +128,68 @@ def test_rmsnorm_closed_form():
     np.testing.assert_allclose(y, [[3.0 * math.sqrt(2) / 5.0, 4.0 * math.sqrt(2) / 5.0]], rtol=1e-15)
 
 
+@pytest.mark.parametrize("eps", [0.5, 1e-5])
+def test_rmsnorm_eps_and_gamma_closed_form(eps):
+    # [3, 4]: mean square 12.5, so y = x / sqrt(12.5 + eps) * gamma.  eps = 0.5
+    # gives sqrt(13) exactly: eps outside the root (sqrt(12.5) + 0.5), eps
+    # added to the sum of squares instead of the mean, or a dropped gamma all
+    # move the values by far more than the tolerance.
+    g = np.array([2.0, -0.5])
+    y = O.rmsnorm(np.array([[3.0, 4.0]]), g, eps)
+    r = math.sqrt(12.5 + eps)
+    np.testing.assert_allclose(y, [[3.0 / r * 2.0, 4.0 / r * -0.5]], rtol=1e-15)
+
+
+def _rms_mp(row, gamma, eps):
+    fr = [Fraction(float(v)) for v in row]
+    ms = sum(v * v for v in fr) / len(fr)   # exact mean square
+    r = mpmath.sqrt(mpmath.mpf(ms.numerator) / ms.denominator + mpmath.mpf(eps))
+    return [mpmath.mpf(v.numerator) / v.denominator / r * mpmath.mpf(float(gamma[j])) for j, v in enumerate(fr)]
+
+
+def test_rmsnorm_exact_4x5_with_gamma():
+    x = _small((4, 5), 31, 0, std=2.0)
+    g = 1.0 + _small((5,), 31, 1, std=0.3)
+    y = O.rmsnorm(x, g, 1e-3)
+    for i in range(4):
+        want = _rms_mp(x[i], g, 1e-3)
+        for j in range(5):
+            assert abs(float(y[i, j]) - float(want[j])) <= 1e-14 * (1 + abs(float(want[j])))
+
+
+def test_rmsnorm_invariant_mean_square():
+    # gamma = 1: the mean of y^2 is ms / (ms + eps), with ms from numpy's own mean
+    x = np.random.default_rng(32).standard_normal((32, 640)) * 1.7
+    ms = np.mean(np.square(x), axis=1)
+    y = O.rmsnorm(x, None, 0.25)
+    np.testing.assert_allclose(np.mean(y * y, axis=1), ms / (ms + 0.25), rtol=1e-13)
+
+
+# ---------------------------------------------------------------- ReLU
+def test_relu_definition_points_and_identities():
+    x = np.array([-3.5, -1e-300, -0.0, 0.0, 5e-324, 2.25, 1e300])
+    y = O.relu(x)
+    assert list(y) == [0.0, 0.0, 0.0, 0.0, 5e-324, 2.25, 1e300]
+    assert not np.any(np.signbit(y))            # no negative zero comes out
+    v = np.random.default_rng(33).standard_normal(5000) * 10
+    np.testing.assert_array_equal(O.relu(v) - O.relu(-v), v)       # odd part is the identity
+    np.testing.assert_array_equal(O.relu(v) + O.relu(-v), np.abs(v))
+
+
+def test_mblr_brute_force():
+    # MatMul - BiasAdd - LayerNorm - ReLU (Sec. VI) on 3 x 5, exact product and
+    # 40-digit LayerNorm, then max(., 0) by comparison
+    X, W = _small((3, 7), 34, 0), _small((7, 5), 34, 1)
+    b, g, be = _small((5,), 34, 2, 0.3), 1 + _small((5,), 34, 3, 0.2), _small((5,), 34, 4, 0.2)
+    got = O.relu(O.layernorm(O.bias_residual(O.matmul(X, W), b), g, be, 1e-5))
+    Pm = _mm_exact(X, W)
+    for i in range(3):
+        x = [Pm[i][j] + Fraction(float(b[j])) for j in range(5)]
+        _, _, y = _ln_mp(x, g, be, 1e-5)
+        want = [float(v) if v > 0 else 0.0 for v in y]
+        np.testing.assert_allclose(got[i], want, rtol=1e-13, atol=1e-14)
+
+
 # ---------------------------------------------------------------- GELU
 def _golden_cdf():
     rows = []
