@@ -73,6 +73,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=320)
     ap.add_argument("--warmup", type=int, default=32)
     ap.add_argument("--sets", type=int, default=16)
+    ap.add_argument("--replays", type=int, default=5, help="extra graph replays of the headline (median / min)")
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 whole-row, 2 cluster, 3 split-N")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu", action="store_true")
@@ -83,8 +84,14 @@ def parse():
     return ap.parse_args()
 
 
-def time_steps(torch, calls, steps, warmup):
-    """Average ms per step: `steps` calls (calls[i % len]) captured in one graph."""
+_REPLAYS = {}   # per-step times of the extra replays of the last time_steps call (ms)
+
+
+def time_steps(torch, calls, steps, warmup, replays=1):
+    """Average ms per step: `steps` calls (calls[i % len]) captured in one graph,
+    replayed once under events on the stream the kernels run on.  With
+    replays > 1 the graph is replayed that many more times; the per-step
+    time of each replay is kept in _REPLAYS["ms"] (median and min reporting)."""
     for i in range(warmup):
         calls[i % len(calls)]()
     torch.cuda.synchronize()
@@ -102,24 +109,99 @@ def time_steps(torch, calls, steps, warmup):
     g.replay()
     e1.record(st)
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / steps
+    ms = e0.elapsed_time(e1) / steps
+    per = [ms]
+    for _ in range(replays - 1):
+        e0.record(st)
+        g.replay()
+        e1.record(st)
+        torch.cuda.synchronize()
+        per.append(e0.elapsed_time(e1) / steps)
+    _REPLAYS["ms"] = per
+    return ms
 
 
-def cpu_baseline(inp, seconds):
+def replay_stats():
+    per = _REPLAYS.get("ms", [])
+    return {"replays": len(per), "mean_us": float(np.mean(per)) * 1e3, "median_us": float(np.median(per)) * 1e3,
+            "min_us": float(np.min(per)) * 1e3}
+
+
+def _cpu_info():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                model = line.split(":", 1)[1].strip()
+    except Exception:
+        pass
+    return {"cpu_model": model, "affinity_cpus": len(os.sched_getaffinity(0))}
+
+
+def _blas_threads():
     from threadpoolctl import threadpool_info
+    return int(max([p.get("num_threads", 1) for p in threadpool_info()] + [1]))
 
-    from oracle import comfuse_oracle as O
-    flops = 2.0 * inp.M * inp.N * inp.K
+
+def _timed(fn, seconds):
+    """Repeat fn until `seconds` have passed (at least once); returns (reps, elapsed)."""
     reps, t0 = 0, time.perf_counter()
     while True:
-        O.postnorm(inp.X, inp.W, inp.bias, inp.R, inp.gamma, inp.beta, inp.alpha, inp.eps)
+        fn()
         reps += 1
         el = time.perf_counter() - t0
         if el >= seconds:
-            break
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": flops * reps / el / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"full {inp.M}x{inp.K}x{inp.N} post-norm, fp64 numpy oracle, {reps} reps in {el:.1f} s"}
+            return reps, el
+
+
+def cpu_baseline(I, inp, seconds):
+    """The fp64 oracle timed on this host: the headline workload in full, and a
+    bounded sample of every other workload (its rate scaled to TFLOP/s of the
+    workload's own contractions).  Input generation is not timed."""
+    from oracle import comfuse_oracle as O
+    flops = 2.0 * inp.M * inp.N * inp.K
+    reps, el = _timed(lambda: O.postnorm(inp.X, inp.W, inp.bias, inp.R, inp.gamma, inp.beta, inp.alpha, inp.eps),
+                      seconds)
+    out = {"value": flops * reps / el / 1e12, "unit": "TFLOP/s", "cores": _blas_threads(), "kind": "oracle",
+           "sample": f"full {inp.M}x{inp.K}x{inp.N} post-norm, fp64 numpy oracle, {reps} reps in {el:.1f} s"}
+    out.update(_cpu_info())
+    per = {}
+    budget = max(1.0, seconds / 4)
+
+    def rec(name, fl, fn, sample):
+        r, e = _timed(fn, budget)
+        per[name] = {"value": fl * r / e / 1e12, "unit": "TFLOP/s", "sample": f"{sample}, {r} reps in {e:.1f} s"}
+
+    t = I.postnorm_tiny_fp32()
+    rec("postnorm_tiny_fp32", 2.0 * t.M * t.N * t.K,
+        lambda: O.postnorm(t.X, t.W, t.bias, t.R, t.gamma, t.beta, 1.0, t.eps), f"full {t.M}x{t.K}x{t.N}")
+    c = I.ln_gelu_amax_inputs()
+    rows = np.arange(0, c.M, c.M // 64)
+    rec("ln_gelu_amax_fp8", 2.0 * len(rows) * c.N * c.K,
+        lambda: O.ln_gelu_amax(c.X[rows], c.W, c.bias, c.R[rows], eps=c.eps),
+        f"{len(rows)} of {c.M} rows, K = N = {c.K}")
+    del c
+    f = I.ffn_inputs()
+    fr = slice(0, 4096)
+    rec("ffn_b2b", 2.0 * 4096 * f.N1 * f.d * 2,
+        lambda: O.ffn_b2b(f.X[fr], f.W1, f.b1, f.W2, f.b2, eps=f.eps), f"4096 of {f.M} rows, d {f.d}, N1 {f.N1}")
+    del f
+    a = I.attention_inputs()
+    rec("attention_b2b", 2.0 * 2 * a.Lq * a.Lk * a.d * 2,
+        lambda: O.attention(a.Q[0, :2], a.K[0, :2], a.V[0, :2]), f"2 of {a.B * a.H} heads, {a.Lq}x{a.Lk}, d {a.d}")
+    del a
+    out["per_workload"] = per
+    return out
 
 
 def summarize(fused_ms, unfused_ms, flop, nbytes, bound, peak, parity, **extra):
@@ -150,7 +232,8 @@ def workload_tiny(torch, cf, I, O, dev):
     Y = torch.empty((M, N), dtype=f, device=dev)
     P = torch.empty((M, N), dtype=f, device=dev)
     ws = cf.workspace(1 << 20, dev)
-    fused = time_steps(torch, [lambda: cf.gemm_postnorm(X, W, b, R, g, be, eps=inp.eps, out=Y, ws=ws)], 400, 20)
+    fused = time_steps(torch, [lambda: cf.gemm_postnorm(X, W, b, R, g, be, eps=inp.eps, out=Y, ws=ws)], 400, 20, replays=3)
+    fstats = replay_stats()
     ref = O.postnorm(inp.X, inp.W, inp.bias, inp.R, inp.gamma, inp.beta, 1.0, inp.eps)
     err = float(np.max(np.abs(Y.cpu().numpy() - ref)))
     spec = [dict(kind=cf.CF_N_RESIDUAL, **{"in": R}, ld=N, dtype=cf.CF_F32),
@@ -162,7 +245,7 @@ def workload_tiny(torch, cf, I, O, dev):
     unfused = time_steps(torch, [unf], 400, 20)
     flop = 2.0 * M * N * K
     nbytes = 4 * (M * K + K * N + 2 * M * N) + 3 * 4 * N
-    return summarize(fused, unfused, flop, nbytes, "mfma_f32", F32_PEAK_TFLOPS, verdict(err, 1e-4),
+    return summarize(fused, unfused, flop, nbytes, "mfma_f32", F32_PEAK_TFLOPS, verdict(err, 1e-4), timing=fstats,
                      shape={"M": M, "K": K, "N": N, "dtype": "f32"})
 
 
@@ -183,7 +266,8 @@ def workload_chain(torch, cf, I, O, dev):
     nodes = cf.make_nodes(spec)
     a = cf.subgraph_args(X, W, nodes)
     ws = cf.workspace(cf.cf_gemm_subgraph_workspace(a), dev)
-    fused = time_steps(torch, [lambda: cf.gemm_subgraph(X, W, spec, ws=ws)], 16, 2)
+    fused = time_steps(torch, [lambda: cf.gemm_subgraph(X, W, spec, ws=ws)], 16, 2, replays=3)
+    fstats = replay_stats()
     rows = np.array([0, 1, 4095, M - 1])
     z, sr, _ = O.ln_gelu_amax(inp.X[rows], inp.W, inp.bias, inp.R[rows], eps=inp.eps)
     err = float(np.max(np.abs(Z[torch.from_numpy(rows).to(dev)].float().cpu().numpy() - z)))
@@ -195,7 +279,7 @@ def workload_chain(torch, cf, I, O, dev):
     unfused = time_steps(torch, [unf], 16, 2)
     flop = 2.0 * M * N * K
     nbytes = 2 * (M * K + K * N + M * N) + 2 * M * N + M * N + 4 * M + 4 * N
-    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2),
+    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2), timing=fstats,
                      shape={"M": M, "K": K, "N": N, "dtype": "bf16", "outputs": "Z bf16, s f32, Q e4m3"})
 
 
@@ -210,7 +294,8 @@ def workload_ffn(torch, cf, I, O, dev):
                  S=torch.empty((M, N1), dtype=bf, device=dev), O2=torch.empty((M, d), dtype=bf, device=dev))
             for _ in range(4)]
     fused = time_steps(torch, [(lambda s=s: cf.b2b_ffn(s["X"], W1t, b1, W2t, b2, s["X"], eps=inp.eps, out=s["Y"]))
-                               for s in sets], 64, 8)
+                               for s in sets], 64, 8, replays=3)
+    fstats = replay_stats()
     rows = np.array([0, 1, 127, M - 1])
     ref = O.ffn_b2b(inp.X[rows], inp.W1, inp.b1, inp.W2, inp.b2, eps=inp.eps)
     err = float(np.max(np.abs(sets[0]["Y"][torch.from_numpy(rows).to(dev)].float().cpu().numpy() - ref)))
@@ -229,7 +314,7 @@ def workload_ffn(torch, cf, I, O, dev):
     unfused = time_steps(torch, [unf(s) for s in sets], 64, 8)
     flop = 2.0 * M * N1 * d * 2
     nbytes = 2 * (2 * M * d + 2 * d * N1) + 4 * (N1 + 3 * d)
-    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2),
+    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2), timing=fstats,
                      shape={"M": M, "d": d, "N1": N1, "dtype": "bf16"})
 
 
@@ -241,7 +326,8 @@ def workload_attention(torch, cf, I, O, dev, a=None):
     for _ in range(2):
         sets.append(dict(Q=tensor(torch, a.Q, bf, dev), K=tensor(torch, a.K, bf, dev), V=tensor(torch, a.V, bf, dev),
                          O=torch.empty((B, H, L, d), dtype=bf, device=dev)))
-    fused = time_steps(torch, [(lambda s=s: cf.b2b_attention(s["Q"], s["K"], s["V"], out=s["O"])) for s in sets], 16, 2)
+    fused = time_steps(torch, [(lambda s=s: cf.b2b_attention(s["Q"], s["K"], s["V"], out=s["O"])) for s in sets], 16, 2, replays=3)
+    fstats = replay_stats()
     rows = np.array([0, min(777, L - 1) // 2, L - 1])
     ref = O.attention(a.Q[:, :, rows], a.K, a.V)
     err = float(np.max(np.abs(sets[0]["O"][:, :, torch.from_numpy(rows).to(dev)].float().cpu().numpy() - ref)))
@@ -261,7 +347,7 @@ def workload_attention(torch, cf, I, O, dev, a=None):
                               for s in sets], 16, 2)
     flop = 2.0 * B * H * L * Lk * d * 2
     nbytes = 2 * B * H * (2 * L * d + 2 * Lk * d)   # Q, O and K, V, bf16
-    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2),
+    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2), timing=fstats,
                      torch_sdpa_us=round(sdpa * 1e3, 2),
                      shape={"B": B, "H": H, "Lq": L, "Lk": Lk, "d": d, "dtype": "bf16"})
 
@@ -413,7 +499,9 @@ def main():
             cf.rowop(s["P"], spec)
         return run
 
-    ms = time_steps(torch, [fused(s) for s in sets], args.steps, args.warmup)
+    ms = time_steps(torch, [fused(s) for s in sets], args.steps, args.warmup, replays=args.replays)
+    stats = replay_stats()
+    cf.check_workspace(ws)           # no peer wait gave up in any timed call
     ms_hot = time_steps(torch, [fused(sets[0])], args.steps, args.warmup)
 
     # Parity spot check of the timed kernel's output (64 rows vs the oracle).
@@ -446,6 +534,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS, "traffic": traffic},
         "parity": verdict(err, 2e-2),
+        "timing": stats,
         "cache_hot_ms": ms_hot,
         "mfma_frac": flops / sec / 1e12 / BF16_PEAK_TFLOPS,
         "kernel_hash": khash,
@@ -473,7 +562,7 @@ def main():
             torch.cuda.empty_cache()
         out["workloads"] = wl
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(I, inp, args.cpu_seconds)
     print(json.dumps(out))
 
 

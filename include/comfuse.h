@@ -52,7 +52,7 @@ extern "C" {
 #endif
 
 #define CF_VERSION 1
-#define CF_WS_HEADER_BYTES 8392704  /* 4096 + 2 * 128 * 16 * 128 * 16 */
+#define CF_WS_HEADER_BYTES 8392704  /* 4096 + 2 stages * 2 parities * 64 * 16 * 128 * 16 */
 
 typedef enum {
   CF_F32 = 0,       /* IEEE binary32 */
@@ -76,7 +76,8 @@ typedef enum {
   CF_ERR_UNSUPPORTED = 7, /* outside the compiled vocabulary */
   CF_ERR_ALIAS = 8,       /* an output aliases an input */
   CF_ERR_HIP = 9,         /* the HIP runtime reported an error */
-  CF_ERR_STRUCT = 10      /* struct_size does not match this library */
+  CF_ERR_STRUCT = 10,     /* struct_size does not match this library */
+  CF_ERR_PEER_TIMEOUT = 11 /* cf_workspace_check: a row-cluster wait gave up */
 } cf_status;
 
 /* ------------------------------------------------------------------------
@@ -98,8 +99,9 @@ typedef enum {
  * records of the row-cluster path): zero-fill that header once before first
  * use and do not modify it afterwards; every call leaves it valid for any
  * later call, whatever its shape or path.  A non-zero first 32-bit word means
- * a wait for peer workgroups exceeded its bound (results of that call are
- * invalid).
+ * a wait for peer workgroups exceeded its bound: results written through the
+ * workspace since it was last cleared are invalid.  cf_workspace_check reads
+ * and clears it.
  * ------------------------------------------------------------------------ */
 typedef struct {
   size_t struct_size;            /* = sizeof(cf_postnorm_args) */
@@ -238,7 +240,11 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes,
  *           Shape rules: N % 32 == 0, K % 16 == 0.
  * cf_rowop: runs a node list (same grammar as cf_gemm_subgraph, or a single
  *           SOFTMAX node, f0 = scale, writing out) over each row of the
- *           materialised P (M x N, dtype in).
+ *           materialised P: batch matrices of M x N (dtype in, leading
+ *           dimension ldp), matrix b at P + b * sp elements (sp a multiple
+ *           of 16 bytes; ignored when batch <= 1).  The node list's matrices
+ *           and s hold the batch * M rows one after another (row b * M + m),
+ *           with their own leading dimensions.
  * ------------------------------------------------------------------------ */
 cf_status cf_gemm(int64_t batch, int64_t M, int64_t N, int64_t K,
                   cf_dtype in, cf_dtype out,
@@ -247,9 +253,22 @@ cf_status cf_gemm(int64_t batch, int64_t M, int64_t N, int64_t K,
                   const float* bias, float alpha,
                   void* C, int64_t ldc, int64_t sc, void* hip_stream);
 
-cf_status cf_rowop(int64_t M, int64_t N, cf_dtype in, const void* P,
-                   int64_t ldp, const cf_node* nodes, int n_nodes,
-                   void* hip_stream);
+cf_status cf_rowop(int64_t batch, int64_t M, int64_t N, cf_dtype in,
+                   const void* P, int64_t ldp, int64_t sp,
+                   const cf_node* nodes, int n_nodes, void* hip_stream);
+
+/* ------------------------------------------------------------------------
+ * cf_workspace_check — reads and clears the error word of a workspace used by
+ * cf_gemm_postnorm / cf_gemm_subgraph.  The row-cluster path (the paper's
+ * inter-CTA reduction, Sec. III-A) waits for its co-resident peers with a
+ * bounded spin; if a wait gives up (peers not resident, for example because
+ * other work holds the compute units), the kernel sets that word, every later
+ * wait gives up at once, and the outputs are invalid.  This call
+ * SYNCHRONISES hip_stream, then returns CF_ERR_PEER_TIMEOUT (and clears the
+ * word) if it was set since the last check, else CF_OK.  workspace may be
+ * NULL (CF_OK).  Not callable during stream capture.
+ * ------------------------------------------------------------------------ */
+cf_status cf_workspace_check(void* workspace, size_t ws_bytes, void* hip_stream);
 
 /* ------------------------------------------------------------------------
  * Diagnostics

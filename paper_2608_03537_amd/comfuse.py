@@ -28,7 +28,7 @@ CF_OUT_STORE, CF_OUT_BIAS_RESIDUAL_LN = 0, 1
 PATH_AUTO, PATH_WHOLE_ROW, PATH_CLUSTER, PATH_SPLIT = 0, 1, 2, 3
 STATUS = {0: "CF_OK", 1: "CF_ERR_NULL", 2: "CF_ERR_SHAPE", 3: "CF_ERR_LD", 4: "CF_ERR_ALIGN",
           5: "CF_ERR_DTYPE", 6: "CF_ERR_WORKSPACE", 7: "CF_ERR_UNSUPPORTED", 8: "CF_ERR_ALIAS",
-          9: "CF_ERR_HIP", 10: "CF_ERR_STRUCT"}
+          9: "CF_ERR_HIP", 10: "CF_ERR_STRUCT", 11: "CF_ERR_PEER_TIMEOUT"}
 
 vp, i64, f32p = C.c_void_p, C.c_int64, C.POINTER(C.c_float)
 
@@ -100,7 +100,9 @@ def lib():
                 L.cf_gemm.argtypes = [i64, i64, i64, i64, C.c_int, C.c_int, vp, i64, i64, vp, i64, i64,
                                       C.c_int, vp, C.c_float, vp, i64, i64, vp]
                 L.cf_rowop.restype = C.c_int
-                L.cf_rowop.argtypes = [i64, i64, C.c_int, vp, i64, C.POINTER(Node), C.c_int, vp]
+                L.cf_rowop.argtypes = [i64, i64, i64, C.c_int, vp, i64, i64, C.POINTER(Node), C.c_int, vp]
+                L.cf_workspace_check.restype = C.c_int
+                L.cf_workspace_check.argtypes = [vp, C.c_size_t, vp]
                 _lib = L
     return _lib
 
@@ -143,8 +145,12 @@ def cf_gemm(*args):
     return lib().cf_gemm(*args)
 
 
-def cf_rowop(M, N, dtype, P, ldp, nodes, n_nodes, stream):
-    return lib().cf_rowop(M, N, dtype, P, ldp, nodes, n_nodes, stream)
+def cf_rowop(batch, M, N, dtype, P, ldp, sp, nodes, n_nodes, stream):
+    return lib().cf_rowop(batch, M, N, dtype, P, ldp, sp, nodes, n_nodes, stream)
+
+
+def cf_workspace_check(workspace, ws_bytes, stream):
+    return lib().cf_workspace_check(workspace, ws_bytes, stream)
 
 
 def cf_status_string(s):
@@ -189,18 +195,39 @@ def _stream(stream):
 _ws_cache: dict = {}
 
 
-def workspace(nbytes, device):
+def _capturing():
+    return _torch().cuda.is_current_stream_capturing()
+
+
+def workspace(nbytes, device, stream=None):
     """A zero-initialised workspace of at least nbytes on ``device``, cached per
-    device.  Calls that share it must not overlap in time (one stream)."""
+    (device, stream): calls on one stream run in order, so they may share it;
+    calls on different streams get different workspaces (the row-cluster
+    round counters live in it)."""
     torch = _torch()
-    key = str(device)
-    ws = _ws_cache.get(key)
     if nbytes == 0:
         return None
+    key = (str(device), _stream(stream))
+    ws = _ws_cache.get(key)
     if ws is None or ws.numel() < nbytes:
         ws = torch.zeros(max(nbytes, 1 << 20), dtype=torch.uint8, device=device)
         _ws_cache[key] = ws
     return ws
+
+
+def check_workspace(ws, stream=None):
+    """Raise CfError(CF_ERR_PEER_TIMEOUT) if a row-cluster wait gave up since
+    the last check of ``ws`` (synchronises the stream; clears the word)."""
+    if ws is not None:
+        _check(cf_workspace_check(_ptr(ws), ws.numel(), _stream(stream)))
+
+
+def _after_call(ws, need, stream, check):
+    # The error word exists only when the plan used a workspace; checking
+    # synchronises, so it is skipped while a graph is being captured (the
+    # caller then checks after replaying, with check_workspace).
+    if check and need > 0 and not _capturing():
+        check_workspace(ws, stream)
 
 
 def postnorm_args(X, W, bias=None, R=None, gamma=None, beta=None, Y=None, *, w_layout=CF_LAYOUT_NK,
@@ -223,8 +250,13 @@ def postnorm_args(X, W, bias=None, R=None, gamma=None, beta=None, Y=None, *, w_l
 
 
 def gemm_postnorm(X, W, bias=None, R=None, gamma=None, beta=None, *, w_layout=CF_LAYOUT_NK, alpha=1.0,
-                  eps=1e-5, out_dtype=None, path=PATH_AUTO, out=None, ws=None, stream=None):
-    """Y = LayerNorm(alpha * X.W + bias + R) * gamma + beta, fused."""
+                  eps=1e-5, out_dtype=None, path=PATH_AUTO, out=None, ws=None, stream=None, check=True):
+    """Y = LayerNorm(alpha * X.W + bias + R) * gamma + beta, fused.
+
+    check=True reads the workspace's error word after the call (a stream
+    synchronisation) and raises if a row-cluster wait gave up; pass
+    check=False to keep the call asynchronous and use check_workspace later.
+    """
     torch = _torch()
     M = X.shape[0]
     N = W.shape[0] if w_layout == CF_LAYOUT_NK else W.shape[1]
@@ -232,8 +264,9 @@ def gemm_postnorm(X, W, bias=None, R=None, gamma=None, beta=None, *, w_layout=CF
     a = postnorm_args(X, W, bias, R, gamma, beta, Y, w_layout=w_layout, alpha=alpha, eps=eps, path=path)
     need = cf_gemm_postnorm_workspace(a)
     if ws is None:
-        ws = workspace(need, X.device)
+        ws = workspace(need, X.device, stream)
     _check(cf_gemm_postnorm(a, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+    _after_call(ws, need, stream, check)
     return Y
 
 
@@ -266,18 +299,20 @@ def subgraph_args(X, W, nodes, *, w_layout=CF_LAYOUT_NK, path=PATH_AUTO):
     return a
 
 
-def gemm_subgraph(X, W, spec, *, w_layout=CF_LAYOUT_NK, path=PATH_AUTO, ws=None, stream=None):
-    """Run X.W followed by the node list ``spec`` (outputs are given in spec)."""
+def gemm_subgraph(X, W, spec, *, w_layout=CF_LAYOUT_NK, path=PATH_AUTO, ws=None, stream=None, check=True):
+    """Run X.W followed by the node list ``spec`` (outputs are given in spec).
+    ``check`` as in gemm_postnorm."""
     nodes = make_nodes(spec)
     a = subgraph_args(X, W, nodes, w_layout=w_layout, path=path)
     need = cf_gemm_subgraph_workspace(a)
     if ws is None:
-        ws = workspace(need, X.device)
+        ws = workspace(need, X.device, stream)
     _check(cf_gemm_subgraph(a, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+    _after_call(ws, need, stream, check)
 
 
 def ln_gelu_amax(X, W, bias=None, R=None, *, eps=1e-5, qmax=448.0, z_dtype=None, quant_codes=True,
-                 w_layout=CF_LAYOUT_NK, path=PATH_AUTO, ws=None, stream=None, gelu=CF_N_GELU):
+                 w_layout=CF_LAYOUT_NK, path=PATH_AUTO, ws=None, stream=None, gelu=CF_N_GELU, check=True):
     """Z = GELU(LN(X.W + b + R)); s = rowmax|Z| / qmax; Q = e4m3(Z / s).  Returns (Z, s, Q)."""
     torch = _torch()
     M = X.shape[0]
@@ -293,7 +328,7 @@ def ln_gelu_amax(X, W, bias=None, R=None, *, eps=1e-5, qmax=448.0, z_dtype=None,
     spec += [dict(kind=CF_N_LAYERNORM, f0=eps), dict(kind=gelu),
              dict(kind=CF_N_STORE, out=Z, ld=_ld(Z), dtype=_dt(Z)),
              dict(kind=CF_N_ROWAMAX_QUANT, out=s, out2=Q, ld=(N if Q is None else _ld(Q)), f0=qmax)]
-    gemm_subgraph(X, W, spec, w_layout=w_layout, path=path, ws=ws, stream=stream)
+    gemm_subgraph(X, W, spec, w_layout=w_layout, path=path, ws=ws, stream=stream, check=check)
     return Z, s, Q
 
 
@@ -314,10 +349,20 @@ def gemm(A, B, *, b_layout=CF_LAYOUT_NK, bias=None, alpha=1.0, out_dtype=None, o
 
 
 def rowop(P, spec, stream=None):
-    """Run a node list over the rows of a materialised matrix P (unfused)."""
+    """Run a node list over the rows of a materialised matrix P (unfused).
+
+    P is [M, N] or a batch [b, M, N] (any batch stride, unit column stride);
+    the node list's matrices then hold the b * M rows one after another."""
     nodes = make_nodes(spec)
-    M, N = P.shape
-    _check(cf_rowop(M, N, _dt(P), _ptr(P), _ld(P), nodes, len(nodes), _stream(stream)))
+    if P.dim() == 3:
+        nb, M, N = P.shape
+        if P.stride(2) != 1:
+            raise ValueError("expected a unit column stride")
+        ldp, sp = P.stride(1), P.stride(0)
+    else:
+        nb, (M, N) = 1, P.shape
+        ldp, sp = _ld(P), 0
+    _check(cf_rowop(nb, M, N, _dt(P), _ptr(P), ldp, sp, nodes, len(nodes), _stream(stream)))
 
 
 def _b2b_args(**kw):

@@ -211,6 +211,7 @@ void bind_workspace(const Plan& pl, void* ws, GemmRowsParams& p) {
     p.ws_arrive = reinterpret_cast<unsigned long long*>(b + 256);
     static_assert(kWsCounterBytes % 256 == 0, "records alignment");
     p.ws_part = reinterpret_cast<float*>(b + pl.off_part);
+    p.spin_limit = kSpinLimitDefault;
   } else if (pl.mode == ROWS_SPLIT) {
     p.ws_part = reinterpret_cast<float*>(b + pl.off_part);
     p.ws_x = reinterpret_cast<float*>(b + pl.off_x);
@@ -483,6 +484,7 @@ const char* cf_status_string(cf_status s) {
     case CF_ERR_ALIAS: return "CF_ERR_ALIAS: an output aliases an input";
     case CF_ERR_HIP: return "CF_ERR_HIP: HIP runtime error";
     case CF_ERR_STRUCT: return "CF_ERR_STRUCT: struct_size mismatch";
+    case CF_ERR_PEER_TIMEOUT: return "CF_ERR_PEER_TIMEOUT: a wait for peer workgroups gave up";
   }
   return "unknown cf_status";
 }
@@ -593,25 +595,55 @@ cf_status cf_gemm(int64_t batch, int64_t M, int64_t N, int64_t K, cf_dtype in, c
   }
 }
 
-cf_status cf_rowop(int64_t M, int64_t N, cf_dtype in, const void* P, int64_t ldp, const cf_node* nodes,
-                   int n_nodes, void* hip_stream) {
+cf_status cf_rowop(int64_t batch, int64_t M, int64_t N, cf_dtype in, const void* P, int64_t ldp, int64_t sp,
+                   const cf_node* nodes, int n_nodes, void* hip_stream) {
   try {
     if (M < 0 || N <= 0 || N % 4 != 0 || N > 8192) return fail(CF_ERR_SHAPE, "need M >= 0, 0 < N <= 8192, N %% 4 == 0");
+    if (batch < 0 || batch > 65535) return fail(CF_ERR_SHAPE, "batch must be in [0, 65535]");
+    if (batch * M > ((int64_t)1 << 31) - 1) return fail(CF_ERR_SHAPE, "batch * M exceeds 2^31 - 1 rows");
     if (in != CF_F32 && in != CF_BF16) return fail(CF_ERR_DTYPE, "input dtype must be F32 or BF16");
-    cf_status s = check_matrix("P", P, M, N, ldp, in, true);
+    cf_status s = check_matrix("P", P, batch > 0 ? M : 0, N, ldp, in, true);
     if (s != CF_OK) return s;
+    if (batch > 1 && (sp < 0 || (sp * (int64_t)dsize(in)) % 16 != 0))
+      return fail(CF_ERR_ALIGN, "batch stride of P must be a non-negative multiple of 16 bytes");
+    const int64_t rows = batch * M;   // node matrices and s hold batch * M consecutive rows
     RowKernelParams r{};
-    if ((s = parse_nodes(nodes, n_nodes, M, N, in, r.epi, true, &r.softmax, &r.softmax_scale)) != CF_OK) return s;
+    if ((s = parse_nodes(nodes, n_nodes, rows, N, in, r.epi, true, &r.softmax, &r.softmax_scale)) != CF_OK) return s;
     for (const void* out : {(const void*)r.epi.Y, (const void*)r.epi.s_out, (const void*)r.epi.q_out})
       if (outputs_alias(out, {P, r.epi.R, (const void*)r.epi.bias}))
         return fail(CF_ERR_ALIAS, "an output aliases an input");
-    if (M == 0) return CF_OK;
-    r.M = (int)M;
+    if (rows == 0) return CF_OK;
+    r.M = (int)rows;
     r.N = (int)N;
     r.P = P;
     r.ldp = ldp;
+    r.rows_per_batch = (int)M;
+    r.sp = batch > 1 ? sp : 0;
     r.p_f32 = in == CF_F32;
     return hip_status(launch_row_kernel(r, reinterpret_cast<hipStream_t>(hip_stream)), "row kernel launch");
+  } catch (...) {
+    return fail(CF_ERR_HIP, "internal error");
+  }
+}
+
+cf_status cf_workspace_check(void* workspace, size_t ws_bytes, void* hip_stream) {
+  try {
+    if (!workspace) return CF_OK;   // no workspace: no cluster exchange ran
+    if (ws_bytes < sizeof(unsigned)) return fail(CF_ERR_WORKSPACE, "workspace smaller than its error word");
+    if (!aligned16(workspace)) return fail(CF_ERR_ALIGN, "workspace is not 16-byte aligned");
+    hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+    cf_status s = hip_status(hipStreamSynchronize(st), "stream synchronize");
+    if (s != CF_OK) return s;
+    unsigned err = 0;
+    if ((s = hip_status(hipMemcpy(&err, workspace, sizeof(err), hipMemcpyDeviceToHost), "read error word")) != CF_OK)
+      return s;
+    if (err == 0) return CF_OK;
+    const unsigned zero = 0;
+    if ((s = hip_status(hipMemcpy(workspace, &zero, sizeof(zero), hipMemcpyHostToDevice), "clear error word")) != CF_OK)
+      return s;
+    return fail(CF_ERR_PEER_TIMEOUT,
+                "a row-cluster wait for peer workgroups exceeded its bound; results written through this "
+                "workspace since the last check are invalid (the word is now cleared)");
   } catch (...) {
     return fail(CF_ERR_HIP, "internal error");
   }

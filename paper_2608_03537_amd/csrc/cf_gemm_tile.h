@@ -34,8 +34,6 @@
 
 namespace cf {
 
-constexpr int kSpinLimit = 1 << 20;   // bounded wait for peers (each poll is one device-scope round trip: ~1 s)
-
 template <typename TIn, int BM_, int BN_, int WM_, int WN_, int TKB_, int STAGES_ = 0>
 struct TileShape {
   using T = TIn;
@@ -478,17 +476,24 @@ __device__ __forceinline__ void wg_row_reduce(float (&v)[S::BM], float* red, int
 // so all adds of a round have landed before any record of the round can be
 // seen, and the next round's adds see the next round number.
 //
-// Records.  record(stage, slot, peer, row) holds one or two 64-bit words,
-// each a 32-bit value with the round number + 1 in its upper half.  A word is
-// written and read with single 64-bit device-coherent atomics (relaxed, agent
-// scope; on gfx950 these bypass the non-coherent caches), so a reader that
-// sees the current round in a word also sees that round's value: no fence,
-// no completion wait on the writer and no separate arrival flag.  Only this
-// path writes the records and a slot's round numbers only grow, so a stale
-// or zero-filled record never carries the current tag.  Agent-scope release
-// / acquire fences are avoided on purpose: on gfx950 they write back and
-// invalidate the whole L2, evicting the operands of every workgroup sharing
-// it.
+// Records.  record(stage, parity, slot, peer, row) holds one or two 64-bit
+// words, each a 32-bit value with the round number + 1 in its upper half.  A
+// word is written and read with single 64-bit device-coherent atomics
+// (relaxed, agent scope; on gfx950 these bypass the non-coherent caches), so
+// a reader that sees the current round in a word also sees that round's
+// value: no fence, no completion wait on the writer and no separate arrival
+// flag.  Only this path writes the records and a slot's round numbers only
+// grow, so a stale or zero-filled record never carries the current tag.
+// Rounds of odd and even number use separate record sets, so a peer that
+// runs one round ahead never overwrites a record another peer still waits
+// for.  Agent-scope release / acquire fences are avoided on purpose: on
+// gfx950 they write back and invalidate the whole L2, evicting the operands
+// of every workgroup sharing it.
+//
+// Failure.  A wait that exceeds p.spin_limit polls sets the sticky error word
+// and moves on; every later wait sees the word and gives up at once, so a
+// broken launch ends quickly.  The host reads and clears the word
+// (cf_workspace_check); results of a call that set it are invalid.
 __device__ __forceinline__ unsigned long long round_begin(const GemmRowsParams& p, int slot, int lane, int nw) {
   unsigned long long old = 0;
   if (lane == 0)
@@ -527,7 +532,7 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
   constexpr int NV = MAX ? 1 : 2;
   constexpr int PB = 4;   // peers read per batch
   unsigned long long* rec = reinterpret_cast<unsigned long long*>(p.ws_part) + stage * kRecStageWords +
-                            (size_t)slot * kRecPeers * kRecRows * 2;
+                            (tag & 1u) * kRecSetWords + (size_t)slot * kRecPeers * kRecRows * 2;
   const int lr = lane & 31;
   if (wn == 0 && lane < 32) {
 #pragma unroll
@@ -547,6 +552,8 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
   for (int c0 = 0; c0 < cn; c0 += PB) {
     unsigned long long w[S::BM][PB][NV];
     for (int spins = 0;; ++spins) {
+      // the sticky error word rides along with every poll
+      const unsigned err = __hip_atomic_load(p.ws_err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       bool ok = true;
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm)
@@ -561,7 +568,8 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
           }
         }
       if (__all(ok)) break;
-      if (spins >= kSpinLimit) {
+      if (__builtin_amdgcn_readfirstlane(err) != 0u) break;   // an earlier wait failed: give up now
+      if (spins >= p.spin_limit) {
         __hip_atomic_store(p.ws_err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
       }

@@ -58,6 +58,7 @@ struct GemmRowsParams {
   float* ws_part;                // CLUSTER: records (kRecStageWords u64 per stage);
                                  // SPLIT: [M][cn] float2
   float* ws_x;                   // SPLIT: [M][N] fp32 pre-norm x
+  int spin_limit;                // polls before a peer wait gives up (sets ws_err)
 };
 
 // Each of the NW waves of the cn workgroups of a peer group adds
@@ -65,21 +66,34 @@ struct GemmRowsParams {
 // adds exactly kArriveUnit.  lcm(1..16) * 8 is divisible by cn * NW for every
 // cn <= 16 and NW in {1, 2, 4, 8}.
 constexpr unsigned long long kArriveUnit = 720720ull * 8ull;
-constexpr int kMaxSlots = 128;                       // concurrent peer groups
-// Exchange records: [stage 2][slot][peer kRecPeers][row kRecRows] x 2 words.
+constexpr int kMaxSlots = 64;                        // concurrent peer groups
+// Exchange records: [stage 2][round parity 2][slot kMaxSlots][peer kRecPeers]
+// [row kRecRows] x 2 words.  A record's position depends only on (slot,
+// peer), never on the launch's peer count: round numbers grow per slot, so a
+// record left by an earlier call in a position only ever carries an older
+// round of the same slot (a position shared by different slots could hold
+// another slot's equal round number).  The parity of the round selects one
+// of two record sets: a fast peer that has finished round r and publishes
+// round r + 1 writes the other set, so a slow peer still reading round r
+// never finds its value overwritten.  (It cannot get two rounds ahead: round
+// r + 1 completes only with every peer's round r + 1 record, written after
+// that peer finished round r.)
 constexpr int kRecPeers = 16, kRecRows = 128;
-constexpr size_t kRecStageWords = (size_t)kMaxSlots * kRecPeers * kRecRows * 2;
+constexpr size_t kRecSetWords = (size_t)kMaxSlots * kRecPeers * kRecRows * 2;   // one parity of one stage
+constexpr size_t kRecStageWords = 2 * kRecSetWords;
 constexpr size_t kWsCounterBytes = 4096;             // err word, then the counters
 constexpr size_t kWsHeaderBytes = kWsCounterBytes + 2 * kRecStageWords * 8;
 static_assert(256 + 8 * kMaxSlots <= kWsCounterBytes, "counter area");
+constexpr int kSpinLimitDefault = 1 << 20;           // ~1 s of device-scope polls
 
 // Wave-per-row kernel: the finish pass of the split path (merge the partial
 // (mean, M2) of each row's tiles, then stages 2..4 on the fp32 x the GEMM
 // wrote) and the unfused row operator (stages 1..4, or softmax, on a
 // materialised matrix).
 struct RowKernelParams {
-  int M, N;
+  int M, N;                               // M counts the rows of every batch
   const void* P; int64_t ldp; int p_f32;  // input rows (finish: fp32 x)
+  int rows_per_batch; int64_t sp;         // row r of P: (r / rows_per_batch) * sp + (r % rows_per_batch) * ldp
   int finish;                             // 1: statistics from partials
   int cn, tn;                             // finish: tiles per row, tile width
   const float* part;                      // finish: [M][cn] (mean, M2)

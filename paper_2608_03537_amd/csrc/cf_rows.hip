@@ -16,6 +16,14 @@
 
 namespace cf {
 
+// Element offset of row m of the input (rows of a batch of matrices with
+// stride sp, or one matrix when sp = 0).
+__device__ __forceinline__ int64_t prow(const RowKernelParams& p, int m) {
+  if (p.sp == 0) return (int64_t)m * p.ldp;
+  const int b = m / p.rows_per_batch;
+  return (int64_t)b * p.sp + (int64_t)(m - b * p.rows_per_batch) * p.ldp;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
@@ -64,8 +72,8 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
     const int n = 256 * j + 4 * lane;
     val[j] = n < N;
     if (val[j]) {
-      if (p.p_f32) load4<float>(reinterpret_cast<const float*>(p.P) + (int64_t)m * p.ldp + n, v[j]);
-      else load4<bf16_t>(reinterpret_cast<const bf16_t*>(p.P) + (int64_t)m * p.ldp + n, v[j]);
+      if (p.p_f32) load4<float>(reinterpret_cast<const float*>(p.P) + prow(p, m) + n, v[j]);
+      else load4<bf16_t>(reinterpret_cast<const bf16_t*>(p.P) + prow(p, m) + n, v[j]);
     } else {
       v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0.0f;
     }
@@ -280,8 +288,8 @@ __global__ __launch_bounds__(256) void wide_row_kernel(RowKernelParams p) {
   for (int j = 0; j < VPW; ++j) {
     val[j] = FULL || col(j) < N;
     if (val[j]) {
-      if (p.p_f32) load4<float>(reinterpret_cast<const float*>(p.P) + (int64_t)m * p.ldp + col(j), v[j]);
-      else load4<bf16_t>(reinterpret_cast<const bf16_t*>(p.P) + (int64_t)m * p.ldp + col(j), v[j]);
+      if (p.p_f32) load4<float>(reinterpret_cast<const float*>(p.P) + prow(p, m) + col(j), v[j]);
+      else load4<bf16_t>(reinterpret_cast<const bf16_t*>(p.P) + prow(p, m) + col(j), v[j]);
     } else {
       v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0.0f;
     }

@@ -38,7 +38,7 @@ def test_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     assert cf.cf_version() == 1
-    for s in range(11):
+    for s in range(12):
         assert cf.cf_status_string(s).startswith(cf.STATUS[s])
 
 
@@ -170,7 +170,18 @@ def test_gemm_and_rowop_validation():
     assert st[cf.cf_gemm(1, 64, 256, 128, cf.CF_BF16, cf.CF_BF16, A, 128, 0, B, 128, 0, cf.CF_LAYOUT_NK,
                          None, 1.0, A, 256, 0, None)] == "CF_ERR_ALIAS"
     nodes = cf.make_nodes([dict(kind=cf.CF_N_SOFTMAX, out=Y, ld=256, dtype=cf.CF_BF16, f0=1.0)])
-    assert cf.cf_rowop(0, 256, cf.CF_BF16, A, 256, nodes, 1, None) == 0
-    assert st[cf.cf_rowop(4, 256, cf.CF_BF16, None, 256, nodes, 1, None)] == "CF_ERR_NULL"
+    assert cf.cf_rowop(1, 0, 256, cf.CF_BF16, A, 256, 0, nodes, 1, None) == 0
+    assert cf.cf_rowop(0, 64, 256, cf.CF_BF16, A, 256, 0, nodes, 1, None) == 0
+    assert st[cf.cf_rowop(1, 4, 256, cf.CF_BF16, None, 256, 0, nodes, 1, None)] == "CF_ERR_NULL"
     nodes2 = cf.make_nodes([dict(kind=cf.CF_N_SOFTMAX, out=A, ld=256, dtype=cf.CF_BF16, f0=1.0)])
-    assert st[cf.cf_rowop(4, 256, cf.CF_BF16, A, 256, nodes2, 1, None)] == "CF_ERR_ALIAS"
+    assert st[cf.cf_rowop(1, 4, 256, cf.CF_BF16, A, 256, 0, nodes2, 1, None)] == "CF_ERR_ALIAS"
+    # batch strides: multiples of 16 bytes, batch within [0, 65535]
+    assert st[cf.cf_rowop(2, 4, 256, cf.CF_BF16, A, 256, 1028, nodes, 1, None)] == "CF_ERR_ALIGN"
+    assert st[cf.cf_rowop(70000, 4, 256, cf.CF_BF16, A, 256, 1024, nodes, 1, None)] == "CF_ERR_SHAPE"
+
+
+def test_workspace_check_without_workspace():
+    # NULL workspace: nothing to check, no device call
+    assert cf.cf_workspace_check(None, 0, None) == 0
+    assert cf.STATUS[cf.cf_workspace_check(A + 8, 64, None)] == "CF_ERR_ALIGN"
+    assert cf.STATUS[cf.cf_workspace_check(A, 2, None)] == "CF_ERR_WORKSPACE"

@@ -110,19 +110,26 @@ def test_attention_table2_shapes(which):
 
 def test_attention_invariants():
     a = I.attention_inputs(seed=6, B=1, H=2, Lq=128, Lk=200, d=128)
+    # V = 1: the row sums l and the numerator come from the same bf16 P, so
+    # every output is exactly 1
     ones = run_attn(a.Q, a.K, np.ones_like(a.V))
-    assert np.max(np.abs(ones - 1.0)) < 8e-3
+    assert np.array_equal(ones, np.ones_like(ones)), np.max(np.abs(ones - 1.0))
     zq = run_attn(np.zeros_like(a.Q), a.K, a.V)
     mean_v = a.V.astype(np.float64).mean(axis=2, keepdims=True)
     assert max_abs(zq, np.broadcast_to(mean_v, zq.shape)) < 4e-3
 
 
 def test_attention_full_size_sampled_rows():
+    # one query row in every 128-query block of every (batch, head), at a
+    # position that moves from block to block and head to head
     a = I.attention_inputs()
     got = run_attn(a.Q, a.K, a.V)
-    rows = np.unique(np.concatenate([[0, 1, 127, 128, a.Lq - 1],
-                                     np.random.default_rng(0).choice(a.Lq, 27, replace=False)]))
-    ref = O.attention(a.Q[:, :, rows], a.K, a.V)
-    g = got[:, :, rows]
-    assert rel_rms(g, ref) < 5e-3, rel_rms(g, ref)
-    assert max_abs(g, ref) < 2e-2
+    nblk = (a.Lq + 127) // 128
+    for b in range(a.B):
+        for h in range(a.H):
+            off = (np.arange(nblk) * 37 + 11 * (b * a.H + h)) % 128
+            rows = np.minimum(np.arange(nblk) * 128 + off, a.Lq - 1)
+            ref = O.attention(a.Q[b, h][rows], a.K[b, h], a.V[b, h])
+            g = got[b, h][rows]
+            assert rel_rms(g, ref) < 5e-3, (b, h, rel_rms(g, ref))
+            assert max_abs(g, ref) < 2e-2, (b, h, max_abs(g, ref))

@@ -59,7 +59,7 @@ def test_chain_small(N, path):
     Zg, sg, Qg = run_chain(inp, path)
     assert_close_bf16(Zg, z, f"Z N={N} path {path}")
     np.testing.assert_allclose(sg, s, rtol=1e-3)
-    check_codes(Qg, q, min_equal=0.999)
+    check_codes(Qg, q)
 
 
 @pytest.mark.parametrize("N", [160, 320])
@@ -73,7 +73,7 @@ def test_chain_ragged_tile_whole_row(N):
     Zg, sg, Qg = run_chain(inp, 1)
     assert_close_bf16(Zg, z, f"Z N={N} whole-row")
     np.testing.assert_allclose(sg, s, rtol=1e-3)
-    check_codes(Qg, q, min_equal=0.999)
+    check_codes(Qg, q)
 
 
 @pytest.mark.parametrize("path", [1, 2, 3])
@@ -97,7 +97,7 @@ def test_chain_split_wide_rows(N):
     Zg, sg, Qg = run_chain(inp, 3)
     assert_close_bf16(Zg, z, f"Z N={N} split")
     np.testing.assert_allclose(sg, s, rtol=1e-3)
-    check_codes(Qg, q, min_equal=0.999)
+    check_codes(Qg, q)
 
 
 def test_chain_split_wide_quant_exact_against_own_z():
@@ -138,17 +138,29 @@ def test_gelu_tanh_variant_is_the_tanh_one():
     assert np.max(np.abs(Zg - O.gelu_erf(y))) > 2e-4
 
 
+def block_rows(M, block=128, seed=0):
+    """One row in every block of `block` rows (at a position that moves from
+    block to block, so every slot of a tile is hit somewhere), plus the
+    first, last and tile-edge rows."""
+    nb = (M + block - 1) // block
+    off = (np.arange(nb) * 37 + seed) % block
+    rows = np.minimum(np.arange(nb) * block + off, M - 1)
+    return np.unique(np.concatenate([rows, [0, 1, block - 1, block, M - 1]]))
+
+
 @pytest.mark.parametrize("path", [0, 2])
 def test_chain_full_size_sampled_rows(path):
     inp = I.ln_gelu_amax_inputs()
     Zg, sg, Qg = run_chain(inp, path)
-    rows = np.unique(np.concatenate([[0, 1, 127, 128, inp.M - 1],
-                                     np.random.default_rng(0).choice(inp.M, 59, replace=False)]))
+    rows = block_rows(inp.M)
+    assert len(rows) >= inp.M // 128
     z, s, q = O.ln_gelu_amax(inp.X[rows], inp.W, inp.bias, inp.R[rows], eps=inp.eps)
     assert_close_bf16(Zg[rows], z, f"cfg3 Z path {path}")
     np.testing.assert_allclose(sg[rows], s, rtol=1e-3)
     check_codes(Qg[rows], q)
-    # Properties that hold at any size: every row's largest code is +-448.
+    # every compared row's largest code is +-448 (s = amax / 448 by construction)
+    assert np.all(np.max(np.abs(O.e4m3_decode(Qg[rows])), axis=1) == 448.0)
+    # and the same on every 97th row of the whole output (a property at any size)
     assert np.all(np.max(np.abs(O.e4m3_decode(Qg[::97])), axis=1) == 448.0)
 
 
@@ -226,7 +238,7 @@ def test_rowop_wide_rows_chain(N, p_dtype):
         z, sr, q = O.ln_gelu_amax(inp.X, inp.W, inp.bias, inp.R, eps=1e-5)
     assert_close_bf16(host(Z), z, f"unfused wide chain N={N}")
     np.testing.assert_allclose(s.cpu().numpy(), sr, rtol=1e-3)
-    check_codes(Q.cpu().numpy(), q, min_equal=0.999)
+    check_codes(Q.cpu().numpy(), q)
 
 
 def test_rowop_wide_rows_rms():
@@ -258,7 +270,7 @@ def test_rowop_matches_fused_chain():
     z, sr, q = O.ln_gelu_amax(inp.X, inp.W, inp.bias, inp.R, eps=1e-5)
     assert_close_bf16(host(Z), z, "unfused chain")
     np.testing.assert_allclose(s.cpu().numpy(), sr, rtol=1e-3)
-    check_codes(Q.cpu().numpy(), q, min_equal=0.999)
+    check_codes(Q.cpu().numpy(), q)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
