@@ -185,6 +185,24 @@ cf_status cf_gemm_subgraph(const cf_subgraph_args* a, void* workspace,
                            size_t ws_bytes, void* hip_stream);
 
 /* ------------------------------------------------------------------------
+ * cf_gemm_subgraph_noalloc — cf_gemm_subgraph for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): same arguments, same results, no
+ * workspace argument, and no allocation of any kind.
+ *
+ * The split-N path's scratch (per-tile partial statistics and the fp32
+ * pre-norm rows) lives in a 32 MiB device array inside the library, one per
+ * GPU, held until the process ends; a shape whose split path needs more
+ * (about M * N * 4 bytes) returns CF_ERR_WORKSPACE.  The row-cluster path is
+ * not used (it keeps state between calls): path 0 (auto) takes whole rows for
+ * N <= 768 and split-N above; path 2 returns CF_ERR_UNSUPPORTED.
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (several streams or threads) race and must be serialised by the
+ * caller.  Validation happens first, as for cf_gemm_subgraph.
+ * ------------------------------------------------------------------------ */
+cf_status cf_gemm_subgraph_noalloc(const cf_subgraph_args* a, void* hip_stream);
+
+/* ------------------------------------------------------------------------
  * cf_b2bgemm — back-to-back GEMM with the intermediate kept on chip
  * (Sec. IV, Eq. 2: P = X W1, S = F(P), O = S W2), batched over `batch`
  * independent problems (strides sx, sw1, ... in elements).

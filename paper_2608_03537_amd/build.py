@@ -20,7 +20,8 @@ LIB = os.path.join(PKG, "libcomfuse.so")
 ARCH = os.environ.get("CF_OFFLOAD_ARCH", "gfx950")
 
 SOURCES = ["cf_api.cpp", "cf_gemm_registry.cpp", "cf_gemm_inst_v2.hip", "cf_gemm_inst_v1.hip",
-           "cf_gemm_inst_wr.hip", "cf_gemm_inst_split.hip", "cf_rows.hip", "cf_b2b.hip", "cf_ffn.hip"]
+           "cf_gemm_inst_wr.hip", "cf_gemm_inst_split.hip", "cf_rows.hip", "cf_b2b.hip", "cf_ffn.hip",
+           "cf_noalloc.hip"]
 
 # -packed-fp32-ops off: hipcc then never forms v_pk_{add,mul,fma}_f32 from
 # scalar float code (the host pass warns that it does not know the feature).

@@ -101,6 +101,8 @@ def lib():
                                       C.c_int, vp, C.c_float, vp, i64, i64, vp]
                 L.cf_rowop.restype = C.c_int
                 L.cf_rowop.argtypes = [i64, i64, i64, C.c_int, vp, i64, i64, C.POINTER(Node), C.c_int, vp]
+                L.cf_gemm_subgraph_noalloc.restype = C.c_int
+                L.cf_gemm_subgraph_noalloc.argtypes = [C.POINTER(SubgraphArgs), vp]
                 L.cf_workspace_check.restype = C.c_int
                 L.cf_workspace_check.argtypes = [vp, C.c_size_t, vp]
                 _lib = L
@@ -131,6 +133,10 @@ def cf_gemm_subgraph(args, workspace, ws_bytes, stream):
 
 def cf_gemm_subgraph_workspace(args):
     return lib().cf_gemm_subgraph_workspace(C.byref(args))
+
+
+def cf_gemm_subgraph_noalloc(args, stream):
+    return lib().cf_gemm_subgraph_noalloc(C.byref(args), stream)
 
 
 def cf_b2bgemm(args, workspace, ws_bytes, stream):
@@ -309,6 +315,15 @@ def gemm_subgraph(X, W, spec, *, w_layout=CF_LAYOUT_NK, path=PATH_AUTO, ws=None,
         ws = workspace(need, X.device, stream)
     _check(cf_gemm_subgraph(a, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
     _after_call(ws, need, stream, check)
+
+
+def gemm_subgraph_noalloc(X, W, spec, *, w_layout=CF_LAYOUT_NK, path=PATH_AUTO, stream=None):
+    """gemm_subgraph without a workspace: the library's own per-GPU scratch
+    array serves the split path (no allocation anywhere; calls on one GPU
+    must not overlap)."""
+    nodes = make_nodes(spec)
+    a = subgraph_args(X, W, nodes, w_layout=w_layout, path=path)
+    _check(cf_gemm_subgraph_noalloc(a, _stream(stream)))
 
 
 def ln_gelu_amax(X, W, bias=None, R=None, *, eps=1e-5, qmax=448.0, z_dtype=None, quant_codes=True,

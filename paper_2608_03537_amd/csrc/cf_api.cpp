@@ -87,12 +87,14 @@ constexpr int kAssumedCUs = 256;   // MI355X; used only to rank tile widths
 // counters and exchange records; only the cluster path writes it), which is
 // all the cluster path needs.  The split path keeps part[M][cn] float2 and
 // x[M][N] after it.
-void size_workspace(Plan& pl, int64_t M, int64_t N) {
+// The allocation-free entry point never runs the cluster path and keeps no
+// header (header = false): its split buffers start at the scratch base.
+void size_workspace(Plan& pl, int64_t M, int64_t N, bool header) {
   if (pl.mode == ROWS_CLUSTER) {
     pl.off_part = kWsCounterBytes;
     pl.ws = kWsHeaderBytes;
   } else if (pl.mode == ROWS_SPLIT) {
-    pl.off_part = kWsHeaderBytes;
+    pl.off_part = header ? kWsHeaderBytes : 0;
     pl.off_x = pl.off_part + round_up((size_t)M * pl.cn * 8, 256);
     pl.ws = pl.off_x + round_up((size_t)M * N * 4, 256);
   } else {
@@ -125,8 +127,13 @@ int pick_tile(int64_t M, int64_t N, int64_t K, int in_f32, int loop, int epi, bo
 // true when the subgraph has a row reduction (then rows must be completed
 // across tiles); without one any tiling is valid.
 cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int path, int epi, bool need_rows,
-                    bool probe_device, Plan& pl) {
+                    bool probe_device, Plan& pl, bool allow_cluster = true) {
   pl = Plan();
+  if (!allow_cluster && need_rows) {
+    if (path == PATH_CLUSTER)
+      return fail(CF_ERR_UNSUPPORTED, "the allocation-free entry point has no row-cluster path");
+    if (path == PATH_AUTO) path = N <= kWholeRowMaxN ? PATH_WHOLE_ROW : PATH_SPLIT;
+  }
   const int tk = in_f32 ? 32 : 64;                     // k per 128-byte stage
   const int loop = (w_nk && K % tk == 0) ? 1 : 0;
   if (!need_rows) {
@@ -200,7 +207,7 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
   if (pl.mode == ROWS_CLUSTER && (pl.tm > kRecRows || pl.cn > kRecPeers))
     return fail(CF_ERR_UNSUPPORTED, "cluster path: tile of %d rows x %d peers exceeds the exchange records",
                 pl.tm, pl.cn);
-  size_workspace(pl, M, N);
+  size_workspace(pl, M, N, allow_cluster);
   return CF_OK;
 }
 
@@ -383,9 +390,12 @@ bool outputs_alias(const void* out, std::initializer_list<const void*> ins) {
 }
 
 // Shared body of cf_gemm_postnorm / cf_gemm_subgraph.
+// scratch = true: ws is the library's own allocation-free scratch (no
+// header, no cluster path; a plan needing more than ws_bytes is refused).
 cf_status rows_common(int64_t M, int64_t N, int64_t K, cf_dtype in, const void* X, int64_t ldx,
                       const void* W, int64_t ldw, cf_layout wl, const RowEpi& epi, int path,
-                      void* ws, size_t ws_bytes, void* stream, bool size_only, size_t* ws_out) {
+                      void* ws, size_t ws_bytes, void* stream, bool size_only, size_t* ws_out,
+                      bool scratch = false) {
   cf_status s = check_gemm_shape(M, N, K);
   if (s != CF_OK) return s;
   if (in != CF_F32 && in != CF_BF16) return fail(CF_ERR_DTYPE, "input dtype must be F32 or BF16");
@@ -399,7 +409,8 @@ cf_status rows_common(int64_t M, int64_t N, int64_t K, cf_dtype in, const void* 
   Plan pl;
   // Validation and sizing never touch the device; residency is queried only
   // right before a launch.
-  if ((s = plan_rows(M, N, K, in == CF_F32, wl == CF_LAYOUT_NK, path, epi_kind, need_rows, false, pl)) != CF_OK)
+  if ((s = plan_rows(M, N, K, in == CF_F32, wl == CF_LAYOUT_NK, path, epi_kind, need_rows, false, pl,
+                     !scratch)) != CF_OK)
     return s;
   if (size_only) {
     *ws_out = pl.ws;
@@ -409,6 +420,9 @@ cf_status rows_common(int64_t M, int64_t N, int64_t K, cf_dtype in, const void* 
     if (outputs_alias(out, {X, W, epi.R, (const void*)epi.bias, (const void*)epi.gamma, (const void*)epi.beta}))
       return fail(CF_ERR_ALIAS, "an output aliases an input");
   if (M == 0) return CF_OK;   // nothing to compute: no workspace needed
+  if (scratch && pl.ws > ws_bytes)
+    return fail(CF_ERR_WORKSPACE, "this shape needs %zu bytes of scratch; the allocation-free entry point holds %zu",
+                pl.ws, ws_bytes);
   if (pl.ws > 0) {
     if (!ws) return fail(CF_ERR_WORKSPACE, "workspace of %zu bytes required", pl.ws);
     if (ws_bytes < pl.ws) return fail(CF_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, pl.ws);
@@ -463,7 +477,49 @@ cf_status postnorm_epi(const cf_postnorm_args* a, RowEpi& e) {
   return CF_OK;
 }
 
+cf_status subgraph_epi(const cf_subgraph_args* a, RowEpi& e) {
+  if (!a) return fail(CF_ERR_NULL, "args is NULL");
+  if (a->struct_size != sizeof(cf_subgraph_args))
+    return fail(CF_ERR_STRUCT, "struct_size %zu != %zu", a->struct_size, sizeof(cf_subgraph_args));
+  if (a->in_dtype != CF_F32 && a->in_dtype != CF_BF16) return fail(CF_ERR_DTYPE, "in_dtype must be F32 or BF16");
+  return parse_nodes(a->nodes, a->n_nodes, a->M, a->N, a->in_dtype, e, false, nullptr, nullptr);
+}
+
 }  // namespace
+
+namespace cf {
+// cf_gemm_subgraph through a given scratch buffer (the allocation-free entry
+// point's device array): validation as cf_gemm_subgraph, then a plan without
+// the row-cluster path whose buffers must fit in scratch_bytes.
+// validate_only: check the arguments and that the plan fits scratch_bytes,
+// touch nothing on the device; *empty tells whether the call is a no-op.
+cf_status gemm_subgraph_scratch(const cf_subgraph_args* a, void* scratch, size_t scratch_bytes, void* hip_stream,
+                                bool validate_only, bool* empty) {
+  try {
+    RowEpi e;
+    cf_status s = subgraph_epi(a, e);
+    if (s != CF_OK) return s;
+    if (validate_only) {
+      size_t need = 0;
+      if ((s = rows_common(a->M, a->N, a->K, a->in_dtype, a->X, a->ldx, a->W, a->ldw, a->w_layout, e, a->path,
+                           nullptr, 0, nullptr, true, &need, true)) != CF_OK)
+        return s;
+      if (need > scratch_bytes)
+        return fail(CF_ERR_WORKSPACE,
+                    "this shape needs %zu bytes of scratch; the allocation-free entry point holds %zu", need,
+                    scratch_bytes);
+      if (empty) *empty = a->M == 0;
+      return CF_OK;
+    }
+    return rows_common(a->M, a->N, a->K, a->in_dtype, a->X, a->ldx, a->W, a->ldw, a->w_layout, e, a->path,
+                       scratch, scratch_bytes, hip_stream, false, nullptr, true);
+  } catch (...) {
+    return fail(CF_ERR_HIP, "internal error");
+  }
+}
+
+cf_status record_error(cf_status s, const char* what) { return fail(s, "%s", what); }
+}  // namespace cf
 
 extern "C" {
 
@@ -513,14 +569,6 @@ cf_status cf_gemm_postnorm(const cf_postnorm_args* a, void* workspace, size_t ws
   } catch (...) {
     return fail(CF_ERR_HIP, "internal error");
   }
-}
-
-static cf_status subgraph_epi(const cf_subgraph_args* a, RowEpi& e) {
-  if (!a) return fail(CF_ERR_NULL, "args is NULL");
-  if (a->struct_size != sizeof(cf_subgraph_args))
-    return fail(CF_ERR_STRUCT, "struct_size %zu != %zu", a->struct_size, sizeof(cf_subgraph_args));
-  if (a->in_dtype != CF_F32 && a->in_dtype != CF_BF16) return fail(CF_ERR_DTYPE, "in_dtype must be F32 or BF16");
-  return parse_nodes(a->nodes, a->n_nodes, a->M, a->N, a->in_dtype, e, false, nullptr, nullptr);
 }
 
 size_t cf_gemm_subgraph_workspace(const cf_subgraph_args* a) {

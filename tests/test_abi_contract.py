@@ -185,3 +185,26 @@ def test_workspace_check_without_workspace():
     assert cf.cf_workspace_check(None, 0, None) == 0
     assert cf.STATUS[cf.cf_workspace_check(A + 8, 64, None)] == "CF_ERR_ALIGN"
     assert cf.STATUS[cf.cf_workspace_check(A, 2, None)] == "CF_ERR_WORKSPACE"
+
+
+def test_noalloc_validation_before_any_device_call():
+    store = dict(kind=cf.CF_N_STORE, out=Y, ld=256, dtype=cf.CF_BF16)
+    ln = [dict(kind=cf.CF_N_LAYERNORM, f0=1e-5), store]
+    a, keep = _sg(ln, M=0)
+    assert cf.cf_gemm_subgraph_noalloc(a, None) == 0                 # M = 0: no-op
+    a, keep = _sg(ln)
+    a.path = cf.PATH_CLUSTER                                         # no cluster path here
+    assert cf.STATUS[cf.cf_gemm_subgraph_noalloc(a, None)] == "CF_ERR_UNSUPPORTED"
+    a, keep = _sg([dict(kind=cf.CF_N_GELU), store])
+    a.struct_size = 8
+    assert cf.STATUS[cf.cf_gemm_subgraph_noalloc(a, None)] == "CF_ERR_STRUCT"
+    # split path larger than the 32 MiB scratch: 4096 x 4096 fp32 rows
+    big_store = dict(kind=cf.CF_N_STORE, out=Y, ld=4096, dtype=cf.CF_BF16)
+    arr = cf.make_nodes([dict(kind=cf.CF_N_LAYERNORM, f0=1e-5), big_store])
+    b = cf.SubgraphArgs()
+    b.struct_size = C.sizeof(cf.SubgraphArgs)
+    b.M, b.N, b.K, b.in_dtype = 4096, 4096, 128, cf.CF_BF16
+    b.X, b.ldx, b.W, b.ldw, b.w_layout = A, 128, B, 128, cf.CF_LAYOUT_NK
+    b.nodes, b.n_nodes, b.path = arr, 2, 0
+    assert cf.STATUS[cf.cf_gemm_subgraph_noalloc(b, None)] == "CF_ERR_WORKSPACE"
+    assert "32" in cf.cf_last_error() or "scratch" in cf.cf_last_error()
