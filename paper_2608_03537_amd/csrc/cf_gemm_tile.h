@@ -67,7 +67,7 @@ struct TileShape {
   static constexpr int B_PT = (B_CHUNKS + NT - 1) / NT;
   static constexpr int LDS_STORE = TM * (TN * 4 + 16);   // staged output tile (fp32 worst case)
   // Row-reduction scratch sits at the end of LDS, past the staged output tile.
-  static constexpr int RED_BYTES = WN * TM * 4, TAIL_BYTES = RED_BYTES;
+  static constexpr int RED_BYTES = 3 * WN * TM * 4, TAIL_BYTES = RED_BYTES;   // (count, mean, M2) per row and wave column
   static constexpr int SMEM_V1 = LDS_V1 > LDS_STORE + TAIL_BYTES ? LDS_V1 : LDS_STORE + TAIL_BYTES;
   static constexpr int SMEM_V2 = LDS_V2 > LDS_STORE + TAIL_BYTES ? LDS_V2 : LDS_STORE + TAIL_BYTES;
   static_assert(SMEM_V1 <= 160 * 1024 && SMEM_V2 <= 160 * 1024, "LDS budget");
@@ -91,6 +91,32 @@ struct TileShape {
 };
 
 // ---------------------------------------------------------------------------
+// Accumulator start value.  When the epilogue adds the bias unscaled
+// (alpha = 1), the accumulators start from the bias of their columns, so
+// x = acc + bias comes out of the MFMA chain and stage 1 loses one add per
+// element.  Columns past N start at 0.  The loads are issued before any
+// main-loop load, so the first wait of the main loop covers them.
+// ---------------------------------------------------------------------------
+template <class S>
+__device__ __forceinline__ void acc_init(f32x16_t (&acc)[S::BM][S::BN], const GemmRowsParams& p, int n0, int lane,
+                                         int wn, bool fold_bias) {
+  const int lg = lane >> 5;
+#pragma unroll
+  for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int n = n0 + wn * S::WTN + bn * 32 + 8 * g + 4 * lg;
+      f32x4_t b = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (fold_bias && n < p.N) b = *reinterpret_cast<const f32x4_t*>(p.epi.bias + n);
+#pragma unroll
+      for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[bm][bn][4 * g + q] = b[q];
+    }
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// ---------------------------------------------------------------------------
 // Main loop: global -> registers -> LDS (double buffered) -> MFMA.
 // ---------------------------------------------------------------------------
 template <class S>
@@ -98,14 +124,9 @@ __device__ __forceinline__ void mainloop(f32x16_t (&acc)[S::BM][S::BN],
                                          const typename S::T* __restrict__ X,
                                          const typename S::T* __restrict__ W,
                                          const GemmRowsParams& p, int m0, int n0,
-                                         char* smem, int tid, int lane, int wm, int wn) {
+                                         char* smem, int tid, int lane, int wm, int wn, bool fold_bias) {
   using T = typename S::T;
-#pragma unroll
-  for (int bm = 0; bm < S::BM; ++bm)
-#pragma unroll
-    for (int bn = 0; bn < S::BN; ++bn)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[bm][bn][i] = 0.0f;
+  acc_init<S>(acc, p, n0, lane, wn, fold_bias);
 
   const int M = p.M, N = p.N, K = p.K;
   const int KT = (K + S::TK - 1) / S::TK;
@@ -272,14 +293,9 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
                                             const typename S::T* __restrict__ X,
                                             const typename S::T* __restrict__ W,
                                             const GemmRowsParams& p, int m0, int n0, int bz,
-                                            char* smem, int lane, int wave, int wm, int wn) {
+                                            char* smem, int lane, int wave, int wm, int wn, bool fold_bias) {
   using T = typename S::T;
-#pragma unroll
-  for (int bm = 0; bm < S::BM; ++bm)
-#pragma unroll
-    for (int bn = 0; bn < S::BN; ++bn)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[bm][bn][i] = 0.0f;
+  acc_init<S>(acc, p, n0, lane, wn, fold_bias);
 
   constexpr int NS = S::STAGES, PW = S::V2_PER_WAVE;
   const int KT = p.K / S::V2_TK;
@@ -466,6 +482,66 @@ __device__ __forceinline__ void wg_row_reduce(float (&v)[S::BM], float* red, int
   }
 }
 
+// Pairwise update of (count, mean, M2) of two disjoint sets (Chan, Golub and
+// LeVeque): d = mean_b - mean_a, mean = mean_a + d n_b / n, M2 = M2_a + M2_b
+// + d^2 n_a n_b / n.  An empty side leaves the other unchanged.
+__device__ __forceinline__ void chan_merge(float& n, float& mean, float& m2, float nb, float mb, float m2b) {
+  const float nn = n + nb;
+  if (nn > 0.0f) {
+    const float f = nb / nn, d = mb - mean;
+    mean = fmaf(d, f, mean);
+    m2 = m2 + m2b + d * d * (n * f);
+    n = nn;
+  }
+}
+
+// Levels 1 and 2 of the statistics reduction for (count, mean, M2) per row:
+// each lane holds its own row's partial statistics; the two lanes of a row
+// (l, l ^ 32) merge, then the WN waves sharing the row merge through LDS.
+// Every merge takes the parts in a fixed order (lane half 0 first, then wave
+// columns 0, 1, ...), so every lane of the row ends with identical values.
+template <class S>
+__device__ __forceinline__ void wg_stat_reduce(float (&n)[S::BM], float (&mean)[S::BM], float (&m2)[S::BM],
+                                               float* red, int lane, int wm, int wn) {
+  const int lg = lane >> 5;
+#pragma unroll
+  for (int bm = 0; bm < S::BM; ++bm) {
+    const float on = __shfl_xor(n[bm], 32), om = __shfl_xor(mean[bm], 32), o2 = __shfl_xor(m2[bm], 32);
+    float an = lg ? on : n[bm], am = lg ? om : mean[bm], a2 = lg ? o2 : m2[bm];
+    chan_merge(an, am, a2, lg ? n[bm] : on, lg ? mean[bm] : om, lg ? m2[bm] : o2);
+    n[bm] = an;
+    mean[bm] = am;
+    m2[bm] = a2;
+  }
+  if constexpr (S::WN > 1) {
+    const int lr = lane & 31;
+    if (lane < 32) {
+#pragma unroll
+      for (int bm = 0; bm < S::BM; ++bm) {
+        float* d = red + (wn * S::TM + wm * S::WTM + bm * 32 + lr) * 3;
+        d[0] = n[bm];
+        d[1] = mean[bm];
+        d[2] = m2[bm];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int bm = 0; bm < S::BM; ++bm) {
+      const int idx = wm * S::WTM + bm * 32 + lr;
+      float an = red[idx * 3], am = red[idx * 3 + 1], a2 = red[idx * 3 + 2];
+#pragma unroll
+      for (int w = 1; w < S::WN; ++w) {
+        const float* q = red + (w * S::TM + idx) * 3;
+        chan_merge(an, am, a2, q[0], q[1], q[2]);
+      }
+      n[bm] = an;
+      mean[bm] = am;
+      m2[bm] = a2;
+    }
+    __syncthreads();
+  }
+}
+
 // Level 3, ROWS_CLUSTER: the cn workgroups of a row block exchange per-row
 // partials through records in the workspace header.
 //
@@ -538,8 +614,8 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm) {
       unsigned long long* w = rec + ((size_t)c * kRecRows + wm * S::WTM + bm * 32 + lr) * 2;
-      __hip_atomic_store(w, rec_word(a[bm], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (!MAX) __hip_atomic_store(w + 1, rec_word(b[bm], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(w, rec_word(a[bm], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (!MAX) __hip_atomic_store(w + 1, rec_word(b[bm], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
   }
   const int cn = p.cn;
@@ -563,7 +639,7 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
           const unsigned long long* r = rec + ((size_t)cc * kRecRows + wm * S::WTM + bm * 32 + lr) * 2;
 #pragma unroll
           for (int v = 0; v < NV; ++v) {
-            w[bm][j][v] = __hip_atomic_load(r + v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            w[bm][j][v] = __builtin_nontemporal_load(r + v);
             ok = ok && (unsigned)(w[bm][j][v] >> 32) == tag;
           }
         }
@@ -718,7 +794,7 @@ __device__ __forceinline__ void epi_prefetch(EpiPrefetch<S>& pf, const GemmRowsP
       const int n = n0 + wn * S::WTN + bn * 32 + 8 * g + 4 * lg;
       const bool nv = n < p.N;
       pf.b[bn][g] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-      if (e.bias && nv) pf.b[bn][g] = *reinterpret_cast<const f32x4_t*>(e.bias + n);
+      if (e.bias && e.alpha != 1.0f && nv) pf.b[bn][g] = *reinterpret_cast<const f32x4_t*>(e.bias + n);
       if constexpr (EpiPrefetch<S>::PF_R) {
 #pragma unroll
         for (int bm = 0; bm < S::BM; ++bm) {
@@ -772,7 +848,9 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
   }
   // LDS operands are read a block at a time, all reads issued before the
   // first use (sched_barrier), so their latencies overlap.
-  if (e.bias) {   // only given terms are added (x + 0 would turn -0 into +0)
+  // Only given terms are added (x + 0 would turn -0 into +0).  With alpha = 1
+  // the accumulators started from the bias.
+  if (e.bias && alpha != 1.0f) {
 #pragma unroll
     for (int bn = 0; bn < S::BN; ++bn) {
       f32x4_t bv[4];
@@ -791,31 +869,37 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     }
   }
   if constexpr (STG) if (e.R) {
-    // Residual row r, columns 4j..4j+3 of chunk group c = j / 2: chunk position
-    // c ^ (r & 7) of that row's slot line.
+    // The residual by two MFMAs per 32 x 32 block with an identity operand:
+    // D[n][m] += sum_k I[n][k] R[m][16h + k] adds R[m][n] for n in
+    // [16h, 16h + 16) exactly (one non-zero product, rounded once into the
+    // accumulator like a VALU add).  Lane l supplies the identity row n = l % 32
+    // at k = 8 (l / 32) .. + 7 and, as the B operand, 8 consecutive residual
+    // values of its row: the 16-byte chunk 2h + l / 32 of the block's 32
+    // columns, which the staged layout keeps at chunk position c ^ (r & 7).
+    u32x4_t eye[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int e0 = lr - 16 * h - 8 * lg - 2 * w;   // one-hot position relative to this dword
+        eye[h][w] = (e0 == 0 ? 0x3F80u : 0u) | (e0 == 1 ? 0x3F800000u : 0u);
+      }
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm) {
       const int r = wm * S::WTM + bm * 32 + lr;
       const char* rowp = r < S::STG_RA ? smem + r * S::TN * 2 : smem + S::V2_STAGE + (r - S::STG_RA) * S::TN * 2;
-      u32x2_t rv[S::BN][4];
+      u32x4_t rv[S::BN][2];
 #pragma unroll
       for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int cl = col_l(bn, g);
-          rv[bn][g] = *reinterpret_cast<const u32x2_t*>(rowp + (((cl >> 3) ^ (r & 7)) << 4) + (cl & 7) * 2);
+        for (int h = 0; h < 2; ++h) {
+          const int cc = (wn * S::WTN + bn * 32) / 8 + 2 * h + lg;
+          rv[bn][h] = lds_read16(rowp + ((cc ^ (r & 7)) << 4));
         }
-      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const u32x2_t u = rv[bn][g];
-          x[bm][bn][4 * g + 0] += bf16_to_f32(u[0] & 0xFFFFu);
-          x[bm][bn][4 * g + 1] += bf16_to_f32(u[0] >> 16);
-          x[bm][bn][4 * g + 2] += bf16_to_f32(u[1] & 0xFFFFu);
-          x[bm][bn][4 * g + 3] += bf16_to_f32(u[1] >> 16);
-        }
+        for (int h = 0; h < 2; ++h) Mma<T>::run(x[bm][bn], eye[h], rv[bn][h]);
     }
   }
   if (!STG && e.R && !EpiPrefetch<S>::PF_R) {
@@ -870,32 +954,29 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
   }
 
   bool exchanged = false;
-  const int cnt_c = min(S::TN, N - n0);   // valid columns in this tile
 
   // ---- stage 2: row statistics and the normalising PostOp
   if (SPLIT || e.norm == NORM_LAYER) {
-    float s[S::BM];
-#pragma unroll
-    for (int bm = 0; bm < S::BM; ++bm) {
-      float t = 0.0f;
-#pragma unroll
-      for (int bn = 0; bn < S::BN; ++bn)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) t += x[bm][bn][i];
-      s[bm] = t;
-    }
-    wg_row_reduce<S, false>(s, red, lane, wm, wn);
-    const float inv_c = 1.0f / (float)cnt_c;
-    float mean[S::BM], m2[S::BM];
-#pragma unroll
-    for (int bm = 0; bm < S::BM; ++bm) mean[bm] = s[bm] * inv_c;
-    // sum of (x - mean)^2 over the tile's valid columns (padding columns of a
-    // ragged tile hold 0, not the mean, and are skipped)
-    auto dev2 = [&](auto ragged_t) {
+    // Per lane, two passes over its values of each row (sum, then squared
+    // deviations from the lane's own mean), then the merges of
+    // wg_stat_reduce: (mean, M2) of the tile's valid columns of every row.
+    float cnt[S::BM], mean[S::BM], m2[S::BM];
+    auto lane_stats = [&](auto ragged_t) {
       constexpr bool RAGGED = decltype(ragged_t)::value;
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) {
-        float t = 0.0f;
+        float t = 0.0f, nl = 0.0f;
+#pragma unroll
+        for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            if (RAGGED && ncol(bn, g) >= N) continue;
+            nl += 4.0f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) t += x[bm][bn][4 * g + q];
+          }
+        const float mu = RAGGED ? (nl > 0.0f ? t / nl : 0.0f) : t * (1.0f / (16 * S::BN));
+        float d2 = 0.0f;
 #pragma unroll
         for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
@@ -903,16 +984,18 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
             if (RAGGED && ncol(bn, g) >= N) continue;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-              const float d = x[bm][bn][4 * g + q] - mean[bm];
-              t = fmaf(d, d, t);
+              const float d = x[bm][bn][4 * g + q] - mu;
+              d2 = fmaf(d, d, d2);
             }
           }
-        m2[bm] = t;
+        cnt[bm] = RAGGED ? nl : (float)(16 * S::BN);
+        mean[bm] = mu;
+        m2[bm] = d2;
       }
     };
-    if (n0 + S::TN <= N) dev2(std::false_type{});
-    else dev2(std::true_type{});
-    wg_row_reduce<S, false>(m2, red, lane, wm, wn);
+    if (n0 + S::TN <= N) lane_stats(std::false_type{});
+    else lane_stats(std::true_type{});
+    wg_stat_reduce<S>(cnt, mean, m2, red, lane, wm, wn);
 
     if constexpr (SPLIT) {
       // Publish the tile's (mean, M2) and fp32 x (coalesced through LDS); the
@@ -1155,13 +1238,17 @@ __device__ __forceinline__ void epilogue_plain(f32x16_t (&x)[S::BM][S::BN], cons
                                                int wm, int wn) {
   const RowEpi& e = p.epi;
   const int lg = lane >> 5;
+  if (e.alpha != 1.0f) {
 #pragma unroll
-  for (int bm = 0; bm < S::BM; ++bm)
+    for (int bm = 0; bm < S::BM; ++bm)
 #pragma unroll
-    for (int bn = 0; bn < S::BN; ++bn)
+      for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) x[bm][bn][i] *= e.alpha;
-  if (e.bias) {   // only a given bias is added (x + 0 would turn -0 into +0)
+        for (int i = 0; i < 16; ++i) x[bm][bn][i] *= e.alpha;
+  }
+  // only a given bias is added (x + 0 would turn -0 into +0); with alpha = 1
+  // the accumulators started from it
+  if (e.bias && e.alpha != 1.0f) {
 #pragma unroll
     for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
@@ -1216,8 +1303,10 @@ void gemm_rows_kernel(GemmRowsParams p) {
     unsigned long long round_old = 0;
     if (cluster) round_old = round_begin(p, q * 8 + xcd, lane, S::NW);
     if constexpr (EPI >= 1 && !STG) epi_prefetch<S>(pf, p, m0, n0, bz, lane, wm, wn);
-    if constexpr (LOOP == 1) mainloop_v2<S, STG>(acc, X, W, p, m0, n0, bz, smem, lane, wave, wm, wn);
-    else mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn);
+    // The bias enters the accumulators unless alpha scales the product.
+    const bool fold_bias = p.epi.bias != nullptr && p.epi.alpha == 1.0f;
+    if constexpr (LOOP == 1) mainloop_v2<S, STG>(acc, X, W, p, m0, n0, bz, smem, lane, wave, wm, wn, fold_bias);
+    else mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn, fold_bias);
     unsigned tag = 0;
     if (cluster) {
       tag = round_tag(round_old);
