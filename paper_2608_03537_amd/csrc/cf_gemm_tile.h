@@ -488,7 +488,7 @@ __device__ __forceinline__ void wg_row_reduce(float (&v)[S::BM], float* red, int
 __device__ __forceinline__ void chan_merge(float& n, float& mean, float& m2, float nb, float mb, float m2b) {
   const float nn = n + nb;
   if (nn > 0.0f) {
-    const float f = nb / nn, d = mb - mean;
+    const float f = nb * __builtin_amdgcn_rcpf(nn), d = mb - mean;
     mean = fmaf(d, f, mean);
     m2 = m2 + m2b + d * d * (n * f);
     n = nn;
@@ -668,12 +668,15 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
                    vb * __builtin_amdgcn_exp2f((va - mn) * 1.4426950408889634f);
           mu[bm] = mn;
         } else {
+          // every peer holds TN columns: merging peer k (k peers merged
+          // before) weighs its mean by 1 / (k + 1) and the squared
+          // difference by TN k / (k + 1)
           const float vb = __uint_as_float((unsigned)w[bm][j][NV - 1]);
-          const float nb = (float)S::TN, nn = n_acc[bm] + nb;
+          const float k = n_acc[bm], f = __builtin_amdgcn_rcpf(k + 1.0f);
           const float d = va - mu[bm];
-          mu[bm] += d * (nb / nn);
-          sq[bm] += vb + d * d * (n_acc[bm] * nb / nn);
-          n_acc[bm] = nn;
+          mu[bm] = fmaf(d, f, mu[bm]);
+          sq[bm] += vb + d * d * ((float)S::TN * k * f);
+          n_acc[bm] = k + 1.0f;
         }
       }
   }
