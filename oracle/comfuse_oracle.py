@@ -282,6 +282,19 @@ def ffn_b2b(X, W1_kn, b1, W2_kn, b2, gamma=None, beta=None, eps=1e-5):
     return layernorm(bias_residual(O, b2, X), gamma, beta, eps)
 
 
+def mlp_b2b(X, W1_kn, b1, W2_kn, b2=None, out_relu=False):
+    """B2BGEMM MLP (Sec. IV, Eq. 2 with F = ReLU(. + b1)), the pattern of the
+    DLRM bottom MLP in Table 2 (1024 -> 512 -> 128):
+    P = X.W1 ; S = ReLU(P + b1) ; O = S.W2 + b2 ; with out_relu, ReLU(O) (the
+    activation of the MLP's next layer).  S is kept in fp64 (not rounded).
+    Reading: the paper names the DLRM MLP but not its activation; ReLU is the
+    activation of DLRM's MLP layers.
+    """
+    S = relu(bias_residual(matmul(X, W1_kn), b1))
+    O = bias_residual(matmul(S, W2_kn), b2)
+    return relu(O) if out_relu else O
+
+
 def attention(Q, K, V, scale=None):
     """Attention-style B2BGEMM (Sec. IV with F = softmax(scale * .)) per
     (batch, head): O = softmax(scale * Q.K^T) . V, plain two-pass softmax.

@@ -35,6 +35,7 @@ WL_ATTENTION = 5
 WL_MSTS = 6
 WL_SELF_ATTN_T2 = 7
 WL_TARGET_ATTN_T2 = 8
+WL_DLRM_MLP = 9
 WL_CUSTOM = 99
 
 
@@ -216,3 +217,29 @@ def target_attention_table2(seed=0, B=4, H=16, d=128) -> AttentionInputs:
     (key/value) rows.  The paper gives no head dimension, batch or head count;
     d = 128 as in its Self-Attention row, B = 4, H = 16 (2048 workgroups)."""
     return attention_inputs(seed, B, H, 4096, 256, d, WL_TARGET_ATTN_T2)
+
+
+@dataclass
+class MlpInputs:
+    """Operands of O = ReLU(X.W1 + b1).W2 + b2 (optionally ReLU(O))."""
+    M: int
+    K: int
+    N1: int
+    N2: int
+    X: np.ndarray    # M x K
+    W1: np.ndarray   # K x N1
+    b1: np.ndarray   # N1
+    W2: np.ndarray   # N1 x N2
+    b2: np.ndarray   # N2
+
+
+def dlrm_mlp_inputs(seed=0, M=65536, K=1024, N1=512, N2=128, workload=WL_DLRM_MLP) -> MlpInputs:
+    """The DLRM bottom-MLP shape of Table 2 (1024 -> 512 -> 128), bf16: X ~ N(0,1);
+    W1 ~ N(0, 1/K); W2 ~ N(0, 1/N1); b1, b2 ~ N(0, 0.02^2).  Table 2 gives no
+    batch; 65536 rows are used (the FFN workload's row count)."""
+    X = _normal(seed, workload, 0, (M, K), 1.0, "bf16")
+    W1 = _normal(seed, workload, 1, (K, N1), 1.0 / np.sqrt(K), "bf16")
+    b1 = _normal(seed, workload, 2, (N1,), 0.02, "f32")
+    W2 = _normal(seed, workload, 3, (N1, N2), 1.0 / np.sqrt(N1), "bf16")
+    b2 = _normal(seed, workload, 4, (N2,), 0.02, "f32")
+    return MlpInputs(M, K, N1, N2, X, W1, b1, W2, b2)

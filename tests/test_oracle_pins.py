@@ -433,3 +433,39 @@ def test_rowamax_quant_f32_matches_f64_off_ties():
     zero = np.zeros((2, 8), np.float32)
     s, q = O.rowamax_quant_f32(zero)
     assert np.all(s == 0) and np.all(q == 0)
+
+
+# ---------------------------------------------------------------- B2B MLP (DLRM pattern)
+def test_mlp_b2b_brute_force():
+    X = _small((4, 6), 40, 0)
+    W1, b1 = _small((6, 5), 40, 1, 0.5), _small((5,), 40, 2, 0.3)
+    W2, b2 = _small((5, 3), 40, 3, 0.5), _small((3,), 40, 4, 0.3)
+    P = _mm_exact(X, W1)
+    for out_relu in (False, True):
+        got = O.mlp_b2b(X, W1, b1, W2, b2, out_relu=out_relu)
+        for i in range(4):
+            h = [max(P[i][j] + Fraction(float(b1[j])), Fraction(0)) for j in range(5)]
+            for c in range(3):
+                o = sum(h[j] * Fraction(float(W2[j, c])) for j in range(5)) + Fraction(float(b2[c]))
+                if out_relu:
+                    o = max(o, Fraction(0))
+                assert abs(float(got[i, c]) - float(o)) <= 1e-14 * (1 + abs(float(o)))
+
+
+def test_mlp_b2b_special_cases():
+    rng = np.random.default_rng(41)
+    X, W1, b1 = rng.standard_normal((7, 16)), rng.standard_normal((16, 12)), rng.standard_normal(12)
+    W2, b2 = rng.standard_normal((12, 4)), rng.standard_normal(4)
+    # W2 = 0: every row is b2 (and ReLU(b2) with the output activation)
+    np.testing.assert_array_equal(O.mlp_b2b(X, W1, b1, np.zeros_like(W2), b2), np.broadcast_to(b2, (7, 4)))
+    np.testing.assert_array_equal(O.mlp_b2b(X, W1, b1, np.zeros_like(W2), b2, out_relu=True),
+                                  np.broadcast_to(np.maximum(b2, 0), (7, 4)))
+    # all pre-activations negative: S = 0, O = b2
+    np.testing.assert_array_equal(O.mlp_b2b(X, np.zeros_like(W1), -np.abs(b1) - 1, W2, b2), np.broadcast_to(b2, (7, 4)))
+    # positive pre-activations: ReLU is the identity, the MLP is linear (associativity, library matmul)
+    Xp, W1p, b1p = np.abs(X), np.abs(W1), np.abs(b1)
+    np.testing.assert_allclose(O.mlp_b2b(Xp, W1p, b1p, W2, b2), Xp @ (W1p @ W2) + (b1p @ W2 + b2), rtol=1e-12)
+    # the partial-sum identity of the N1 split: O = sum over hidden chunks of S_c W2_c
+    S = np.maximum(X @ W1 + b1, 0)
+    parts = sum(S[:, c:c + 4] @ W2[c:c + 4] for c in range(0, 12, 4))
+    np.testing.assert_allclose(O.mlp_b2b(X, W1, b1, W2, b2), parts + b2, rtol=1e-12, atol=1e-12)
