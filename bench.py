@@ -14,6 +14,8 @@ fraction of the bounding roofline (lower bound / time):
   ln_gelu_amax_fp8     Z = GELU(LN(X.W + b + R)), s = rowmax|Z|/448, Q = e4m3(Z/s),
                        bf16, 16384 x 4096 x 4096
   ffn_b2b              Y = LN(GELU(X.W1 + b1).W2 + b2 + X), bf16, 65536 x 256 x 512
+  dlrm_mlp_b2b         Y = ReLU(ReLU(X.W1 + b1).W2 + b2), bf16, 65536 x 1024 -> 512 -> 128 (Table 2),
+                       hidden units split over two workgroups per row block
   attention_b2b        O = softmax(Q.K^T / sqrt(128)).V, bf16, 4 x 16 heads, 2048 x 2048 x 128
   self_attention_table2    the same at sequence 512, head dim 128, 16 x 16 heads (Table 2)
   target_attention_table2  4096 target rows against 256 source rows, d 128, 4 x 16 heads (Table 2)
@@ -193,6 +195,12 @@ def cpu_baseline(I, inp, seconds):
     rec("ffn_b2b", 2.0 * 4096 * f.N1 * f.d * 2,
         lambda: O.ffn_b2b(f.X[fr], f.W1, f.b1, f.W2, f.b2, eps=f.eps), f"4096 of {f.M} rows, d {f.d}, N1 {f.N1}")
     del f
+    d = I.dlrm_mlp_inputs()
+    dr = slice(0, 2048)
+    rec("dlrm_mlp_b2b", 2.0 * 2048 * d.N1 * (d.K + d.N2),
+        lambda: O.mlp_b2b(d.X[dr], d.W1, d.b1, d.W2, d.b2, out_relu=True),
+        f"2048 of {d.M} rows, {d.K} -> {d.N1} -> {d.N2}")
+    del d
     a = I.attention_inputs()
     rec("attention_b2b", 2.0 * 2 * a.Lq * a.Lk * a.d * 2,
         lambda: O.attention(a.Q[0, :2], a.K[0, :2], a.V[0, :2]), f"2 of {a.B * a.H} heads, {a.Lq}x{a.Lk}, d {a.d}")
@@ -313,6 +321,45 @@ def workload_ffn(torch, cf, I, O, dev):
     nbytes = 2 * (2 * M * d + 2 * d * N1) + 4 * (N1 + 3 * d)
     return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2), timing=fstats,
                      shape={"M": M, "d": d, "N1": N1, "dtype": "bf16"})
+
+
+def workload_mlp(torch, cf, I, O, dev):
+    """DLRM bottom MLP of Table 2 (1024 -> 512 -> 128, 65536 rows, ReLU after
+    both layers): one B2B launch with the hidden units split over two
+    workgroups per row block, against cf_gemm + cf_rowop twice."""
+    inp = I.dlrm_mlp_inputs()
+    M, K, N1, N2 = inp.M, inp.K, inp.N1, inp.N2
+    bf = torch.bfloat16
+    W1t, W2t = tensor(torch, I.lay_out_weight(inp.W1, "nk"), bf, dev), tensor(torch, I.lay_out_weight(inp.W2, "nk"), bf, dev)
+    b1, b2 = tensor(torch, inp.b1, torch.float32, dev), tensor(torch, inp.b2, torch.float32, dev)
+    X0 = tensor(torch, inp.X, bf, dev)
+    sets = [dict(X=X0.clone(), Y=torch.empty((M, N2), dtype=bf, device=dev), P=torch.empty((M, N1), dtype=bf, device=dev),
+                 S=torch.empty((M, N1), dtype=bf, device=dev), O2=torch.empty((M, N2), dtype=bf, device=dev))
+            for _ in range(2)]
+    a = cf._b2b_args(batch=1, M=M, K=K, N1=N1, N2=N2, mid=cf.CF_MID_RELU_BIAS)
+    ws = cf.workspace(cf.cf_b2bgemm_workspace(a), dev, kind="b2b")
+    fused = time_steps(torch, [(lambda s=s: cf.b2b_mlp(s["X"], W1t, b1, W2t, b2, out_relu=True, out=s["Y"], ws=ws))
+                               for s in sets], 32, 4, replays=3)
+    fstats = replay_stats()
+    rows = np.array([0, 1, 127, 128, M - 1])
+    ref = O.mlp_b2b(inp.X[rows], inp.W1, inp.b1, inp.W2, inp.b2, out_relu=True)
+    err = float(np.max(np.abs(sets[0]["Y"][torch.from_numpy(rows).to(dev)].float().cpu().numpy() - ref)))
+
+    def unf(s):
+        g1 = [dict(kind=cf.CF_N_RELU), dict(kind=cf.CF_N_STORE, out=s["S"], ld=N1, dtype=cf.CF_BF16)]
+        g2 = [dict(kind=cf.CF_N_RELU), dict(kind=cf.CF_N_STORE, out=s["Y"], ld=N2, dtype=cf.CF_BF16)]
+
+        def run():
+            cf.gemm(s["X"], W1t, bias=b1, out=s["P"])
+            cf.rowop(s["P"], g1)
+            cf.gemm(s["S"], W2t, bias=b2, out=s["O2"])
+            cf.rowop(s["O2"], g2)
+        return run
+    unfused = time_steps(torch, [unf(s) for s in sets], 32, 4)
+    flop = 2.0 * M * N1 * (K + N2)
+    nbytes = 2 * (M * K + K * N1 + N1 * N2 + M * N2) + 4 * (N1 + N2)
+    return summarize(fused, unfused, flop, nbytes, "mfma_bf16", BF16_PEAK_TFLOPS, verdict(err, 2e-2), timing=fstats,
+                     shape={"M": M, "K": K, "N1": N1, "N2": N2, "dtype": "bf16", "hidden_split": N1 // 256})
 
 
 def workload_attention(torch, cf, I, O, dev, a=None):
@@ -548,7 +595,7 @@ def main():
     if not args.only_main:
         wl = {}
         for name, fn in [("postnorm_tiny_fp32", workload_tiny), ("ln_gelu_amax_fp8", workload_chain),
-                         ("ffn_b2b", workload_ffn), ("attention_b2b", workload_attention),
+                         ("ffn_b2b", workload_ffn), ("dlrm_mlp_b2b", workload_mlp), ("attention_b2b", workload_attention),
                          ("self_attention_table2",
                           lambda *w: workload_attention(*w, a=I.self_attention_table2())),
                          ("target_attention_table2",

@@ -208,12 +208,15 @@ cf_status cf_gemm_subgraph_noalloc(const cf_subgraph_args* a, void* hip_stream);
  * independent problems (strides sx, sw1, ... in elements).
  *
  *   mid = CF_MID_GELU_BIAS : S = GELU(P + b1)                       (FFN)
+ *   mid = CF_MID_RELU_BIAS : S = ReLU(P + b1)        (MLP, the DLRM bottom
+ *                            MLP of Table 2)
  *   mid = CF_MID_SOFTMAX   : S = softmax_row(mid_scale * P), computed
  *                            online over blocks of N1 (running row max and
  *                            sum in fp32), so O = S W2 is exact softmax   (attention);
  *                            mid_scale must be finite and > 0 (CF_ERR_SHAPE)
  *   out = CF_OUT_STORE     : Y = O (+ b2 if given)
  *   out = CF_OUT_BIAS_RESIDUAL_LN : Y = LN(O + b2 + R) * gamma + beta
+ *   out = CF_OUT_BIAS_RELU : Y = ReLU(O + b2)                     (MLP only)
  *
  * FFN: W1 is given as W1^T (N1 x K, CF_LAYOUT_NK), W2 as W2^T (N2 x N1,
  * CF_LAYOUT_NK); the model width d = K = N2 (CF_ERR_UNSUPPORTED otherwise);
@@ -225,10 +228,21 @@ cf_status cf_gemm_subgraph_noalloc(const cf_subgraph_args* a, void* hip_stream);
  * Lk x d (CF_LAYOUT_KN); out = CF_OUT_STORE, b1 = b2 = R = NULL.
  * All matrices bf16 (dtype = CF_BF16), 16-byte aligned, leading dimensions
  * and batch strides multiples of 8 elements.  Output O is M x N2 bf16.
- * Workspace: none (cf_b2bgemm_workspace returns 0).
+ * MLP: W1 given as W1^T (N1 x K, CF_LAYOUT_NK), W2 as W2^T (N2 x N1,
+ * CF_LAYOUT_NK); N2 = 128, N1 a multiple of 256, K a multiple of 64 and
+ * >= 128; b1 [N1] / b2 [N2] fp32 or NULL; out = CF_OUT_STORE or
+ * CF_OUT_BIAS_RELU; R, gamma, beta NULL.  N1 is split into chunks of 256
+ * hidden units, one workgroup per chunk and 128-row block (the cross-CTA
+ * dataflow of Sec. IV-A); their partial second products are summed at
+ * commit, in chunk order, by the last workgroup of the row block to finish.
+ * Workspace: 0 bytes for the FFN, attention, and MLP with N1 = 256; for MLP
+ * with N1 > 256, cf_b2bgemm_workspace() bytes: arrival counters, then fp32
+ * partial products.  Zero-fill the workspace once before its first MLP call;
+ * every call leaves the counters at zero again.  Do not share it with calls
+ * of another kind, and do not let calls that share it overlap in time.
  * ------------------------------------------------------------------------ */
-typedef enum { CF_MID_GELU_BIAS = 0, CF_MID_SOFTMAX = 1 } cf_mid_op;
-typedef enum { CF_OUT_STORE = 0, CF_OUT_BIAS_RESIDUAL_LN = 1 } cf_out_op;
+typedef enum { CF_MID_GELU_BIAS = 0, CF_MID_SOFTMAX = 1, CF_MID_RELU_BIAS = 2 } cf_mid_op;
+typedef enum { CF_OUT_STORE = 0, CF_OUT_BIAS_RESIDUAL_LN = 1, CF_OUT_BIAS_RELU = 2 } cf_out_op;
 
 typedef struct {
   size_t struct_size;            /* = sizeof(cf_b2b_args) */

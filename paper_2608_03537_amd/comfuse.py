@@ -23,8 +23,8 @@ CF_F32, CF_BF16, CF_FP8_E4M3 = 0, 1, 2
 CF_LAYOUT_KN, CF_LAYOUT_NK = 0, 1
 (CF_N_SCALE, CF_N_BIAS, CF_N_RESIDUAL, CF_N_LAYERNORM, CF_N_RMSNORM, CF_N_GELU,
  CF_N_GELU_TANH, CF_N_RELU, CF_N_STORE, CF_N_ROWAMAX_QUANT, CF_N_SOFTMAX, CF_N_SOFTCAP) = range(12)
-CF_MID_GELU_BIAS, CF_MID_SOFTMAX = 0, 1
-CF_OUT_STORE, CF_OUT_BIAS_RESIDUAL_LN = 0, 1
+CF_MID_GELU_BIAS, CF_MID_SOFTMAX, CF_MID_RELU_BIAS = 0, 1, 2
+CF_OUT_STORE, CF_OUT_BIAS_RESIDUAL_LN, CF_OUT_BIAS_RELU = 0, 1, 2
 PATH_AUTO, PATH_WHOLE_ROW, PATH_CLUSTER, PATH_SPLIT = 0, 1, 2, 3
 STATUS = {0: "CF_OK", 1: "CF_ERR_NULL", 2: "CF_ERR_SHAPE", 3: "CF_ERR_LD", 4: "CF_ERR_ALIGN",
           5: "CF_ERR_DTYPE", 6: "CF_ERR_WORKSPACE", 7: "CF_ERR_UNSUPPORTED", 8: "CF_ERR_ALIAS",
@@ -205,15 +205,16 @@ def _capturing():
     return _torch().cuda.is_current_stream_capturing()
 
 
-def workspace(nbytes, device, stream=None):
+def workspace(nbytes, device, stream=None, kind="rows"):
     """A zero-initialised workspace of at least nbytes on ``device``, cached per
-    (device, stream): calls on one stream run in order, so they may share it;
-    calls on different streams get different workspaces (the row-cluster
-    round counters live in it)."""
+    (device, stream, kind): calls on one stream run in order, so they may
+    share it; calls on different streams get different workspaces (the
+    row-cluster round counters live in it).  kind "b2b" is the split MLP's
+    (its arrival counters must not meet another entry point's data)."""
     torch = _torch()
     if nbytes == 0:
         return None
-    key = (str(device), _stream(stream))
+    key = (str(device), _stream(stream), kind)
     ws = _ws_cache.get(key)
     if ws is None or ws.numel() < nbytes:
         ws = torch.zeros(max(nbytes, 1 << 20), dtype=torch.uint8, device=device)
@@ -407,6 +408,27 @@ def b2b_ffn(X, W1t, b1, W2t, b2=None, R=None, gamma=None, beta=None, *, eps=1e-5
                   R=_ptr(R), ldr=(_ld(R) if R is not None else 0), sr=0,
                   gamma=_ptr(gamma), beta=_ptr(beta), eps=eps, O=_ptr(O), ldo=_ld(O), so=0)
     _check(cf_b2bgemm(a, None, 0, _stream(stream)))
+    return O
+
+
+def b2b_mlp(X, W1t, b1, W2t, b2=None, *, out_relu=False, out=None, ws=None, stream=None):
+    """Fused MLP block O = ReLU(X W1 + b1) W2 + b2 (ReLU(O) with out_relu), the
+    DLRM bottom-MLP pattern.  X [M, K] bf16; W1t = W1^T [N1, K]; W2t = W2^T
+    [N2, N1]; hidden units split over workgroups in chunks of 256."""
+    torch = _torch()
+    M, K = X.shape
+    N1, N2 = W1t.shape[0], W2t.shape[0]
+    O = out if out is not None else torch.empty((M, N2), dtype=torch.bfloat16, device=X.device)
+    a = _b2b_args(batch=1, M=M, K=K, N1=N1, N2=N2, dtype=CF_BF16,
+                  X=_ptr(X), ldx=_ld(X), sx=0, W1=_ptr(W1t), ldw1=_ld(W1t), sw1=0, w1_layout=CF_LAYOUT_NK,
+                  b1=_ptr(b1), mid=CF_MID_RELU_BIAS, mid_scale=1.0,
+                  W2=_ptr(W2t), ldw2=_ld(W2t), sw2=0, w2_layout=CF_LAYOUT_NK,
+                  out=CF_OUT_BIAS_RELU if out_relu else CF_OUT_STORE, b2=_ptr(b2),
+                  R=None, ldr=0, sr=0, gamma=None, beta=None, eps=0.0, O=_ptr(O), ldo=_ld(O), so=0)
+    need = cf_b2bgemm_workspace(a)
+    if ws is None:
+        ws = workspace(need, X.device, stream, kind="b2b")
+    _check(cf_b2bgemm(a, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
     return O
 
 

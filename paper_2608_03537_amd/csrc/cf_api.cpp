@@ -697,14 +697,25 @@ cf_status cf_workspace_check(void* workspace, size_t ws_bytes, void* hip_stream)
   }
 }
 
+// Workspace of the split MLP: arrival counters [batch][row blocks] (256-byte
+// aligned block), then fp32 partials [batch][cn][M][N2].  Other B2B forms need none.
+static size_t mlp_workspace(const cf_b2b_args* a) {
+  if (!a || a->struct_size != sizeof(cf_b2b_args) || a->mid != CF_MID_RELU_BIAS || a->N1 <= kMlpHidden ||
+      a->M <= 0 || a->batch <= 0)
+    return 0;
+  const int64_t rbs = (a->M + kMlpRows - 1) / kMlpRows, cn = a->N1 / kMlpHidden;
+  return round_up((size_t)(a->batch * rbs * 4), 256) + (size_t)(a->batch * cn * a->M * a->N2 * 4);
+}
+
 size_t cf_b2bgemm_workspace(const cf_b2b_args* a) {
-  (void)a;
-  return 0;
+  try {
+    return mlp_workspace(a);
+  } catch (...) {
+    return 0;
+  }
 }
 
 cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, void* hip_stream) {
-  (void)workspace;
-  (void)ws_bytes;
   try {
     if (!a) return fail(CF_ERR_NULL, "args is NULL");
     if (a->struct_size != sizeof(cf_b2b_args))
@@ -713,11 +724,30 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, voi
     if (a->batch < 0 || a->batch > 65535 || a->M < 0 || a->K <= 0 || a->N1 <= 0 || a->N2 <= 0)
       return fail(CF_ERR_SHAPE, "need 0 <= batch <= 65535, M >= 0, K, N1, N2 > 0");
     if (a->M > (int64_t)1 << 30 || a->N1 > (int64_t)1 << 30) return fail(CF_ERR_SHAPE, "size exceeds 2^30");
-    const bool ffn = a->mid == CF_MID_GELU_BIAS;
-    if (!ffn && a->mid != CF_MID_SOFTMAX) return fail(CF_ERR_UNSUPPORTED, "unknown mid op");
-    if (a->out != CF_OUT_STORE && a->out != CF_OUT_BIAS_RESIDUAL_LN) return fail(CF_ERR_UNSUPPORTED, "unknown out op");
+    const bool ffn = a->mid == CF_MID_GELU_BIAS, mlp = a->mid == CF_MID_RELU_BIAS;
+    if (!ffn && !mlp && a->mid != CF_MID_SOFTMAX) return fail(CF_ERR_UNSUPPORTED, "unknown mid op");
+    if (a->out != CF_OUT_STORE && a->out != CF_OUT_BIAS_RESIDUAL_LN && a->out != CF_OUT_BIAS_RELU)
+      return fail(CF_ERR_UNSUPPORTED, "unknown out op");
+    if (a->out == CF_OUT_BIAS_RELU && !mlp) return fail(CF_ERR_UNSUPPORTED, "the output ReLU belongs to the MLP form");
     cf_status s;
-    if (ffn) {
+    if (mlp) {
+      if (a->w1_layout != CF_LAYOUT_NK || a->w2_layout != CF_LAYOUT_NK)
+        return fail(CF_ERR_UNSUPPORTED, "MLP weights must be stored N x K (W1^T: N1 x K, W2^T: N2 x N1)");
+      if (!b2b_mlp_supported((int)std::min<int64_t>(a->K, 1 << 30), (int)a->N1, (int)a->N2))
+        return fail(CF_ERR_UNSUPPORTED, "MLP needs N2 = 128, N1 a multiple of %d, K a multiple of 64 and >= 128 "
+                    "(K = %lld, N1 = %lld, N2 = %lld)", kMlpHidden, (long long)a->K, (long long)a->N1, (long long)a->N2);
+      if (a->out == CF_OUT_BIAS_RESIDUAL_LN || a->R || a->gamma || a->beta)
+        return fail(CF_ERR_UNSUPPORTED, "the MLP form stores O + b2 or ReLU(O + b2) only");
+      if ((s = check_vec("b1", a->b1)) != CF_OK) return s;
+      if (a->M > 0 && a->batch > 0) {
+        const size_t need = mlp_workspace(a);
+        if (need > 0) {
+          if (!workspace) return fail(CF_ERR_WORKSPACE, "workspace of %zu bytes required (N1 split over workgroups)", need);
+          if (ws_bytes < need) return fail(CF_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+          if (!aligned16(workspace)) return fail(CF_ERR_ALIGN, "workspace is not 16-byte aligned");
+        }
+      }
+    } else if (ffn) {
       if (a->w1_layout != CF_LAYOUT_NK || a->w2_layout != CF_LAYOUT_NK)
         return fail(CF_ERR_UNSUPPORTED, "FFN weights must be stored N x K (W1^T: N1 x K, W2^T: N2 x N1)");
       if (a->K != a->N2) return fail(CF_ERR_UNSUPPORTED, "FFN needs K == N2 = d (K = %lld, N2 = %lld)", (long long)a->K, (long long)a->N2);
@@ -736,8 +766,8 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, voi
         return fail(CF_ERR_SHAPE, "mid_scale must be finite and > 0");
     }
     const bool empty = a->M == 0 || a->batch == 0;
-    const int64_t w1_rows = ffn ? a->N1 : a->N1, w1_cols = a->K;
-    const int64_t w2_rows = ffn ? a->N2 : a->N1, w2_cols = ffn ? a->N1 : a->N2;
+    const int64_t w1_rows = a->N1, w1_cols = a->K;
+    const int64_t w2_rows = (ffn || mlp) ? a->N2 : a->N1, w2_cols = (ffn || mlp) ? a->N1 : a->N2;
     if ((s = check_matrix("X", a->X, empty ? 0 : a->M, a->K, a->ldx, CF_BF16, true)) != CF_OK) return s;
     if ((s = check_matrix("W1", a->W1, empty ? 0 : w1_rows, w1_cols, a->ldw1, CF_BF16, true)) != CF_OK) return s;
     if ((s = check_matrix("W2", a->W2, empty ? 0 : w2_rows, w2_cols, a->ldw2, CF_BF16, true)) != CF_OK) return s;
@@ -781,6 +811,17 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, voi
     p.ldo = a->ldo;
     p.so = a->so;
     hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+    if (mlp) {
+      p.out_relu = a->out == CF_OUT_BIAS_RELU;
+      p.cn = (int)(a->N1 / kMlpHidden);
+      if (p.cn > 1) {
+        const int64_t rbs = (a->M + kMlpRows - 1) / kMlpRows;
+        char* b = reinterpret_cast<char*>(workspace);
+        p.ws_count = reinterpret_cast<unsigned*>(b);
+        p.ws_part = reinterpret_cast<float*>(b + round_up((size_t)(a->batch * rbs * 4), 256));
+      }
+      return hip_status(launch_b2b_mlp(p, st), "B2B MLP launch");
+    }
     return hip_status(ffn ? launch_b2b_ffn(p, st) : launch_b2b_attention(p, st), "B2B launch");
   } catch (...) {
     return fail(CF_ERR_HIP, "internal error");

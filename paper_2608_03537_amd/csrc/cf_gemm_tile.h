@@ -97,7 +97,12 @@ struct TileShape {
 // element.  Columns past N start at 0.  The loads are issued before any
 // main-loop load, so the first wait of the main loop covers them.
 // ---------------------------------------------------------------------------
-template <class S>
+// PERM: the main loop loads the W^T rows of every 32-row block with bits 2
+// and 3 of the row index swapped (perm23), so accumulator elements 4g..4g+3
+// of lane half lg hold columns 16 (g / 2) + 8 lg + 4 (g % 2) + 0..3 of the block.
+__device__ __forceinline__ int perm23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
+
+template <class S, bool PERM = false>
 __device__ __forceinline__ void acc_init(f32x16_t (&acc)[S::BM][S::BN], const GemmRowsParams& p, int n0, int lane,
                                          int wn, bool fold_bias) {
   const int lg = lane >> 5;
@@ -105,7 +110,7 @@ __device__ __forceinline__ void acc_init(f32x16_t (&acc)[S::BM][S::BN], const Ge
   for (int bn = 0; bn < S::BN; ++bn)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const int n = n0 + wn * S::WTN + bn * 32 + 8 * g + 4 * lg;
+      const int n = n0 + wn * S::WTN + bn * 32 + (PERM ? 16 * (g >> 1) + 8 * lg + 4 * (g & 1) : 8 * g + 4 * lg);
       f32x4_t b = {0.0f, 0.0f, 0.0f, 0.0f};
       if (fold_bias && n < p.N) b = *reinterpret_cast<const f32x4_t*>(p.epi.bias + n);
 #pragma unroll
@@ -288,14 +293,14 @@ __device__ __forceinline__ void wait_vmcnt() {
 // Rows past M (or N) are clamped to the last valid row: they only feed output
 // rows/columns that the epilogue masks.
 // ---------------------------------------------------------------------------
-template <class S, bool STG>
+template <class S, bool STG, bool PERM = false>
 __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
                                             const typename S::T* __restrict__ X,
                                             const typename S::T* __restrict__ W,
                                             const GemmRowsParams& p, int m0, int n0, int bz,
                                             char* smem, int lane, int wave, int wm, int wn, bool fold_bias) {
   using T = typename S::T;
-  acc_init<S>(acc, p, n0, lane, wn, fold_bias);
+  acc_init<S, PERM>(acc, p, n0, lane, wn, fold_bias);
 
   constexpr int NS = S::STAGES, PW = S::V2_PER_WAVE;
   const int KT = p.K / S::V2_TK;
@@ -308,7 +313,7 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
     const int row = (wave + j * S::NW) * 8 + (lane >> 3);
     const int c = (lane & 7) ^ ((row >> 1) & 7);
     if (row < S::TN) {
-      const int n = min(n0 + row, p.N - 1);
+      const int n = min(n0 + (PERM ? perm23(row) : row), p.N - 1);
       src[j] = reinterpret_cast<const char*>(W + (int64_t)n * p.ldw) + c * 16;
     } else {
       const int m = min(m0 + row - S::TN, p.M - 1);

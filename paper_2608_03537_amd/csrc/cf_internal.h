@@ -131,6 +131,12 @@ struct B2BParams {
   const uint16_t* R; int64_t ldr, sr;     // residual M x N2 or NULL
   const float* gamma; const float* beta; float eps;
   uint16_t* O; int64_t ldo, so;           // M x N2 output (bf16)
+  // MLP (S = ReLU(P + b1)): output ReLU, and the split of N1 over cn
+  // workgroups whose partial second products are summed at commit
+  int out_relu;
+  int cn;                                  // workgroups per row block (N1 / 256)
+  unsigned* ws_count;                      // [batch][row blocks] arrival counters (zero between calls)
+  float* ws_part;                          // [batch][cn][M][N2] fp32 partial products
 };
 
 // Launchers (return hipSuccess or the launch error).
@@ -138,7 +144,10 @@ hipError_t launch_gemm_rows(const GemmRowsParams& p, int idx, hipStream_t st);
 hipError_t launch_row_kernel(const RowKernelParams& p, hipStream_t st);
 hipError_t launch_b2b_ffn(const B2BParams& p, hipStream_t st);        // -> hipErrorInvalidValue if N1/N2 not compiled
 hipError_t launch_b2b_attention(const B2BParams& p, hipStream_t st);  // -> hipErrorInvalidValue if d not compiled
+hipError_t launch_b2b_mlp(const B2BParams& p, hipStream_t st);        // -> hipErrorInvalidValue if N2 not compiled
 bool b2b_ffn_supported(int N1, int N2);
+bool b2b_mlp_supported(int K, int N1, int N2);
+constexpr int kMlpRows = 128, kMlpHidden = 256;   // rows and hidden units of one MLP workgroup
 bool b2b_attention_supported(int d);
 
 }  // namespace cf

@@ -208,3 +208,26 @@ def test_noalloc_validation_before_any_device_call():
     b.nodes, b.n_nodes, b.path = arr, 2, 0
     assert cf.STATUS[cf.cf_gemm_subgraph_noalloc(b, None)] == "CF_ERR_WORKSPACE"
     assert "32" in cf.cf_last_error() or "scratch" in cf.cf_last_error()
+
+
+def _mlp(**kw):
+    a = cf.B2BArgs()
+    a.struct_size = C.sizeof(cf.B2BArgs)
+    a.batch, a.M, a.K, a.N1, a.N2 = 1, kw.get("M", 300), kw.get("K", 1024), kw.get("N1", 512), kw.get("N2", 128)
+    a.dtype, a.mid, a.out = cf.CF_BF16, cf.CF_MID_RELU_BIAS, kw.get("out", cf.CF_OUT_STORE)
+    a.X, a.ldx, a.W1, a.ldw1, a.w1_layout = A, a.K, B, a.K, cf.CF_LAYOUT_NK
+    a.W2, a.ldw2, a.w2_layout = R, a.N1, cf.CF_LAYOUT_NK
+    a.b1, a.b2, a.O, a.ldo = V, V, Y, a.N2
+    return a
+
+
+def test_mlp_workspace_and_validation():
+    # counters for ceil(300 / 128) = 3 row blocks (256-byte block), then 2 x 300 x 128 fp32 partials
+    assert cf.cf_b2bgemm_workspace(_mlp()) == 256 + 2 * 300 * 128 * 4
+    assert cf.cf_b2bgemm_workspace(_mlp(N1=256)) == 0           # one chunk: nothing to sum
+    assert cf.STATUS[cf.cf_b2bgemm(_mlp(), None, 0, None)] == "CF_ERR_WORKSPACE"
+    assert cf.STATUS[cf.cf_b2bgemm(_mlp(N2=64), A, 1 << 30, None)] == "CF_ERR_UNSUPPORTED"
+    assert cf.STATUS[cf.cf_b2bgemm(_mlp(N1=384), A, 1 << 30, None)] == "CF_ERR_UNSUPPORTED"
+    assert cf.STATUS[cf.cf_b2bgemm(_mlp(K=96), A, 1 << 30, None)] == "CF_ERR_UNSUPPORTED"
+    assert cf.STATUS[cf.cf_b2bgemm(_mlp(out=cf.CF_OUT_BIAS_RESIDUAL_LN), A, 1 << 30, None)] == "CF_ERR_UNSUPPORTED"
+    assert cf.cf_b2bgemm(_mlp(M=0), None, 0, None) == 0

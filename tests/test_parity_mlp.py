@@ -1,0 +1,78 @@
+"""GPU parity of the back-to-back MLP (cf_b2bgemm with S = ReLU(X W1 + b1),
+the DLRM bottom-MLP pattern of Table 2) against the fp64 oracle.
+
+O is bf16: max-abs 2e-2 and rel-RMS 5e-3 (the intermediate S is rounded to
+bf16 as the second product's operand; the oracle keeps it exact).  The hidden
+dimension is split over workgroups in chunks of 256 units; their partial
+second products are summed at commit by the last workgroup of each row block
+to finish, in chunk order, so the result is the same whichever finishes last.
+"""
+import numpy as np
+import pytest
+
+from oracle import comfuse_oracle as O
+from paper_2608_03537_amd import inputs as I
+from tests.helpers import assert_close_bf16, dev, host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2608_03537_amd import comfuse as cf  # noqa: E402
+
+
+def run_mlp(inp, out_relu=False, with_b2=True, ws=None):
+    Y = cf.b2b_mlp(dev(inp.X), dev(I.lay_out_weight(inp.W1, "nk")), dev(inp.b1, "f32"),
+                   dev(I.lay_out_weight(inp.W2, "nk")), dev(inp.b2, "f32") if with_b2 else None,
+                   out_relu=out_relu, ws=ws)
+    torch.cuda.synchronize()
+    return Y
+
+
+@pytest.mark.parametrize("M,K,N1", [(300, 128, 256), (257, 256, 512), (129, 192, 768), (77, 1024, 512)])
+@pytest.mark.parametrize("out_relu", [False, True])
+def test_mlp_small(M, K, N1, out_relu):
+    inp = I.dlrm_mlp_inputs(seed=3, M=M, K=K, N1=N1)
+    got = host(run_mlp(inp, out_relu))
+    ref = O.mlp_b2b(inp.X, inp.W1, inp.b1, inp.W2, inp.b2, out_relu=out_relu)
+    assert_close_bf16(got, ref, f"MLP {M}x{K}x{N1} relu={out_relu}")
+
+
+def test_mlp_without_b2_and_all_negative_hidden():
+    inp = I.dlrm_mlp_inputs(seed=4, M=200, K=256, N1=512)
+    got = host(run_mlp(inp, with_b2=False))
+    assert_close_bf16(got, O.mlp_b2b(inp.X, inp.W1, inp.b1, inp.W2, None), "MLP without b2")
+    # every pre-activation negative: S = 0 and O = b2 exactly
+    inp.b1[:] = -100.0
+    got = host(run_mlp(inp))
+    assert np.array_equal(got, np.broadcast_to(I.round_to_bf16(inp.b2.astype(np.float32)).astype(np.float64),
+                                                got.shape))
+
+
+def test_mlp_split_is_deterministic_and_leaves_counters_at_zero():
+    inp = I.dlrm_mlp_inputs(seed=5, M=4096, K=512, N1=1024)
+    X, W1, W2 = dev(inp.X), dev(I.lay_out_weight(inp.W1, "nk")), dev(I.lay_out_weight(inp.W2, "nk"))
+    b1, b2 = dev(inp.b1, "f32"), dev(inp.b2, "f32")
+    ws = torch.zeros(64 << 20, dtype=torch.uint8, device="cuda")
+    outs = [cf.b2b_mlp(X, W1, b1, W2, b2, ws=ws) for _ in range(3)]
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
+    rbs = (inp.M + 127) // 128
+    assert int(ws[:rbs * 4].view(torch.int32).abs().sum().item()) == 0
+    assert_close_bf16(host(outs[0]), O.mlp_b2b(inp.X, inp.W1, inp.b1, inp.W2, inp.b2), "MLP 4096x512x1024")
+
+
+def test_mlp_dlrm_full_size_block_rows():
+    # the Table 2 widths 1024 -> 512 -> 128 at 65536 rows: one row in every
+    # 128-row block (both workgroups of the block and their commit) against
+    # the oracle, and the ReLU output's exact zero count against the oracle's
+    inp = I.dlrm_mlp_inputs()
+    Y = host(run_mlp(inp, out_relu=True))
+    nb = inp.M // 128
+    rows = np.arange(nb) * 128 + (np.arange(nb) * 37) % 128
+    ref = O.mlp_b2b(inp.X[rows], inp.W1, inp.b1, inp.W2, inp.b2, out_relu=True)
+    assert_close_bf16(Y[rows], ref, "DLRM MLP 65536x1024x512x128")
+    assert np.all(Y >= 0.0)
