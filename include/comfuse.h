@@ -52,7 +52,7 @@ extern "C" {
 #endif
 
 #define CF_VERSION 1
-#define CF_WS_HEADER_BYTES 8392704  /* 4096 + 2 stages * 2 parities * 64 * 16 * 128 * 16 */
+#define CF_WS_HEADER_BYTES 8916992  /* 4096 + 2 stages * 2 parities * 64 slots * 17 records * 128 rows * 16 */
 
 typedef enum {
   CF_F32 = 0,       /* IEEE binary32 */

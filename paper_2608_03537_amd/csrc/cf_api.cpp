@@ -219,6 +219,7 @@ void bind_workspace(const Plan& pl, void* ws, GemmRowsParams& p) {
     static_assert(kWsCounterBytes % 256 == 0, "records alignment");
     p.ws_part = reinterpret_cast<float*>(b + pl.off_part);
     p.spin_limit = kSpinLimitDefault;
+    p.leader = pl.cn >= kLeaderFollowerPeers;
   } else if (pl.mode == ROWS_SPLIT) {
     p.ws_part = reinterpret_cast<float*>(b + pl.off_part);
     p.ws_x = reinterpret_cast<float*>(b + pl.off_x);

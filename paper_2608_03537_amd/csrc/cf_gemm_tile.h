@@ -604,7 +604,10 @@ enum MergeKind {
 // Publishes (a, b) (MERGE_MAX: a only) of this workgroup's rows, then reads
 // every peer's records of the lane's rows, peer 0 first, until all carry
 // `tag`, and merges them in that order.  Every workgroup merges in the same
-// order, so all get bit-identical values.
+// order, so all get bit-identical values.  With p.leader (many peers, the
+// dual-mode aggregation of Sec. III-A) only peer 0 reads and merges all
+// records; it publishes the merged values in record kRecLead, which the
+// other peers read instead.
 template <class S, int MERGE>
 __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int stage, int slot, int c, unsigned tag,
                                                  float (&a)[S::BM], float (&b)[S::BM], int lane, int wm, int wn) {
@@ -624,6 +627,37 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
     }
   }
   const int cn = p.cn;
+  if (p.leader && c != 0) {
+    // Leader-follower (for many peers): peer 0 merges every record and
+    // publishes the result; the others read that one record only.
+    unsigned long long w[S::BM][NV];
+    for (int spins = 0;; ++spins) {
+      const unsigned err = __hip_atomic_load(p.ws_err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      bool ok = true;
+#pragma unroll
+      for (int bm = 0; bm < S::BM; ++bm) {
+        const unsigned long long* r = rec + ((size_t)kRecLead * kRecRows + wm * S::WTM + bm * 32 + lr) * 2;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+          w[bm][v] = __builtin_nontemporal_load(r + v);
+          ok = ok && (unsigned)(w[bm][v] >> 32) == tag;
+        }
+      }
+      if (__all(ok)) break;
+      if (__builtin_amdgcn_readfirstlane(err) != 0u) break;
+      if (spins >= p.spin_limit) {
+        __hip_atomic_store(p.ws_err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+#pragma unroll
+    for (int bm = 0; bm < S::BM; ++bm) {
+      a[bm] = __uint_as_float((unsigned)w[bm][0]);
+      if (!MAX) b[bm] = __uint_as_float((unsigned)w[bm][NV - 1]);
+    }
+    return;
+  }
   float n_acc[S::BM], mu[S::BM], sq[S::BM];
 #pragma unroll
   for (int bm = 0; bm < S::BM; ++bm) {
@@ -689,6 +723,14 @@ __device__ __forceinline__ void cluster_exchange(const GemmRowsParams& p, int st
   for (int bm = 0; bm < S::BM; ++bm) {
     a[bm] = mu[bm];
     if (!MAX) b[bm] = sq[bm];
+  }
+  if (p.leader && wn == 0 && lane < 32) {   // the leader broadcasts the merged values
+#pragma unroll
+    for (int bm = 0; bm < S::BM; ++bm) {
+      unsigned long long* w = rec + ((size_t)kRecLead * kRecRows + wm * S::WTM + bm * 32 + lr) * 2;
+      __hip_atomic_store(w, rec_word(a[bm], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (!MAX) __hip_atomic_store(w + 1, rec_word(b[bm], tag), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    }
   }
 }
 

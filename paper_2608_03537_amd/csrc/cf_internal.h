@@ -59,6 +59,7 @@ struct GemmRowsParams {
                                  // SPLIT: [M][cn] float2
   float* ws_x;                   // SPLIT: [M][N] fp32 pre-norm x
   int spin_limit;                // polls before a peer wait gives up (sets ws_err)
+  int leader;                    // CLUSTER: leader-follower exchange (peer 0 merges and broadcasts)
 };
 
 // Each of the NW waves of the cn workgroups of a peer group adds
@@ -68,7 +69,7 @@ struct GemmRowsParams {
 constexpr unsigned long long kArriveUnit = 720720ull * 8ull;
 constexpr int kMaxSlots = 64;                        // concurrent peer groups
 // Exchange records: [stage 2][round parity 2][slot kMaxSlots][peer kRecPeers]
-// [row kRecRows] x 2 words.  A record's position depends only on (slot,
+// [row kRecRows] x 2 words (peer kRecLead: the leader's merged values).  A record's position depends only on (slot,
 // peer), never on the launch's peer count: round numbers grow per slot, so a
 // record left by an earlier call in a position only ever carries an older
 // round of the same slot (a position shared by different slots could hold
@@ -78,7 +79,9 @@ constexpr int kMaxSlots = 64;                        // concurrent peer groups
 // never finds its value overwritten.  (It cannot get two rounds ahead: round
 // r + 1 completes only with every peer's round r + 1 record, written after
 // that peer finished round r.)
-constexpr int kRecPeers = 16, kRecRows = 128;
+constexpr int kRecPeers = 17, kRecRows = 128;        // peers 0..15, then the leader's broadcast
+constexpr int kRecLead = 16;                         // record of the merged values (leader-follower)
+constexpr int kLeaderFollowerPeers = 8;              // peer counts from which the leader merges for all
 constexpr size_t kRecSetWords = (size_t)kMaxSlots * kRecPeers * kRecRows * 2;   // one parity of one stage
 constexpr size_t kRecStageWords = 2 * kRecSetWords;
 constexpr size_t kWsCounterBytes = 4096;             // err word, then the counters
