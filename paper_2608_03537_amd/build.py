@@ -21,7 +21,7 @@ ARCH = os.environ.get("CF_OFFLOAD_ARCH", "gfx950")
 
 SOURCES = ["cf_api.cpp", "cf_gemm_registry.cpp", "cf_gemm_inst_v2.hip", "cf_gemm_inst_v1.hip",
            "cf_gemm_inst_wr.hip", "cf_gemm_inst_split.hip", "cf_rows.hip", "cf_b2b.hip", "cf_ffn.hip",
-           "cf_noalloc.hip", "cf_mlp.hip"]
+           "cf_noalloc.hip", "cf_mlp.hip", "cf_gemm_inst_kn.hip"]
 
 # -packed-fp32-ops off: hipcc then never forms v_pk_{add,mul,fma}_f32 from
 # scalar float code (the host pass warns that it does not know the feature).
@@ -42,6 +42,7 @@ def _hipcc():
 # AGPRs would cost a copy each way for every such step.
 FILE_FLAGS = {f: ["-mllvm", "-amdgpu-mfma-vgpr-form"]
               for f in ("cf_gemm_inst_v2.hip", "cf_gemm_inst_v1.hip", "cf_gemm_inst_wr.hip", "cf_gemm_inst_split.hip",
+                        "cf_gemm_inst_kn.hip",
                         "cf_b2b.hip", "cf_mlp.hip")}
 
 

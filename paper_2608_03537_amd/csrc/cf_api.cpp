@@ -112,7 +112,7 @@ int pick_tile(int64_t M, int64_t N, int64_t K, int in_f32, int loop, int epi, bo
     const int idx = find_gemm_kernel(in_f32, 128, tn, loop, epi);
     if (idx < 0) continue;
     // the direct-to-LDS ring is filled with stages-1 stages before the first MFMA
-    if (loop == 1 && K / (in_f32 ? 32 : 64) < gemm_kernel(idx).stages - 1) continue;
+    if (loop >= 1 && K / (in_f32 ? 32 : 64) < gemm_kernel(idx).stages - 1) continue;
     const int64_t cn = (N + tn - 1) / tn;
     if (divides && (N % tn != 0 || cn > max_cn)) continue;
     const int64_t wgs = ((M + 127) / 128) * cn;
@@ -135,7 +135,9 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
     if (path == PATH_AUTO) path = N <= kWholeRowMaxN ? PATH_WHOLE_ROW : PATH_SPLIT;
   }
   const int tk = in_f32 ? 32 : 64;                     // k per 128-byte stage
-  const int loop = (w_nk && K % tk == 0) ? 1 : 0;
+  // Direct-to-LDS ring when K fills whole stages: W stored N x K (loop 1), or
+  // bf16 W stored K x N with N a multiple of 8 (loop 2, transposing reads).
+  const int loop = K % tk != 0 ? 0 : w_nk ? 1 : (!in_f32 && N % 8 == 0) ? 2 : 0;
   if (!need_rows) {
     pl.kidx = pick_tile(M, N, K, in_f32, loop, epi, false, 0);
     if (pl.kidx < 0) pl.kidx = pick_tile(M, N, K, in_f32, 0, epi, false, 0);
@@ -166,7 +168,7 @@ cf_status plan_rows(int64_t M, int64_t N, int64_t K, int in_f32, bool w_nk, int 
       for (int tn : {128, 256, 384, 512, 768})
         if (tn >= N) {
           // the direct-to-LDS ring where compiled and K fills its prologue
-          const int v2 = loop == 1 ? find_gemm_kernel(in_f32, 32, tn, 1, 1) : -1;
+          const int v2 = loop >= 1 ? find_gemm_kernel(in_f32, 32, tn, loop, 1) : -1;
           if (v2 >= 0 && K / tk >= gemm_kernel(v2).stages - 1) pl.kidx = v2;
           else pl.kidx = find_gemm_kernel(in_f32, 32, tn, 0, 1);
           break;

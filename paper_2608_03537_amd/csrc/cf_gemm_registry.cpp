@@ -12,7 +12,7 @@ static std::vector<GemmKernel>& table() {
   static std::vector<GemmKernel> t;
   static std::once_flag once;
   std::call_once(once, [] {
-    for (auto get : {gemm_kernels_v2, gemm_kernels_v1, gemm_kernels_wr, gemm_kernels_split}) {
+    for (auto get : {gemm_kernels_v2, gemm_kernels_v1, gemm_kernels_wr, gemm_kernels_split, gemm_kernels_kn}) {
       int n = 0;
       const GemmKernel* k = get(&n);
       t.insert(t.end(), k, k + n);

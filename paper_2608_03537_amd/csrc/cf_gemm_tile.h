@@ -37,9 +37,9 @@ namespace cf {
 template <typename TIn, int BM_, int BN_, int WM_, int WN_, int TKB_, int STAGES_ = 0>
 struct TileShape {
   using T = TIn;
-  // STAGES > 0 selects the direct-to-LDS pipeline (mainloop_v2) for weights
-  // stored N x K with K a multiple of the 128-byte stage; the register-staged
-  // loop (mainloop) remains for K x N weights and ragged K.
+  // STAGES > 0 selects the direct-to-LDS pipeline (mainloop_v2) for K a
+  // multiple of the 128-byte stage (bf16 weights in either layout, fp32 ones
+  // stored N x K); the register-staged loop (mainloop) serves the rest.
   static constexpr int STAGES = STAGES_;
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr int NW = WM * WN, NT = 64 * NW;
@@ -292,8 +292,18 @@ __device__ __forceinline__ void wait_vmcnt() {
 //
 // Rows past M (or N) are clamped to the last valid row: they only feed output
 // rows/columns that the epilogue masks.
+//
+// KN (bf16, W stored K x N, N a multiple of 8, TN a multiple of 128): the W
+// part of a stage holds the 64 k-rows of the tile as they lie in memory, TN
+// columns each, the 64-byte blocks of row k XOR-swizzled by (k & 3).  The A
+// fragment (8 consecutive k of one column) comes from two transposing reads
+// (ds_read_b64_tr_b16): in each group of 16 lanes, lane r points at 4
+// consecutive columns of k-row r / 4, and lane i gets the 4 k-values of
+// column i.  The 32 lanes served together read 4 k-rows x 64 bytes, which the
+// swizzle places on 4 distinct 64-byte bank groups.  Columns past N are
+// clamped to the last 8-column chunk.
 // ---------------------------------------------------------------------------
-template <class S, bool STG, bool PERM = false>
+template <class S, bool STG, bool PERM = false, bool KN = false>
 __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
                                             const typename S::T* __restrict__ X,
                                             const typename S::T* __restrict__ W,
@@ -307,22 +317,35 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
   // Ring slot of stage st: rotated so that the last stage lands in slot NS-1
   // and the slots freed during the last iterations are 0, 1, ...
   const int rot = (NS - KT % NS) % NS;
+  static_assert(!KN || (sizeof(T) == 2 && S::TN % 128 == 0 && !PERM), "K x N ring: bf16, TN % 128 == 0");
+  constexpr int KN_RW = S::TN * 2;                 // bytes of one k-row of the W part (KN)
   const char* src[PW];
 #pragma unroll
   for (int j = 0; j < PW; ++j) {
     const int row = (wave + j * S::NW) * 8 + (lane >> 3);
     const int c = (lane & 7) ^ ((row >> 1) & 7);
     if (row < S::TN) {
-      const int n = min(n0 + (PERM ? perm23(row) : row), p.N - 1);
-      src[j] = reinterpret_cast<const char*>(W + (int64_t)n * p.ldw) + c * 16;
+      if constexpr (KN) {
+        const int o = (wave + j * S::NW) * 1024 + lane * 16;   // byte within the W part
+        const int k = o / KN_RW, gc = ((o % KN_RW) >> 4) ^ ((k & 3) << 2);
+        const int n = min(n0 + gc * 8, p.N - 8);
+        src[j] = reinterpret_cast<const char*>(W + (int64_t)k * p.ldw + n);
+      } else {
+        const int n = min(n0 + (PERM ? perm23(row) : row), p.N - 1);
+        src[j] = reinterpret_cast<const char*>(W + (int64_t)n * p.ldw) + c * 16;
+      }
     } else {
       const int m = min(m0 + row - S::TN, p.M - 1);
       src[j] = reinterpret_cast<const char*>(X + (int64_t)m * p.ldx) + c * 16;
     }
   }
+  // Bytes between consecutive stages of a load: 128 along k, or (KN W part)
+  // 64 k-rows of W.
+  const int64_t w_step = KN ? (int64_t)S::V2_TK * p.ldw * (int64_t)sizeof(T) : S::V2_ROWB;
   auto slot = [&](int st) { return smem + ((st + rot) % NS) * S::V2_STAGE; };
   auto dma = [&](int j, int st) {
-    dma16(src[j] + (int64_t)st * S::V2_ROWB, slot(st) + (wave + j * S::NW) * 1024);
+    const bool wpart = (wave + j * S::NW) * 8 < S::TN;
+    dma16(src[j] + (int64_t)st * (wpart ? w_step : (int64_t)S::V2_ROWB), slot(st) + (wave + j * S::NW) * 1024);
   };
   // Epilogue staging loads: residual rows (part 0: rows [0, RA) into slot 0,
   // part 1: rows [RA, TM) into slot 1) with the 16-byte chunk of column group
@@ -361,9 +384,22 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
   // Fragment `idx` of MFMA step ks of stage st: idx < BN -> W^T block idx, else X block idx-BN.
   auto frag1 = [&](int st, int ks, int idx) {
     const int off = ((2 * ks + lg) ^ sw) << 4;
-    if (idx < S::BN)
-      fa[ks][idx] = lds_read16(slot(st) + (wn * S::WTN + idx * 32 + lr) * S::V2_ROWB + off);
-    else
+    if (idx < S::BN) {
+      if constexpr (KN) {
+        typedef short v4i16 __attribute__((ext_vector_type(4)));
+        const int r = lane & 15;
+        const int k = 16 * ks + 8 * lg + (r >> 2);
+        const int nb = (wn * S::WTN + idx * 32 + (lane & 16) + 4 * (r & 3)) * 2;
+        const char* a = slot(st) + k * KN_RW + (nb ^ ((r >> 2) << 6));
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16*)(a));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4i16*)(a + 4 * KN_RW));
+        const u32x2_t l2 = __builtin_bit_cast(u32x2_t, lo), h2 = __builtin_bit_cast(u32x2_t, hi);
+        fa[ks][idx] = u32x4_t{l2[0], l2[1], h2[0], h2[1]};
+      } else {
+        fa[ks][idx] = lds_read16(slot(st) + (wn * S::WTN + idx * 32 + lr) * S::V2_ROWB + off);
+      }
+    } else
       fb[ks][idx - S::BN] = lds_read16(slot(st) + (S::TN + wm * S::WTM + (idx - S::BN) * 32 + lr) * S::V2_ROWB + off);
   };
   constexpr int NFR = S::BN + S::BM;               // fragments per step
@@ -1317,7 +1353,8 @@ __device__ __forceinline__ void epilogue_plain(f32x16_t (&x)[S::BM][S::BN], cons
 }
 
 // LOOP: 0 = register-staged main loop (any layout, ragged K),
-//       1 = direct-to-LDS pipeline (W stored N x K, K a multiple of the stage).
+//       1 = direct-to-LDS pipeline (W stored N x K, K a multiple of the stage),
+//       2 = the same pipeline for bf16 W stored K x N (N a multiple of 8).
 // EPI:  0 = plain epilogue (alpha, bias, store), 1 = row-subgraph epilogue
 //       (whole rows or row clusters), 2 = the split-N GEMM pass.
 template <class S, int LOOP, int EPI>
@@ -1325,7 +1362,7 @@ __global__ __launch_bounds__(S::NT, 1) __attribute__((amdgpu_waves_per_eu(1, 1))
 void gemm_rows_kernel(GemmRowsParams p) {
   using T = typename S::T;
   constexpr int SMEM = LOOP ? S::SMEM_V2 : S::SMEM_V1;
-  constexpr bool STG = LOOP == 1 && EPI >= 1 && S::STG;   // epilogue operands staged by the main loop
+  constexpr bool STG = LOOP >= 1 && EPI >= 1 && S::STG;   // epilogue operands staged by the main loop
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   float* red = reinterpret_cast<float*>(smem + SMEM - S::TAIL_BYTES);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1355,7 +1392,8 @@ void gemm_rows_kernel(GemmRowsParams p) {
     if constexpr (EPI >= 1 && !STG) epi_prefetch<S>(pf, p, m0, n0, bz, lane, wm, wn);
     // The bias enters the accumulators unless alpha scales the product.
     const bool fold_bias = p.epi.bias != nullptr && p.epi.alpha == 1.0f;
-    if constexpr (LOOP == 1) mainloop_v2<S, STG>(acc, X, W, p, m0, n0, bz, smem, lane, wave, wm, wn, fold_bias);
+    if constexpr (LOOP >= 1)
+      mainloop_v2<S, STG, false, LOOP == 2>(acc, X, W, p, m0, n0, bz, smem, lane, wave, wm, wn, fold_bias);
     else mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn, fold_bias);
     unsigned tag = 0;
     if (cluster) {

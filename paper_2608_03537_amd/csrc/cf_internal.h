@@ -115,6 +115,7 @@ const GemmKernel* gemm_kernels_v2(int* n);     // direct-to-LDS pipeline
 const GemmKernel* gemm_kernels_v1(int* n);     // register-staged, any layout
 const GemmKernel* gemm_kernels_wr(int* n);     // whole-row tiles (register-staged)
 const GemmKernel* gemm_kernels_split(int* n);  // split-N GEMM pass (both main loops)
+const GemmKernel* gemm_kernels_kn(int* n);     // direct-to-LDS pipeline, bf16 W stored K x N
 int find_gemm_kernel(int in_f32, int tm, int tn, int loop, int epi);   // -1 if none
 const GemmKernel& gemm_kernel(int idx);
 int resident_wgs(int idx);   // co-resident workgroups of this kernel on the device

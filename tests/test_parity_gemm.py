@@ -38,6 +38,36 @@ def test_gemm(M, K, N, layout, dtype):
     assert rel_rms(got, ref) < 1e-6
 
 
+# bf16 B stored K x N with K a multiple of 64 (>= 192) takes the direct-to-LDS
+# ring with transposing LDS reads: ragged M, N not a multiple of the tile
+# width (clamped columns), batched operands.
+@pytest.mark.parametrize("M,K,N,nb", [(300, 256, 224, 1), (129, 192, 288, 1), (64, 512, 1024, 2),
+                                      (257, 256, 96, 1), (33, 2048, 128, 3)])
+def test_gemm_kn_ring(M, K, N, nb):
+    A = np.stack([_rand((M, K), 11 + i, "bf16") for i in range(nb)])
+    Bm = np.stack([_rand((K, N), 21 + i, "bf16", 1 / np.sqrt(K)) for i in range(nb)])
+    Cg = cf.gemm(dev(A), dev(Bm), b_layout=cf.CF_LAYOUT_KN, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = np.stack([O.matmul(A[i], Bm[i]) for i in range(nb)])
+    got = host(Cg)
+    assert got.shape == ref.shape
+    assert rel_rms(got, ref) < 1e-6
+    assert np.max(np.abs(got - ref)) < 1e-4 * np.max(np.abs(ref))
+
+
+def test_gemm_kn_attention_pv_full_length():
+    """P.V of two heads at the attention workload's length (2048 keys, d = 128):
+    the unfused comparator's second product, B stored K x N."""
+    nb, L, d = 2, 2048, 128
+    rng = np.random.default_rng(31)
+    Pb = I.round_to_bf16((rng.random((nb, L, L)) / L * 2).astype(np.float32))
+    V = np.stack([_rand((L, d), 32 + i, "bf16") for i in range(nb)])
+    O2 = cf.gemm(dev(Pb), dev(V), b_layout=cf.CF_LAYOUT_KN, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = np.stack([O.matmul(Pb[i], V[i]) for i in range(nb)])
+    assert rel_rms(host(O2), ref) < 1e-6
+
+
 def test_gemm_batched_attention_shapes():
     B, L, d = 3, 160, 64
     Q, K, V = (_rand((B, L, d), s, "bf16") for s in (4, 5, 6))
