@@ -22,12 +22,15 @@
 // step s of the second product O^T = W2^T S^T, whose A operand is then one
 // contiguous 16-byte piece of a W2^T row.
 //
-// LDS operands are stored in MFMA fragment order: wave-wide direct loads
-// (global_load_lds) place lane l's 16 bytes of fragment f at f * 1024 + 16 l,
-// so every fragment read is one conflict-free 1 KB read at an immediate
-// offset.  Layout (bytes):
-//   ring 1: 2 stages x {W1^T chunk 2t, W1^T chunk 2t+1}, KS1 fragments each
-//   ring 2: 2 stages x {W2^T chunk 2t, W2^T chunk 2t+1}, 2 B2 fragments each
+// Weight loads.  Every wave-wide direct load (global_load_lds) brings 8 whole
+// 128-byte lines: 8 rows x 128 bytes of one operand, which lands as 8
+// consecutive 128-byte LDS rows whose 16-byte chunks are XOR-swizzled by
+// (row >> 1) & 7.  A fragment read (16 consecutive rows, one chunk column per
+// 16 lanes) is then conflict-free.  Loads that gather 32-byte pieces of 32
+// rows instead touch four times as many lines per byte, and the weights'
+// L2-to-LDS stream ran at about a quarter of this rate.  Layout (bytes):
+//   ring 1: 2 stages x W1^T rows of chunks 2t, 2t+1: [k block D/64][row 64][128 B]
+//   ring 2: 2 stages x W2^T columns of chunks 2t, 2t+1: [row D][128 B]
 //   S exchange: 2 stages x [row group 4][half 2][lane 64][32 B]
 #include "cf_gemm_tile.h"
 #include "comfuse.h"
@@ -72,26 +75,38 @@ __device__ __forceinline__ u32x4_t ffn_pack_step(const f32x16_t& v, int s) {
 }
 
 // GELU(x) = x/2 (1 + erf(x / sqrt 2)) with the erf of Abramowitz and Stegun
-// 7.1.26 (as erf_as), split into 8 stages of about two operations so that
-// four independent elements advance one stage between two MFMAs.  The input
-// x stays in place until the last stage (it carries the sign and x/2).
+// 7.1.26 (as erf_as), in the form
+//   GELU(x) = max(x, 0) - |x| y(t) exp(-x^2 / 2) / 2,
+//   t = 1 / (1 + p |x| / sqrt 2),  y(t) = a1 t + ... + a5 t^5,
+// which follows from erf(z) = 1 - y(t) exp(-z^2) for z >= 0 and the odd
+// extension (for x >= 0 the two halves x/2 + x/2 erf give x - x y e / 2; for
+// x < 0 they give x y e / 2).  Eleven vector operations and two
+// transcendentals per element, split into 8 stages so that four independent
+// elements advance one stage between two MFMAs.  The input x stays in place
+// until the last stage.
 struct GeluPipe {
   float t[4], y[4], e[4];
 };
 __device__ __forceinline__ void gelu_stage(GeluPipe& g, const float* x, float* out, int st) {
-  constexpr float kRs2 = 0.70710678118654752f;            // 1 / sqrt 2
-  constexpr float kHalfLog2e = 0.72134752044448170f;      // log2(e) / 2: exp(-x^2 / 2) = exp2(-x^2 kHalfLog2e)
+  constexpr float kP = 0.3275911f * 0.70710678118654752f;   // p / sqrt 2
+  constexpr float kNegHalfLog2e = -0.72134752044448170f;    // -log2(e) / 2
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     switch (st) {
-      case 0: g.t[j] = fmaf(0.3275911f * kRs2, fabsf(x[j]), 1.0f); break;
-      case 1: g.t[j] = __builtin_amdgcn_rcpf(g.t[j]); g.e[j] = -(x[j] * x[j]) * kHalfLog2e; break;
-      case 2: g.y[j] = fmaf(1.061405429f, g.t[j], -1.453152027f); g.e[j] = __builtin_amdgcn_exp2f(g.e[j]); break;
-      case 3: g.y[j] = fmaf(g.y[j], g.t[j], 1.421413741f); break;
-      case 4: g.y[j] = fmaf(g.y[j], g.t[j], -0.284496736f); break;
-      case 5: g.y[j] = fmaf(g.y[j], g.t[j], 0.254829592f) * g.t[j]; break;
-      case 6: g.y[j] = copysignf(fmaf(-g.y[j], g.e[j], 1.0f), x[j]); break;
-      default: { const float hx = 0.5f * x[j]; out[j] = fmaf(hx, g.y[j], hx); } break;
+      case 0: g.t[j] = fmaf(kP, fabsf(x[j]), 1.0f); break;
+      case 1: g.t[j] = __builtin_amdgcn_rcpf(g.t[j]); g.e[j] = x[j] * kNegHalfLog2e; break;
+      // 2^(-x^2 log2(e) / 2 - 1) = exp(-x^2 / 2) / 2
+      case 2: g.e[j] = __builtin_amdgcn_exp2f(fmaf(x[j], g.e[j], -1.0f)); break;
+      case 3: g.y[j] = fmaf(1.061405429f, g.t[j], -1.453152027f); break;
+      case 4: g.y[j] = fmaf(g.y[j], g.t[j], 1.421413741f); break;
+      case 5: g.y[j] = fmaf(g.y[j], g.t[j], -0.284496736f); break;
+      case 6: g.y[j] = fmaf(g.y[j], g.t[j], 0.254829592f); g.e[j] = fabsf(x[j]) * g.e[j]; break;
+      default: {
+        // max(x, 0) as one v_max_f32 (fmaxf adds a canonicalising max in front)
+        float r;
+        asm("v_max_f32_e32 %0, 0, %1" : "=v"(r) : "v"(x[j]));
+        out[j] = fmaf(-g.e[j], g.y[j] * g.t[j], r);
+      } break;
     }
   }
 }
@@ -113,16 +128,24 @@ void b2b_ffn_kernel(B2BParams p) {
   const bf16_t* W2 = p.W2 + (int64_t)bz * p.sw2;
   const int nb0 = h * F::B2H;                   // first output block of this half
 
-  // Wave-wide loads.  Waves 0-3 load the two W1^T chunks of a round: load
-  // q = DMA_W wave + j in [0, 2 KS1) is fragment q % KS1 of chunk 2 r + q / KS1
-  // (32 hidden rows in ffn_hidden_row order, k step 16 (q % KS1)).  Waves 4-7
-  // load the two W2^T chunks: load q in [0, 4 B2) is fragment (b, s) of chunk
-  // 2 r + e (rows 32 b .. +31, hidden 32 (2 r + e) + 16 s ..), q = 2 B2 e + 2 b + s.
-  // Addresses are a wave-uniform base plus a 32-bit lane offset.
+  // Wave-wide loads of one round.  Waves 0-3 load the W1^T rows of chunks 2r
+  // and 2r+1: load q in [0, D/8) covers k block q / 8 (64 k) of LDS rows
+  // 8 (q % 8) .. +7, and LDS row i holds hidden unit
+  // 32 (2r + i / 32) + ffn_hidden_row(i % 32).  Waves 4-7 load the W2^T
+  // columns of both chunks (hidden 64r .. 64r+63, 128 bytes of each of the D
+  // rows): load q covers rows 8q .. 8q+7.
+  // A load's address is a wave-uniform part (q, round) plus one of two lane
+  // offsets: the lane's row within the 8-row group (W1: its bits of the hidden
+  // unit) and its swizzled chunk, which depends on q only through q % 2
+  // (bit 2 of the swizzle term).
   const bool w1part = wave < 4;
+  const int lrow = lane >> 3, lch = lane & 7;
   const char* gbase = w1part ? reinterpret_cast<const char*>(W1) : reinterpret_cast<const char*>(W2);
-  const uint32_t loff = w1part ? (uint32_t)(ffn_hidden_row(lr) * p.ldw1 * 2 + 16 * lg)
-                               : (uint32_t)(lr * p.ldw2 * 2 + 16 * lg);
+  const int64_t pitch = 2 * (w1part ? p.ldw1 : p.ldw2);
+  const int lrow_h = w1part ? ((lrow & 3) | ((lrow & 4) << 1)) : lrow;
+  uint32_t loff[2];
+#pragma unroll
+  for (int v = 0; v < 2; ++v) loff[v] = (uint32_t)(lrow_h * pitch + 16 * (lch ^ (lrow >> 1) ^ (v << 2)));
   auto issue = [&](int r1, bool do1, int r2, bool do2) {
     if (w1part ? !do1 : !do2) return;
     const int r = w1part ? r1 : r2;
@@ -132,17 +155,24 @@ void b2b_ffn_kernel(B2BParams p) {
       int64_t goff;
       int soff;
       if (w1part) {
-        const int e = q / F::KS1, f = q % F::KS1;
-        goff = (int64_t)((2 * r + e) * F::HC) * p.ldw1 * 2 + 32 * f;
+        const int i8 = q & 7;   // 8-row group of LDS rows 8 i8 .. +7
+        const int hid = 64 * r + 32 * (i8 >> 2) + 16 * ((i8 >> 1) & 1) + 4 * (i8 & 1);
+        goff = hid * pitch + 128 * (q >> 3);
         soff = (r & 1) * F::W1S + q * 1024;
       } else {
-        const int e = q / (2 * F::B2), f = q % (2 * F::B2), b = f >> 1, sb = f & 1;
-        goff = (int64_t)(32 * b) * p.ldw2 * 2 + ((2 * r + e) * F::HC + 16 * sb) * 2;
+        goff = 8 * q * pitch + 128 * r;
         soff = F::OFF_W2 + (r & 1) * F::W2S + q * 1024;
       }
-      dma16(gbase + goff + (uint64_t)loff, smem + soff);
+      dma16(gbase + goff + loff[q & 1], smem + soff);
     }
   };
+  // Lane offsets of the fragment reads.  First product, step ks: LDS row
+  // 32 h + lr of k block ks / 4, chunk 2 (ks % 4) + lg.  Second product,
+  // output block b, step s of chunk 2t + e: row 32 (nb0 + b) + lr, chunk
+  // 4 e + 2 s + lg.  The swizzle term (row >> 1) & 7 is (lr >> 1) & 7 for both.
+  const int sw = (lr >> 1) & 7;
+  auto o1 = [&](int u) { return (32 * h + lr) * 128 + ((((u << 1) | lg) ^ sw) << 4); };
+  auto o2 = [&](int e, int s2) { return lr * 128 + (((4 * e + 2 * s2 + lg) ^ sw) << 4); };
 
   // X^T fragments of this pair's 32 rows: xf[ks] = X[m][16 ks + 8 lg .. +8].
   const bf16_t* xrow = X + (int64_t)min(m, p.M - 1) * p.ldx + 8 * lg;
@@ -168,23 +198,26 @@ void b2b_ffn_kernel(B2BParams p) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) Oa[b][i] = 0.0f;
   }
-  // b1 of hidden chunk c in the accumulator order: element 4 g + q holds hidden
-  // unit 16 (g / 2) + 8 lg + 4 (g % 2) + q of the chunk.
-  auto load_b1 = [&](int c, f32x4_t (&v)[4]) {
-    if (p.b1) {
-      const float* b1l = p.b1 + c * F::HC + 8 * lg;
+  // b1 enters the first product as one more MFMA step: A holds b1 of the
+  // lane's hidden row split into two bf16 (hi = bf16(b1), lo = bf16(b1 - hi))
+  // at k = 0, 1 and B holds ones there, so P^T starts at hi + lo (within about
+  // 2^-16 |b1| of b1) and needs no zeroing or vector add.  bq[r] holds the
+  // pair for the chunk of round r (lanes of group lg = 1 hold 0), shifted one
+  // place per round.
+  uint32_t bq[F::NR];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) v[g] = *reinterpret_cast<const f32x4_t*>(b1l + 16 * (g >> 1) + 4 * (g & 1));
-    } else {
+  for (int r = 0; r < F::NR; ++r) {
+    const float v = p.b1 ? p.b1[32 * (2 * r + h) + ffn_hidden_row(lr)] : 0.0f;
+    const float hi = __uint_as_float(pack_bf16x2(v, 0.0f) << 16);
+    bq[r] = lg == 0 ? pack_bf16x2(hi, v - hi) : 0u;
+  }
+  const u32x4_t ones = {lg == 0 ? 0x3F803F80u : 0u, 0u, 0u, 0u};
+  auto first_step = [&](f32x16_t& P) {
+    const u32x4_t a = {bq[0], 0u, 0u, 0u};
+    P = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, ones),
+                                                f32x16_t{}, 0, 0, 0);
 #pragma unroll
-      for (int g = 0; g < 4; ++g) v[g] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-    }
-  };
-  auto add_b1 = [&](f32x16_t& P, const f32x4_t (&v)[4]) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) P[4 * g + q] += v[g][q];
+    for (int r = 0; r + 1 < F::NR; ++r) bq[r] = bq[r + 1];
   };
 
   issue(0, true, 0, false);
@@ -223,9 +256,8 @@ void b2b_ffn_kernel(B2BParams p) {
     constexpr int NS = GEL ? (NM > F::GSLOTS ? NM : F::GSLOTS) : NM;
     constexpr int FG = F::FG;
     static_assert(!GEL || NS == F::GSLOTS, "one GELU stage per slot");
-    const char* a1 = smem + ((t + 1) & 1) * F::W1S + h * F::W1C + lane * 16;
-    const char* a2o = smem + F::OFF_W2 + ((t - 1) & 1) * F::W2S + h * F::W2C + lane * 16;   // own chunk
-    const char* a2p = smem + F::OFF_W2 + ((t - 1) & 1) * F::W2S + (1 - h) * F::W2C + lane * 16;   // partner's
+    const char* a1 = smem + ((t + 1) & 1) * F::W1S;
+    const char* a2 = smem + F::OFF_W2 + ((t - 1) & 1) * F::W2S + nb0 * 32 * 128;
     auto is1 = [&](int i) { return ONE && (TWO ? (i & 1) == 0 : true); };
     auto idx = [&](int i) { return ONE && TWO ? i >> 1 : i; };
     // second-product op j: block nb0 + j % B2H, step j / (2 B2H), with this
@@ -233,14 +265,11 @@ void b2b_ffn_kernel(B2BParams p) {
     // partner's chunk (S in Sx)
     auto afrag = [&](int i) -> u32x4_t {
       const int j = idx(i);
-      if (is1(i)) return lds_read16(a1 + j * 1024);
+      if (is1(i)) return lds_read16(a1 + o1(j & 3) + (j >> 2) * 64 * 128);
       const int b = j % F::B2H, own = ((j / F::B2H) & 1) == 0, s = j / (2 * F::B2H);
-      return lds_read16((own ? a2o : a2p) + (2 * (nb0 + b) + s) * 1024);
+      return lds_read16(a2 + o2(own ? h : 1 - h, s) + b * 32 * 128);
     };
-    if constexpr (ONE) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) Pn[i] = 0.0f;
-    }
+    if constexpr (ONE) first_step(Pn);
     u32x4_t fr[2][FG];
     GeluPipe gp;
 #pragma unroll
@@ -305,12 +334,7 @@ void b2b_ffn_kernel(B2BParams p) {
     char* dst = xch_own + (t & 1) * F::XCH;
     lds_write16(dst, Sp[0]);
     lds_write16(dst + 16, Sp[1]);
-    if (t + 1 < F::NR) {
-      f32x4_t b1v[4];
-      load_b1(2 * (t + 1) + h, b1v);
-      add_b1(Pn, b1v);
-      Pc = Pn;
-    }
+    if (t + 1 < F::NR) Pc = Pn;
   };
 
   // Prologue: the first product of round 0, then round 0 (no second product yet).
@@ -318,11 +342,6 @@ void b2b_ffn_kernel(B2BParams p) {
   __syncthreads();
   if (F::NR > 1) issue(1, true, 0, false);
   iter(-1, T_{}, F_{}, F_{});
-  {
-    f32x4_t b1v[4];
-    load_b1(h, b1v);
-    add_b1(Pn, b1v);
-  }
   Pc = Pn;
   top(0);
   if constexpr (F::NR > 1) iter(0, T_{}, F_{}, T_{});
