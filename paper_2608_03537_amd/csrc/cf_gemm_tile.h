@@ -1372,11 +1372,25 @@ void gemm_rows_kernel(GemmRowsParams p) {
   const T* W = reinterpret_cast<const T*>(p.W) + (int64_t)bz * p.sw;
   // blockIdx.x -> (XCD, slot, peer).  Consecutive block ids go round-robin
   // over the 8 XCDs, so the cn peers of a row block share one XCD and its L2.
+  // Row block rb runs on XCD rb % 8.  Without peer groups (one tile per
+  // workgroup) an XCD's tiles go in the grouped order of kTileGroupRows.
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
-  const int c = local % p.cn, q = local / p.cn;
+  const bool grouped = p.mode != ROWS_CLUSTER;
+  const int q = local / p.cn;
   for (int it = 0;; ++it) {
-    const int rb = (it * p.slots + q) * 8 + xcd;
-    if (rb >= p.num_rb) break;
+    int rb, c;
+    if (grouped) {
+      const int R = (p.num_rb - xcd + 7) / 8;            // row blocks of this XCD
+      if (it > 0 || local >= R * p.cn) break;
+      const int span = kTileGroupRows * p.cn;
+      const int g0 = local / span * kTileGroupRows, gsz = min(R - g0, kTileGroupRows), w = local % span;
+      rb = (g0 + w % gsz) * 8 + xcd;
+      c = w / gsz;
+    } else {
+      rb = (it * p.slots + q) * 8 + xcd;
+      if (rb >= p.num_rb) break;
+      c = local % p.cn;
+    }
     int m0 = rb * S::TM, n0 = c * S::TN;
     // Opaque copies of the tile origin and lane ids for this iteration: the
     // epilogue's addresses and column masks would otherwise be hoisted out of

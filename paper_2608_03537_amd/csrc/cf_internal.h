@@ -88,6 +88,12 @@ constexpr size_t kWsCounterBytes = 4096;             // err word, then the count
 constexpr size_t kWsHeaderBytes = kWsCounterBytes + 2 * kRecStageWords * 8;
 static_assert(256 + 8 * kMaxSlots <= kWsCounterBytes, "counter area");
 constexpr int kSpinLimitDefault = 1 << 20;           // ~1 s of device-scope polls
+// Tile order of launches without peer groups: each XCD's tiles run in groups
+// of kTileGroupRows row blocks by every column tile, column by column, so the
+// about 32 tiles an XCD runs at once cover 8 row blocks x 4 column tiles and
+// share their operands in its L2 (2 row blocks x 16 column tiles fetch about
+// twice as many bytes per k-step at N = 4096).
+constexpr int kTileGroupRows = 8;
 
 // Wave-per-row kernel: the finish pass of the split path (merge the partial
 // (mean, M2) of each row's tiles, then stages 2..4 on the fp32 x the GEMM
