@@ -20,8 +20,16 @@ The compilation stack of Sec. V, for this library's compiled vocabulary:
             the kernels are compiled ahead of time, so the spec is matched,
             from its terminal node inwards, against the node grammar of
             cf_gemm_subgraph ([SCALE] [BIAS] [RESIDUAL] [LAYERNORM | RMSNORM]
-            [GELU | GELU_TANH | RELU | SOFTCAP] [SOFTMAX] STORE).  A spec that
-            matches nothing is reported as unsupported.
+            [GELU | GELU_TANH | RELU | SOFTCAP] [SOFTMAX] STORE
+            [ROWAMAX_QUANT]).  A spec that matches nothing is reported as
+            unsupported.
+
+A function returns the stored tensor z, or a tuple holding z and the row
+quantisation tail of the LN -> GELU -> amax chain: the scale
+s = amax(|z|, -1, keepdim) / qmax and/or the codes (z / s).to(float8_e4m3fn)
+(ROWAMAX_QUANT, Sec. III-B).  The amax is taken over the fp32 z before its
+rounding to the output dtype, and a row whose amax is 0 gets s = 0 and codes
+0, where eager PyTorch would divide by zero.
 
 `compile_epilogue(fn)` returns a callable that runs the fused kernel.  A
 function outside the domain raises `UnsupportedEpilogue` with the reason; only
@@ -79,7 +87,8 @@ class FusionSpec:
                "passthrough": index of the reduced tensor,
                "nodes": indices of the nodes that depend on the statistic}.
     w_layout  layout of the weight operand (cf.CF_LAYOUT_NK or _KN);
-    x_arg, w_arg: argument positions of the product's operands.
+    x_arg, w_arg: argument positions of the product's operands;
+    outputs   the function's results in order (one entry: the terminal).
     """
     nodes: list
     edges: list
@@ -89,6 +98,7 @@ class FusionSpec:
     w_layout: int
     x_arg: int
     w_arg: int
+    outputs: list = field(default_factory=list)
 
 
 # ---------------------------------------------------------------------------
@@ -190,7 +200,9 @@ def phi(gm) -> FusionSpec:
               aten.mul_.Tensor: "mul", aten.div.Tensor: "div", aten.div.Scalar: "div"}
     unary = {aten.tanh.default: "tanh", aten.exp.default: "exp", aten.relu.default: "relu",
              aten.rsqrt.default: "rsqrt", aten.sqrt.default: "sqrt", aten.neg.default: "neg",
-             aten.gelu.default: "gelu", aten.reciprocal.default: "reciprocal"}
+             aten.gelu.default: "gelu", aten.reciprocal.default: "reciprocal", aten.abs.default: "abs"}
+    import torch
+    fp8 = getattr(torch, "float8_e4m3fn", None)
     output = None
     for n in graph.nodes:
         if n.op == "output":
@@ -243,11 +255,23 @@ def phi(gm) -> FusionSpec:
             # and rounds once at the store
             if not (hasattr(n.args[0], "op") and n.args[0] in ids):
                 raise UnsupportedEpilogue("only derived values may be converted")
-            ids[n] = ids[n.args[0]]
+            if fp8 is not None and n.kwargs.get("dtype") == fp8:
+                ids[n] = new("compute", op="e4m3", inputs=(ids[n.args[0]],))   # E4M3 codes
+            else:
+                ids[n] = ids[n.args[0]]
         else:
             raise UnsupportedEpilogue(f"{t} is outside the pattern set")
-    if output is None or not hasattr(output, "op") or output not in ids:
-        raise UnsupportedEpilogue("the function must return one tensor derived from the product")
+    outs = list(output) if isinstance(output, (tuple, list)) else [output]
+    if not outs or any(not hasattr(o, "op") or o not in ids for o in outs):
+        raise UnsupportedEpilogue("the function must return tensors derived from the product")
+    # the stored value: the one result that is neither codes nor a row statistic
+    main = [o for o in outs if nodes[ids[o]].op != "e4m3" and
+            not (o.meta.get("val") is not None and o.meta["val"].dim() == 2 and o.meta["val"].shape[-1] == 1
+                 and meta_rank(o) == 2 and len(outs) > 1)]
+    if len(main) != 1:
+        raise UnsupportedEpilogue("the function must return one stored tensor (plus, optionally, its row "
+                                  "quantisation scale and codes)")
+    output = main[0]
     edges = [(i, sn.idx) for sn in nodes for i in sn.inputs]
     users = {}
     for p_, c_ in edges:
@@ -266,7 +290,7 @@ def phi(gm) -> FusionSpec:
                     todo.append(u)
         nested.append({"reduce": sn.idx, "stat": stat, "passthrough": sn.inputs[0], "nodes": sorted(seen)})
     return FusionSpec(nodes=nodes, edges=edges, terminal=ids[output], params=params, nested=nested,
-                      w_layout=w_layout, x_arg=pos[a], w_arg=pos[w])
+                      w_layout=w_layout, x_arg=pos[a], w_arg=pos[w], outputs=[ids[o] for o in outs])
 
 
 # ---------------------------------------------------------------------------
@@ -443,8 +467,69 @@ class _Matcher:
         return None
 
 
+def quant_tail(spec: FusionSpec):
+    """(qmax, roles) for the results beside the stored tensor, or None when
+    the function returns only it.  roles[i] is "z", "s" or "q" for result i:
+    s = amax(|z|) / qmax (row statistic), q = e4m3(z / s)."""
+    outs = spec.outputs or [spec.terminal]
+    if len(outs) == 1:
+        return None
+    m = _Matcher(spec)
+    z = spec.terminal
+
+    def scale_of(i):   # qmax if node i is amax(|z|) / qmax (or * 1/qmax)
+        sc = m.scaled(i)
+        if sc is None or not (sc[1] > 0 and math.isfinite(sc[1])):
+            return None
+        r = m.node(sc[0])
+        if r.kind == "reduce" and r.op == "amax" and m.is_op(r.inputs[0], "abs") and m.node(r.inputs[0]).inputs[0] == z:
+            return 1.0 / sc[1]
+        return None
+
+    roles, qmax, s_node = [], None, None
+    for o in outs:
+        if o == z:
+            roles.append("z")
+            continue
+        if m.is_op(o, "e4m3"):
+            d = m.node(o).inputs[0]
+            q_s = None
+            if m.is_op(d, "div") and m.node(d).inputs[0] == z:
+                q_s = m.node(d).inputs[1]
+            elif m.is_op(d, "mul"):
+                for zz, rcp in m.commuted(d, "mul"):
+                    if zz == z and m.is_op(rcp, "reciprocal"):
+                        q_s = m.node(rcp).inputs[0]
+            if q_s is None or scale_of(q_s) is None:
+                raise UnsupportedEpilogue("codes must be (z / s).to(float8_e4m3fn) with s = amax(|z|) / qmax")
+            if s_node is not None and s_node != q_s:
+                raise UnsupportedEpilogue("the codes and the returned scale use different scales")
+            s_node, qmax = q_s, scale_of(q_s)
+            roles.append("q")
+            continue
+        if scale_of(o) is not None:
+            if s_node is not None and s_node != o:
+                raise UnsupportedEpilogue("the codes and the returned scale use different scales")
+            s_node, qmax = o, scale_of(o)
+            roles.append("s")
+            continue
+        raise UnsupportedEpilogue("a second result must be the row scale amax(|z|) / qmax or the E4M3 codes")
+    if roles.count("z") != 1 or roles.count("s") > 1 or roles.count("q") > 1:
+        raise UnsupportedEpilogue("results: the stored tensor once, the scale and the codes at most once each")
+    return qmax, roles
+
+
 def lower(spec: FusionSpec) -> list:
-    """Node-list template for spec (without the STORE), or UnsupportedEpilogue."""
+    """Node-list template for spec (without the STORE; a row quantisation tail
+    comes last, after the place of the STORE), or UnsupportedEpilogue."""
+    tail = quant_tail(spec)
+    out = _lower_main(spec)
+    if tail is not None:
+        out.append(NodeTemplate(cf.CF_N_ROWAMAX_QUANT, f0=tail[0]))
+    return out
+
+
+def _lower_main(spec: FusionSpec) -> list:
     m = _Matcher(spec)
     out = []
     t = spec.terminal
@@ -504,9 +589,12 @@ class FusedGemmEpilogue:
 
     def __init__(self, spec, templates, out_dtype=None, path=cf.PATH_AUTO):
         self.spec, self.templates, self.out_dtype, self.path = spec, templates, out_dtype, path
+        tail = quant_tail(spec)
+        self.roles = tail[1] if tail is not None else None
 
     def node_kinds(self):
-        return [t.kind for t in self.templates] + [cf.CF_N_STORE]
+        k = [t.kind for t in self.templates if t.kind != cf.CF_N_ROWAMAX_QUANT] + [cf.CF_N_STORE]
+        return k + [t.kind for t in self.templates if t.kind == cf.CF_N_ROWAMAX_QUANT]
 
     def __call__(self, *args, out=None, ws=None, stream=None):
         torch = cf._torch()
@@ -515,8 +603,11 @@ class FusedGemmEpilogue:
         N = W.shape[0] if self.spec.w_layout == cf.CF_LAYOUT_NK else W.shape[1]
         names = {name: args[p] for name, (_, p) in self.spec.params.items()}
         Y = out if out is not None else torch.empty((M, N), dtype=self.out_dtype or X.dtype, device=X.device)
-        spec = []
+        spec, quant = [], None
         for t in self.templates:
+            if t.kind == cf.CF_N_ROWAMAX_QUANT:
+                quant = t
+                continue
             d = dict(kind=t.kind, f0=t.f0)
             if t.v0:
                 d["v0"] = names[t.v0]
@@ -532,8 +623,17 @@ class FusedGemmEpilogue:
                     raise UnsupportedEpilogue("row-vector operands must be fp32 [N]")
             spec.append(d)
         spec.append(dict(kind=cf.CF_N_STORE, out=Y, ld=cf._ld(Y), dtype=cf._dt(Y)))
+        if quant is None:
+            cf.gemm_subgraph(X, W, spec, w_layout=self.spec.w_layout, path=self.path, ws=ws, stream=stream)
+            return Y
+        # the row scale (fp32 [M], returned as [M, 1]) and the codes (bytes,
+        # returned as float8_e4m3fn)
+        s = torch.empty(M, dtype=torch.float32, device=X.device)
+        Q = torch.empty((M, N), dtype=torch.uint8, device=X.device) if "q" in self.roles else None
+        spec.append(dict(kind=cf.CF_N_ROWAMAX_QUANT, out=s, out2=Q, ld=N if Q is not None else 0, f0=quant.f0))
         cf.gemm_subgraph(X, W, spec, w_layout=self.spec.w_layout, path=self.path, ws=ws, stream=stream)
-        return Y
+        res = {"z": Y, "s": s.view(M, 1), "q": Q.view(torch.float8_e4m3fn) if Q is not None else None}
+        return tuple(res[r] for r in self.roles)
 
 
 class EagerEpilogue:

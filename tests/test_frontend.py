@@ -230,3 +230,94 @@ def test_lowered_epilogue_on_gpu(name):
     err = float(np.max(np.abs(got - ref)))
     rel = float(np.sqrt(np.sum((got - ref) ** 2) / np.sum(ref ** 2)))
     assert err < 2e-2 and rel < 5e-3, (err, rel)
+
+
+# -- the row quantisation tail (ROWAMAX_QUANT): extra results beside z
+FP8 = torch.float8_e4m3fn
+
+
+def _chain_div(X, W, b, r):
+    z = F.gelu(_ln(X @ W.t() + b + r))
+    s = z.abs().amax(dim=-1, keepdim=True) / 448.0
+    return z, s, (z / s).to(FP8)
+
+
+def _chain_rcp_reordered(X, W, b, r):
+    z = F.gelu(_ln(X @ W.t() + b + r))
+    s = z.abs().amax(dim=-1, keepdim=True) * (1.0 / 448.0)
+    return (z * torch.reciprocal(s)).to(FP8), z, s
+
+
+def _chain_scale_only(X, W, b, r):
+    z = F.gelu(_ln(X @ W.t() + b + r))
+    return z, z.abs().amax(dim=-1, keepdim=True) / 448.0
+
+
+QUANT = {"div": (_chain_div, ["z", "s", "q"]), "rcp_reordered": (_chain_rcp_reordered, ["q", "z", "s"]),
+         "scale_only": (_chain_scale_only, ["z", "s"])}
+
+
+@pytest.mark.parametrize("name", sorted(QUANT))
+def test_quant_tail_lowering(name):
+    fn, roles = QUANT[name]
+    ep = fe.compile_epilogue(fn, _args("X W b r".split(), dtype=torch.float32))
+    assert ep.fused and ep.roles == roles
+    assert [KIND[k] for k in ep.node_kinds()] == ["BIAS", "RESIDUAL", "LAYERNORM", "GELU", "STORE", "ROWAMAX_QUANT"]
+    assert ep.templates[-1].f0 == pytest.approx(448.0)
+
+
+def test_quant_tail_semantics():
+    """Oracle evaluation of the lowered list (main part, then the oracle's
+    row-amax quantiser) == the function evaluated by PyTorch in fp64."""
+    args = _args("X W b r".split(), seed=2)
+    z_t, s_t, q_t = _chain_div(*args)
+    ep = fe.compile_epilogue(_chain_div, tuple(a.float() for a in args))
+    X, W = args[ep.spec.x_arg].numpy(), args[ep.spec.w_arg].numpy()
+    main = fe.FusedGemmEpilogue(ep.spec, ep.templates[:-1])
+    z = _eval_oracle(O.matmul(X, W.T), main, args)
+    s, q = O.rowamax_quant(z, ep.templates[-1].f0)
+    assert np.max(np.abs(z - z_t.numpy())) < 2e-6          # the oracle's erf vs torch's
+    np.testing.assert_allclose(s, s_t.numpy()[:, 0], rtol=1e-5)
+    codes_t = q_t.view(torch.uint8).numpy()
+    assert np.mean(codes_t == q) >= 0.99
+    assert np.max(np.abs(O.e4m3_decode(codes_t) - O.e4m3_decode(q)) / s[:, None]) <= 32.0
+
+
+UNSUPPORTED_TAIL = {
+    "amax_without_abs": lambda X, W: (lambda z: (z, z.amax(-1, keepdim=True) / 448.0))(F.gelu(X @ W.t())),
+    "codes_of_another_scale": lambda X, W: (lambda z: (z, (z / 2.0).to(FP8)))(F.gelu(X @ W.t())),
+    "two_stored_tensors": lambda X, W: (lambda z: (z, z * 2.0))(F.gelu(X @ W.t())),
+}
+
+
+@pytest.mark.parametrize("name", sorted(UNSUPPORTED_TAIL))
+def test_quant_tail_outside_the_domain(name):
+    with pytest.raises(fe.UnsupportedEpilogue):
+        fe.compile_epilogue(UNSUPPORTED_TAIL[name], _args("X W".split(), dtype=torch.float32))
+
+
+@pytest.mark.gpu
+def test_lowered_quant_tail_on_gpu():
+    """The LN -> GELU -> amax -> E4M3 chain written in PyTorch, lowered and run
+    fused (fp32 z out, so the codes can be recomputed exactly from it), against
+    the fp64 oracle (ragged 300 rows, K = N = 256)."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    small = tuple(a.cuda() for a in _args("X W b r".split(), dtype=torch.float32))
+    ep = fe.compile_epilogue(_chain_div, small, out_dtype=torch.float32)
+    g = torch.Generator().manual_seed(9)
+    X = torch.randn(300, 256, generator=g).to(torch.bfloat16)
+    W = (torch.randn(256, 256, generator=g) / 16.0).to(torch.bfloat16)
+    b = 0.02 * torch.randn(256, generator=g)
+    r = torch.randn(300, 256, generator=g).to(torch.bfloat16)
+    z, s, q = ep(X.cuda(), W.cuda(), b.cuda(), r.cuda())
+    torch.cuda.synchronize()
+    assert q.dtype == FP8 and s.shape == (300, 1)
+    zg, sg, qg = z.cpu().numpy(), s.cpu().numpy()[:, 0], q.view(torch.uint8).cpu().numpy()
+    zr, sr, qr = O.ln_gelu_amax(X.double().numpy(), W.double().numpy().T, b.double().numpy(), r.double().numpy())
+    assert np.max(np.abs(zg - zr)) < 1e-4
+    np.testing.assert_allclose(sg, sr, rtol=1e-3)
+    s32, q32 = O.rowamax_quant_f32(zg)
+    np.testing.assert_array_equal(sg, s32)
+    np.testing.assert_array_equal(qg, q32)
+    assert np.mean(qg == qr) >= 0.9999
