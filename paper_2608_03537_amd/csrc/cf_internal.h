@@ -81,7 +81,7 @@ constexpr int kMaxSlots = 64;                        // concurrent peer groups
 // that peer finished round r.)
 constexpr int kRecPeers = 17, kRecRows = 128;        // peers 0..15, then the leader's broadcast
 constexpr int kRecLead = 16;                         // record of the merged values (leader-follower)
-constexpr int kLeaderFollowerPeers = 8;              // peer counts from which the leader merges for all
+constexpr int kLeaderFollowerPeers = 16;             // peer counts from which the leader merges for all
 constexpr size_t kRecSetWords = (size_t)kMaxSlots * kRecPeers * kRecRows * 2;   // one parity of one stage
 constexpr size_t kRecStageWords = 2 * kRecSetWords;
 constexpr size_t kWsCounterBytes = 4096;             // err word, then the counters
