@@ -53,6 +53,7 @@ extern "C" {
 
 #define CF_VERSION 1
 #define CF_WS_HEADER_BYTES 8916992  /* 4096 + 2 stages * 2 parities * 64 slots * 17 records * 128 rows * 16 */
+#define CF_B2B_WS_HEADER_BYTES 1048576  /* split-MLP arrival counters: 262144 words of 4 bytes */
 
 typedef enum {
   CF_F32 = 0,       /* IEEE binary32 */
@@ -236,10 +237,14 @@ cf_status cf_gemm_subgraph_noalloc(const cf_subgraph_args* a, void* hip_stream);
  * dataflow of Sec. IV-A); their partial second products are summed at
  * commit, in chunk order, by the last workgroup of the row block to finish.
  * Workspace: 0 bytes for the FFN, attention, and MLP with N1 = 256; for MLP
- * with N1 > 256, cf_b2bgemm_workspace() bytes: arrival counters, then fp32
- * partial products.  Zero-fill the workspace once before its first MLP call;
- * every call leaves the counters at zero again.  Do not share it with calls
- * of another kind, and do not let calls that share it overlap in time.
+ * with N1 > 256, cf_b2bgemm_workspace() bytes, 16-byte aligned:
+ * CF_B2B_WS_HEADER_BYTES of arrival counters (one 32-bit word per batch
+ * entry and 128-row block, so batch * ceil(M / 128) <= 262144, else
+ * CF_ERR_SHAPE), then the fp32 partial products.  Zero-fill the header once
+ * before the first MLP call; every call leaves it all zero again and the
+ * partials never reach into it, so later calls of any shape find it valid.
+ * Do not share the workspace with calls of another kind, and do not let
+ * calls that share it overlap in time.
  * ------------------------------------------------------------------------ */
 typedef enum { CF_MID_GELU_BIAS = 0, CF_MID_SOFTMAX = 1, CF_MID_RELU_BIAS = 2 } cf_mid_op;
 typedef enum { CF_OUT_STORE = 0, CF_OUT_BIAS_RESIDUAL_LN = 1, CF_OUT_BIAS_RELU = 2 } cf_out_op;

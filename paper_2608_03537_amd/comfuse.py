@@ -26,6 +26,7 @@ CF_LAYOUT_KN, CF_LAYOUT_NK = 0, 1
 CF_MID_GELU_BIAS, CF_MID_SOFTMAX, CF_MID_RELU_BIAS = 0, 1, 2
 CF_OUT_STORE, CF_OUT_BIAS_RESIDUAL_LN, CF_OUT_BIAS_RELU = 0, 1, 2
 PATH_AUTO, PATH_WHOLE_ROW, PATH_CLUSTER, PATH_SPLIT = 0, 1, 2, 3
+CF_B2B_WS_HEADER_BYTES = 1 << 20   # split-MLP arrival counters at the start of its workspace
 STATUS = {0: "CF_OK", 1: "CF_ERR_NULL", 2: "CF_ERR_SHAPE", 3: "CF_ERR_LD", 4: "CF_ERR_ALIGN",
           5: "CF_ERR_DTYPE", 6: "CF_ERR_WORKSPACE", 7: "CF_ERR_UNSUPPORTED", 8: "CF_ERR_ALIAS",
           9: "CF_ERR_HIP", 10: "CF_ERR_STRUCT", 11: "CF_ERR_PEER_TIMEOUT"}
@@ -381,6 +382,19 @@ def rowop(P, spec, stream=None):
     _check(cf_rowop(nb, M, N, _dt(P), _ptr(P), ldp, sp, nodes, len(nodes), _stream(stream)))
 
 
+def _stack(t, batch=None):
+    """(batch, rows, cols, ld, batch stride) of a [rows, cols] or [batch, rows,
+    cols] operand with unit column stride.  A 2-D operand beside batched ones
+    is shared by every batch entry (stride 0)."""
+    if t.dim() == 2:
+        return (batch or 1), t.shape[0], t.shape[1], _ld(t), 0
+    if t.dim() != 3 or t.stride(2) != 1:
+        raise ValueError("expected a 2-D or 3-D tensor with unit column stride")
+    if batch is not None and t.shape[0] != batch:
+        raise ValueError(f"batch {t.shape[0]} != {batch}")
+    return t.shape[0], t.shape[1], t.shape[2], t.stride(1), t.stride(0)
+
+
 def _b2b_args(**kw):
     a = B2BArgs()
     a.struct_size = C.sizeof(B2BArgs)
@@ -395,18 +409,25 @@ def b2b_ffn(X, W1t, b1, W2t, b2=None, R=None, gamma=None, beta=None, *, eps=1e-5
 
     X [M, K] bf16; W1t = W1^T [N1, K]; W2t = W2^T [N2, N1]; R [M, N2] (pass X
     for the residual FFN block).  With layernorm=False, O = S W2 (+ b2 + R).
+    Batched: X [B, M, K] (and R, out [B, M, N2]); a 3-D weight holds one
+    matrix per batch entry, a 2-D one is shared; vectors are shared.
     """
     torch = _torch()
-    M, K = X.shape
-    N1, N2 = W1t.shape[0], W2t.shape[0]
-    O = out if out is not None else torch.empty((M, N2), dtype=torch.bfloat16, device=X.device)
-    a = _b2b_args(batch=1, M=M, K=K, N1=N1, N2=N2, dtype=CF_BF16,
-                  X=_ptr(X), ldx=_ld(X), sx=0, W1=_ptr(W1t), ldw1=_ld(W1t), sw1=0, w1_layout=CF_LAYOUT_NK,
+    B, M, K, ldx, sx = _stack(X)
+    B = B if X.dim() == 3 else None
+    _, N1, _, ldw1, sw1 = _stack(W1t, B)
+    _, N2, _, ldw2, sw2 = _stack(W2t, B)
+    shape = (M, N2) if B is None else (B, M, N2)
+    O = out if out is not None else torch.empty(shape, dtype=torch.bfloat16, device=X.device)
+    _, _, _, ldo, so = _stack(O, B)
+    ldr, sr = _stack(R, B)[3:] if R is not None else (0, 0)
+    a = _b2b_args(batch=B or 1, M=M, K=K, N1=N1, N2=N2, dtype=CF_BF16,
+                  X=_ptr(X), ldx=ldx, sx=sx, W1=_ptr(W1t), ldw1=ldw1, sw1=sw1, w1_layout=CF_LAYOUT_NK,
                   b1=_ptr(b1), mid=CF_MID_GELU_BIAS, mid_scale=1.0,
-                  W2=_ptr(W2t), ldw2=_ld(W2t), sw2=0, w2_layout=CF_LAYOUT_NK,
+                  W2=_ptr(W2t), ldw2=ldw2, sw2=sw2, w2_layout=CF_LAYOUT_NK,
                   out=CF_OUT_BIAS_RESIDUAL_LN if layernorm else CF_OUT_STORE, b2=_ptr(b2),
-                  R=_ptr(R), ldr=(_ld(R) if R is not None else 0), sr=0,
-                  gamma=_ptr(gamma), beta=_ptr(beta), eps=eps, O=_ptr(O), ldo=_ld(O), so=0)
+                  R=_ptr(R), ldr=ldr, sr=sr,
+                  gamma=_ptr(gamma), beta=_ptr(beta), eps=eps, O=_ptr(O), ldo=ldo, so=so)
     _check(cf_b2bgemm(a, None, 0, _stream(stream)))
     return O
 
@@ -414,17 +435,22 @@ def b2b_ffn(X, W1t, b1, W2t, b2=None, R=None, gamma=None, beta=None, *, eps=1e-5
 def b2b_mlp(X, W1t, b1, W2t, b2=None, *, out_relu=False, out=None, ws=None, stream=None):
     """Fused MLP block O = ReLU(X W1 + b1) W2 + b2 (ReLU(O) with out_relu), the
     DLRM bottom-MLP pattern.  X [M, K] bf16; W1t = W1^T [N1, K]; W2t = W2^T
-    [N2, N1]; hidden units split over workgroups in chunks of 256."""
+    [N2, N1]; hidden units split over workgroups in chunks of 256.  Batched
+    as b2b_ffn: X, out [B, M, .], weights 3-D (per entry) or 2-D (shared)."""
     torch = _torch()
-    M, K = X.shape
-    N1, N2 = W1t.shape[0], W2t.shape[0]
-    O = out if out is not None else torch.empty((M, N2), dtype=torch.bfloat16, device=X.device)
-    a = _b2b_args(batch=1, M=M, K=K, N1=N1, N2=N2, dtype=CF_BF16,
-                  X=_ptr(X), ldx=_ld(X), sx=0, W1=_ptr(W1t), ldw1=_ld(W1t), sw1=0, w1_layout=CF_LAYOUT_NK,
+    B, M, K, ldx, sx = _stack(X)
+    B = B if X.dim() == 3 else None
+    _, N1, _, ldw1, sw1 = _stack(W1t, B)
+    _, N2, _, ldw2, sw2 = _stack(W2t, B)
+    shape = (M, N2) if B is None else (B, M, N2)
+    O = out if out is not None else torch.empty(shape, dtype=torch.bfloat16, device=X.device)
+    _, _, _, ldo, so = _stack(O, B)
+    a = _b2b_args(batch=B or 1, M=M, K=K, N1=N1, N2=N2, dtype=CF_BF16,
+                  X=_ptr(X), ldx=ldx, sx=sx, W1=_ptr(W1t), ldw1=ldw1, sw1=sw1, w1_layout=CF_LAYOUT_NK,
                   b1=_ptr(b1), mid=CF_MID_RELU_BIAS, mid_scale=1.0,
-                  W2=_ptr(W2t), ldw2=_ld(W2t), sw2=0, w2_layout=CF_LAYOUT_NK,
+                  W2=_ptr(W2t), ldw2=ldw2, sw2=sw2, w2_layout=CF_LAYOUT_NK,
                   out=CF_OUT_BIAS_RELU if out_relu else CF_OUT_STORE, b2=_ptr(b2),
-                  R=None, ldr=0, sr=0, gamma=None, beta=None, eps=0.0, O=_ptr(O), ldo=_ld(O), so=0)
+                  R=None, ldr=0, sr=0, gamma=None, beta=None, eps=0.0, O=_ptr(O), ldo=ldo, so=so)
     need = cf_b2bgemm_workspace(a)
     if ws is None:
         ws = workspace(need, X.device, stream, kind="b2b")

@@ -16,6 +16,9 @@
 
 using namespace cf;
 
+static_assert(kWsHeaderBytes == CF_WS_HEADER_BYTES, "row-cluster workspace header size in the header file");
+static_assert(kMlpCounterBytes == CF_B2B_WS_HEADER_BYTES, "split-MLP counter region size in the header file");
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -700,14 +703,17 @@ cf_status cf_workspace_check(void* workspace, size_t ws_bytes, void* hip_stream)
   }
 }
 
-// Workspace of the split MLP: arrival counters [batch][row blocks] (256-byte
-// aligned block), then fp32 partials [batch][cn][M][N2].  Other B2B forms need none.
+// Workspace of the split MLP: the fixed counter region (words [batch][row
+// blocks] at its start), then fp32 partials [batch][cn][M][N2].  The counter
+// region does not depend on the shape, so partials of one call never land
+// where a later call of another shape expects zeroed counters.  Other B2B
+// forms need none.
 static size_t mlp_workspace(const cf_b2b_args* a) {
   if (!a || a->struct_size != sizeof(cf_b2b_args) || a->mid != CF_MID_RELU_BIAS || a->N1 <= kMlpHidden ||
       a->M <= 0 || a->batch <= 0)
     return 0;
-  const int64_t rbs = (a->M + kMlpRows - 1) / kMlpRows, cn = a->N1 / kMlpHidden;
-  return round_up((size_t)(a->batch * rbs * 4), 256) + (size_t)(a->batch * cn * a->M * a->N2 * 4);
+  const int64_t cn = a->N1 / kMlpHidden;
+  return kMlpCounterBytes + (size_t)(a->batch * cn * a->M * a->N2 * 4);
 }
 
 size_t cf_b2bgemm_workspace(const cf_b2b_args* a) {
@@ -745,6 +751,9 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, voi
       if (a->M > 0 && a->batch > 0) {
         const size_t need = mlp_workspace(a);
         if (need > 0) {
+          if (a->batch * ((a->M + kMlpRows - 1) / kMlpRows) > kMlpMaxRowBlocks)
+            return fail(CF_ERR_SHAPE, "split MLP: batch * ceil(M / %d) exceeds %lld counters", kMlpRows,
+                        (long long)kMlpMaxRowBlocks);
           if (!workspace) return fail(CF_ERR_WORKSPACE, "workspace of %zu bytes required (N1 split over workgroups)", need);
           if (ws_bytes < need) return fail(CF_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
           if (!aligned16(workspace)) return fail(CF_ERR_ALIGN, "workspace is not 16-byte aligned");
@@ -818,10 +827,9 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, voi
       p.out_relu = a->out == CF_OUT_BIAS_RELU;
       p.cn = (int)(a->N1 / kMlpHidden);
       if (p.cn > 1) {
-        const int64_t rbs = (a->M + kMlpRows - 1) / kMlpRows;
         char* b = reinterpret_cast<char*>(workspace);
         p.ws_count = reinterpret_cast<unsigned*>(b);
-        p.ws_part = reinterpret_cast<float*>(b + round_up((size_t)(a->batch * rbs * 4), 256));
+        p.ws_part = reinterpret_cast<float*>(b + kMlpCounterBytes);
       }
       return hip_status(launch_b2b_mlp(p, st), "B2B MLP launch");
     }

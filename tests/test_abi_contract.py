@@ -13,7 +13,9 @@ from paper_2608_03537_amd import comfuse as cf
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "comfuse.h")
 with open(HEADER) as _f:
-    HDR = int(re.search(r"#define CF_WS_HEADER_BYTES (\d+)", _f.read()).group(1))
+    _TEXT = _f.read()
+    HDR = int(re.search(r"#define CF_WS_HEADER_BYTES (\d+)", _TEXT).group(1))
+    B2B_HDR = int(re.search(r"#define CF_B2B_WS_HEADER_BYTES (\d+)", _TEXT).group(1))
 
 A = 0x7F0000000000          # 16-byte aligned fake device addresses
 B = 0x7F0000100000
@@ -213,7 +215,8 @@ def test_noalloc_validation_before_any_device_call():
 def _mlp(**kw):
     a = cf.B2BArgs()
     a.struct_size = C.sizeof(cf.B2BArgs)
-    a.batch, a.M, a.K, a.N1, a.N2 = 1, kw.get("M", 300), kw.get("K", 1024), kw.get("N1", 512), kw.get("N2", 128)
+    a.batch, a.M, a.K, a.N1, a.N2 = (kw.get("batch", 1), kw.get("M", 300), kw.get("K", 1024), kw.get("N1", 512),
+                                     kw.get("N2", 128))
     a.dtype, a.mid, a.out = cf.CF_BF16, cf.CF_MID_RELU_BIAS, kw.get("out", cf.CF_OUT_STORE)
     a.X, a.ldx, a.W1, a.ldw1, a.w1_layout = A, a.K, B, a.K, cf.CF_LAYOUT_NK
     a.W2, a.ldw2, a.w2_layout = R, a.N1, cf.CF_LAYOUT_NK
@@ -222,8 +225,17 @@ def _mlp(**kw):
 
 
 def test_mlp_workspace_and_validation():
-    # counters for ceil(300 / 128) = 3 row blocks (256-byte block), then 2 x 300 x 128 fp32 partials
-    assert cf.cf_b2bgemm_workspace(_mlp()) == 256 + 2 * 300 * 128 * 4
+    # the fixed counter region, then 2 chunks x 300 rows x 128 fp32 partials (per batch entry)
+    assert B2B_HDR == cf.CF_B2B_WS_HEADER_BYTES
+    assert cf.cf_b2bgemm_workspace(_mlp()) == B2B_HDR + 2 * 300 * 128 * 4
+    assert cf.cf_b2bgemm_workspace(_mlp(batch=3, M=1000, N1=1024)) == B2B_HDR + 3 * 4 * 1000 * 128 * 4
+    # one counter per (batch entry, 128-row block): 3 x 87382 > 2^18 counters
+    big = _mlp(batch=3, M=128 * 87382)
+    big.sx, big.so = big.M * big.K, big.M * big.N2
+    assert cf.STATUS[cf.cf_b2bgemm(big, A, 1 << 62, None)] == "CF_ERR_SHAPE"
+    assert "counters" in cf.cf_last_error()
+    big.batch = 2                                                # 2 x 87382 fits
+    assert cf.STATUS[cf.cf_b2bgemm(big, A, 1, None)] == "CF_ERR_WORKSPACE"
     assert cf.cf_b2bgemm_workspace(_mlp(N1=256)) == 0           # one chunk: nothing to sum
     assert cf.STATUS[cf.cf_b2bgemm(_mlp(), None, 0, None)] == "CF_ERR_WORKSPACE"
     assert cf.STATUS[cf.cf_b2bgemm(_mlp(N2=64), A, 1 << 30, None)] == "CF_ERR_UNSUPPORTED"

@@ -81,6 +81,28 @@ def test_ffn_full_size():
     assert_close_bf16(run_ffn(inp), ref, "FFN 65536x256x512")
 
 
+@pytest.mark.parametrize("residual", ["x", "other"])
+def test_ffn_batched(residual):
+    """batch = 3 entries of 257 rows, d = 256, N1 = 512: X, R, O [3, M, d];
+    W1 shared (2-D), W2 per entry (3-D); b1, b2, gamma, beta shared.  R = X
+    takes the kernel's residual-from-the-X-tile path, another R the load."""
+    Bn, M, d, N1 = 3, 257, 256, 512
+    ins = [I.ffn_inputs(seed=30 + b, M=M, d=d, N1=N1) for b in range(Bn)]
+    X = dev(np.stack([t.X for t in ins]))
+    Rh = np.stack([t.X for t in ins]) if residual == "x" else \
+        I.round_to_bf16(np.random.default_rng(9).standard_normal((Bn, M, d)).astype(np.float32))
+    R = X if residual == "x" else dev(Rh)
+    W1t = dev(I.lay_out_weight(ins[0].W1, "nk"))
+    W2t = dev(np.stack([I.lay_out_weight(t.W2, "nk") for t in ins]))
+    Y = cf.b2b_ffn(X, W1t, dev(ins[0].b1, "f32"), W2t, dev(ins[0].b2, "f32"), R, eps=ins[0].eps)
+    torch.cuda.synchronize()
+    got = host(Y)
+    for b in range(Bn):
+        S = O.gelu_erf(O.bias_residual(O.matmul(ins[b].X, ins[0].W1), ins[0].b1))
+        ref = O.layernorm(O.bias_residual(O.matmul(S, ins[b].W2), ins[0].b2, Rh[b]), eps=ins[0].eps)
+        assert_close_bf16(got[b], ref, f"FFN batch entry {b} residual={residual}")
+
+
 def run_attn(Q, K, V, scale=None):
     o = cf.b2b_attention(dev(Q), dev(K), dev(V), scale)
     torch.cuda.synchronize()

@@ -60,8 +60,7 @@ def test_mlp_split_is_deterministic_and_leaves_counters_at_zero():
     torch.cuda.synchronize()
     for o in outs[1:]:
         assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
-    rbs = (inp.M + 127) // 128
-    assert int(ws[:rbs * 4].view(torch.int32).abs().sum().item()) == 0
+    assert int(ws[:cf.CF_B2B_WS_HEADER_BYTES].view(torch.int32).abs().sum().item()) == 0
     assert_close_bf16(host(outs[0]), O.mlp_b2b(inp.X, inp.W1, inp.b1, inp.W2, inp.b2), "MLP 4096x512x1024")
 
 
@@ -76,3 +75,36 @@ def test_mlp_dlrm_full_size_block_rows():
     ref = O.mlp_b2b(inp.X[rows], inp.W1, inp.b1, inp.W2, inp.b2, out_relu=True)
     assert_close_bf16(Y[rows], ref, "DLRM MLP 65536x1024x512x128")
     assert np.all(Y >= 0.0)
+
+
+def test_mlp_shape_change_on_one_workspace():
+    """Calls of different shapes share a workspace: the second call has more
+    row blocks (more arrival counters) than the first, and the first call's
+    partials must not be read as the second call's counters."""
+    ws = torch.zeros(96 << 20, dtype=torch.uint8, device="cuda")
+    for M, K, N1 in [(16384, 128, 1024), (40000, 128, 512), (300, 256, 768)]:
+        inp = I.dlrm_mlp_inputs(seed=6, M=M, K=K, N1=N1)
+        got = host(run_mlp(inp, ws=ws))
+        assert_close_bf16(got, O.mlp_b2b(inp.X, inp.W1, inp.b1, inp.W2, inp.b2), f"MLP {M}x{K}x{N1} after another shape")
+        assert int(ws[:cf.CF_B2B_WS_HEADER_BYTES].view(torch.int32).abs().sum().item()) == 0
+
+
+@pytest.mark.parametrize("shared_w1,shared_w2", [(False, True), (True, False), (False, False)])
+def test_mlp_batched(shared_w1, shared_w2):
+    """batch = 3 entries of 300 rows: X and O [3, M, .], each weight per entry
+    (3-D, batch stride) or shared (2-D, stride 0); biases shared."""
+    Bn, M, K, N1 = 3, 300, 256, 512
+    ins = [I.dlrm_mlp_inputs(seed=20 + b, M=M, K=K, N1=N1) for b in range(Bn)]
+    w1 = [ins[0 if shared_w1 else b].W1 for b in range(Bn)]
+    w2 = [ins[0 if shared_w2 else b].W2 for b in range(Bn)]
+    X = dev(np.stack([t.X for t in ins]))
+    W1t = dev(I.lay_out_weight(w1[0], "nk")) if shared_w1 else dev(np.stack([I.lay_out_weight(w, "nk") for w in w1]))
+    W2t = dev(I.lay_out_weight(w2[0], "nk")) if shared_w2 else dev(np.stack([I.lay_out_weight(w, "nk") for w in w2]))
+    Y = cf.b2b_mlp(X, W1t, dev(ins[0].b1, "f32"), W2t, dev(ins[0].b2, "f32"), out_relu=True)
+    torch.cuda.synchronize()
+    assert tuple(Y.shape) == (Bn, M, 128)
+    got = host(Y)
+    for b in range(Bn):
+        ref = O.mlp_b2b(ins[b].X, w1[b], ins[0].b1, w2[b], ins[0].b2, out_relu=True)
+        assert_close_bf16(got[b], ref, f"MLP batch entry {b}")
+
