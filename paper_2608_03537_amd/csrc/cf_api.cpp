@@ -16,6 +16,11 @@
 
 using namespace cf;
 
+// Split-MLP arrival counters: a fixed region at the start of the workspace,
+// one word per (batch entry, row block); the partials start after it.
+static constexpr size_t kMlpCounterBytes = size_t(1) << 20;
+static constexpr int64_t kMlpMaxRowBlocks = int64_t(kMlpCounterBytes / 4);
+
 static_assert(kWsHeaderBytes == CF_WS_HEADER_BYTES, "row-cluster workspace header size in the header file");
 static_assert(kMlpCounterBytes == CF_B2B_WS_HEADER_BYTES, "split-MLP counter region size in the header file");
 

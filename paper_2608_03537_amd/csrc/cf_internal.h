@@ -158,10 +158,6 @@ hipError_t launch_b2b_mlp(const B2BParams& p, hipStream_t st);        // -> hipE
 bool b2b_ffn_supported(int N1, int N2);
 bool b2b_mlp_supported(int K, int N1, int N2);
 constexpr int kMlpRows = 128, kMlpHidden = 256;   // rows and hidden units of one MLP workgroup
-// Split-MLP arrival counters: a fixed region at the start of the workspace,
-// one word per (batch entry, row block); the partials start after it.
-constexpr size_t kMlpCounterBytes = size_t(1) << 20;
-constexpr int64_t kMlpMaxRowBlocks = int64_t(kMlpCounterBytes / 4);
 bool b2b_attention_supported(int d);
 
 }  // namespace cf
