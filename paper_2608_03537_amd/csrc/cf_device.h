@@ -162,6 +162,23 @@ __device__ __forceinline__ void load4<float>(const float* p, float (&v)[4]) {
   const f32x4_t u = *reinterpret_cast<const f32x4_t*>(p);
   v[0] = u[0]; v[1] = u[1]; v[2] = u[2]; v[3] = u[3];
 }
+// The same for data read once (row-pass inputs, residuals): non-temporal
+// loads, so the lines do not displace reused operands in the caches.
+template <typename T>
+__device__ __forceinline__ void load4_once(const T* p, float (&v)[4]);
+template <>
+__device__ __forceinline__ void load4_once<bf16_t>(const bf16_t* p, float (&v)[4]) {
+  const u32x2_t u = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+  v[0] = bf16_to_f32(u[0] & 0xFFFFu);
+  v[1] = bf16_to_f32(u[0] >> 16);
+  v[2] = bf16_to_f32(u[1] & 0xFFFFu);
+  v[3] = bf16_to_f32(u[1] >> 16);
+}
+template <>
+__device__ __forceinline__ void load4_once<float>(const float* p, float (&v)[4]) {
+  const f32x4_t u = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(p));
+  v[0] = u[0]; v[1] = u[1]; v[2] = u[2]; v[3] = u[3];
+}
 
 // tanh(z) = sign(z) (1 - t) / (1 + t), t = exp(-2 |z|): no overflow for any z;
 // near 0 the absolute error stays at the fp32 rounding of 1 - t (~6e-8).
@@ -173,10 +190,10 @@ __device__ __forceinline__ float tanh_exp(float z) {
 __device__ __forceinline__ void store4(void* base, int64_t off, int f32, const float (&v)[4]) {
   if (f32) {
     f32x4_t o = {v[0], v[1], v[2], v[3]};
-    *reinterpret_cast<f32x4_t*>(reinterpret_cast<float*>(base) + off) = o;
+    __builtin_nontemporal_store(o, reinterpret_cast<f32x4_t*>(reinterpret_cast<float*>(base) + off));
   } else {
     u32x2_t o = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-    *reinterpret_cast<u32x2_t*>(reinterpret_cast<bf16_t*>(base) + off) = o;
+    __builtin_nontemporal_store(o, reinterpret_cast<u32x2_t*>(reinterpret_cast<bf16_t*>(base) + off));
   }
 }
 

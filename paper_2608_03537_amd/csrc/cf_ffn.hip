@@ -371,7 +371,7 @@ void b2b_ffn_kernel(B2BParams p) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         float r[4];
-        load4<bf16_t>(p.R + (int64_t)bz * p.sr + (int64_t)m * p.ldr + (nb0 + b) * 32 + 8 * g + 4 * lg, r);
+        load4_once<bf16_t>(p.R + (int64_t)bz * p.sr + (int64_t)m * p.ldr + (nb0 + b) * 32 + 8 * g + 4 * lg, r);
 #pragma unroll
         for (int q = 0; q < 4; ++q) Oa[b][4 * g + q] += r[q];
       }

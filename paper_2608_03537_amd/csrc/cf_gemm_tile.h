@@ -246,8 +246,9 @@ __device__ __forceinline__ void mainloop(f32x16_t (&acc)[S::BM][S::BN],
 
 // 16-byte global -> LDS copy for the whole wave: lane i's 16 bytes land at
 // LDS address lds + 16 * i (lds must be wave-uniform).
+template <int AUX = 0>
 __device__ __forceinline__ void dma16(const void* gptr, char* lds) {
-  __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+  __builtin_amdgcn_global_load_lds(gptr, (__attribute__((address_space(3))) void*)lds, 16, 0, AUX);
 }
 // Workgroup barrier without the implicit wait for outstanding memory
 // operations (callers wait explicitly); also a compiler reordering fence.
@@ -364,7 +365,7 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
         g = reinterpret_cast<const char*>(reinterpret_cast<const T*>(e.R) + (int64_t)bz * e.sr +
                                           (int64_t)m * e.ldr + n);
       }
-      dma16(g, smem + part * S::V2_STAGE + (wave * (part ? S::STG_IB : S::STG_IA) + i) * 1024);
+      dma16<2>(g, smem + part * S::V2_STAGE + (wave * (part ? S::STG_IB : S::STG_IA) + i) * 1024);
     }
   };
   auto vec_dma = [&]() {
@@ -833,7 +834,7 @@ __device__ __forceinline__ void store_tile_staged_t(const f32x16_t (&x)[S::BM][S
       const int id = tid + (j0 + j) * S::NT;
       const int r = id / CPR, cc = id % CPR;
       if (j0 + j < ITER && (TOTAL % S::NT == 0 || id < TOTAL) && (full || (r < rows && cc * EPC < cols)))
-        *reinterpret_cast<u32x4_t*>(yb + (unsigned)(r * ldyb + cc * 16)) = v[j];
+        __builtin_nontemporal_store(v[j], reinterpret_cast<u32x4_t*>(yb + (unsigned)(r * ldyb + cc * 16)));
     }
   }
   // The staging area is reused by the next reduction: every lane has read

@@ -267,7 +267,7 @@ void b2b_mlp_kernel(B2BParams p) {
     float2 y = t[j];
     if (p.b2) y = make_float2(y.x + bb.x, y.y + bb.y);
     if (p.out_relu) y = make_float2(fmaxf(y.x, 0.0f), fmaxf(y.y, 0.0f));
-    *reinterpret_cast<uint32_t*>(O + (int64_t)m * p.ldo + 2 * c2) = pack_bf16x2(y.x, y.y);
+    __builtin_nontemporal_store(pack_bf16x2(y.x, y.y), reinterpret_cast<uint32_t*>(O + (int64_t)m * p.ldo + 2 * c2));
   }
 }
 

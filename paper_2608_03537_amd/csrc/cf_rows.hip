@@ -72,8 +72,8 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
     const int n = 256 * j + 4 * lane;
     val[j] = n < N;
     if (val[j]) {
-      if (p.p_f32) load4<float>(reinterpret_cast<const float*>(p.P) + prow(p, m) + n, v[j]);
-      else load4<bf16_t>(reinterpret_cast<const bf16_t*>(p.P) + prow(p, m) + n, v[j]);
+      if (p.p_f32) load4_once<float>(reinterpret_cast<const float*>(p.P) + prow(p, m) + n, v[j]);
+      else load4_once<bf16_t>(reinterpret_cast<const bf16_t*>(p.P) + prow(p, m) + n, v[j]);
     } else {
       v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0.0f;
     }
@@ -124,8 +124,8 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
       }
       if (e.R) {
         float r[4];
-        if (e.r_f32) load4<float>(reinterpret_cast<const float*>(e.R) + (int64_t)m * e.ldr + n, r);
-        else load4<bf16_t>(reinterpret_cast<const bf16_t*>(e.R) + (int64_t)m * e.ldr + n, r);
+        if (e.r_f32) load4_once<float>(reinterpret_cast<const float*>(e.R) + (int64_t)m * e.ldr + n, r);
+        else load4_once<bf16_t>(reinterpret_cast<const bf16_t*>(e.R) + (int64_t)m * e.ldr + n, r);
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[j][q] += r[q];
       }
@@ -252,7 +252,7 @@ __global__ __launch_bounds__(256) void row_kernel(RowKernelParams p) {
         if (!val[j]) continue;
         const uint32_t w = e4m3x4(div_rn(v[j][0], sd, inv), div_rn(v[j][1], sd, inv), div_rn(v[j][2], sd, inv),
                                   div_rn(v[j][3], sd, inv));
-        *reinterpret_cast<uint32_t*>(e.q_out + (int64_t)m * e.ldq + 256 * j + 4 * lane) = nz ? w : 0u;
+        __builtin_nontemporal_store(nz ? w : 0u, reinterpret_cast<uint32_t*>(e.q_out + (int64_t)m * e.ldq + 256 * j + 4 * lane));
       }
     }
   }
@@ -288,8 +288,8 @@ __global__ __launch_bounds__(256) void wide_row_kernel(RowKernelParams p) {
   for (int j = 0; j < VPW; ++j) {
     val[j] = FULL || col(j) < N;
     if (val[j]) {
-      if (p.p_f32) load4<float>(reinterpret_cast<const float*>(p.P) + prow(p, m) + col(j), v[j]);
-      else load4<bf16_t>(reinterpret_cast<const bf16_t*>(p.P) + prow(p, m) + col(j), v[j]);
+      if (p.p_f32) load4_once<float>(reinterpret_cast<const float*>(p.P) + prow(p, m) + col(j), v[j]);
+      else load4_once<bf16_t>(reinterpret_cast<const bf16_t*>(p.P) + prow(p, m) + col(j), v[j]);
     } else {
       v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0.0f;
     }
@@ -309,8 +309,8 @@ __global__ __launch_bounds__(256) void wide_row_kernel(RowKernelParams p) {
       }
       if (e.R) {
         float r[4];
-        if (e.r_f32) load4<float>(reinterpret_cast<const float*>(e.R) + (int64_t)m * e.ldr + col(j), r);
-        else load4<bf16_t>(reinterpret_cast<const bf16_t*>(e.R) + (int64_t)m * e.ldr + col(j), r);
+        if (e.r_f32) load4_once<float>(reinterpret_cast<const float*>(e.R) + (int64_t)m * e.ldr + col(j), r);
+        else load4_once<bf16_t>(reinterpret_cast<const bf16_t*>(e.R) + (int64_t)m * e.ldr + col(j), r);
 #pragma unroll
         for (int q = 0; q < 4; ++q) v[j][q] += r[q];
       }
@@ -404,7 +404,7 @@ __global__ __launch_bounds__(256) void wide_row_kernel(RowKernelParams p) {
         if (!val[j]) continue;
         const uint32_t w = e4m3x4(div_rn(v[j][0], sd, inv), div_rn(v[j][1], sd, inv), div_rn(v[j][2], sd, inv),
                                   div_rn(v[j][3], sd, inv));
-        *reinterpret_cast<uint32_t*>(e.q_out + (int64_t)m * e.ldq + col(j)) = nz ? w : 0u;
+        __builtin_nontemporal_store(nz ? w : 0u, reinterpret_cast<uint32_t*>(e.q_out + (int64_t)m * e.ldq + col(j)));
       }
     }
   }
