@@ -1,6 +1,7 @@
 // Registry of the compiled GEMM kernels and their launcher.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -42,8 +43,12 @@ int resident_wgs(int idx) {
   if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
   const GemmKernel& k = table()[idx];
+  // Both forms must fit: the one-tile form runs when the grid is not capped.
+  int per_cu_persist = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k.fn, k.threads, 0) != hipSuccess) return 0;
-  cache[idx] = cus * per_cu;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_persist, k.fn_persist, k.threads, 0) != hipSuccess)
+    return 0;
+  cache[idx] = cus * std::min(per_cu, per_cu_persist);
   return cache[idx];
 }
 
@@ -51,7 +56,11 @@ hipError_t launch_gemm_rows(const GemmRowsParams& p, int idx, hipStream_t st) {
   const GemmKernel& k = table()[idx];
   dim3 grid((unsigned)(8 * p.slots * p.cn), (unsigned)p.batch), block((unsigned)k.threads);
   void* args[] = {const_cast<GemmRowsParams*>(&p)};
-  return hipLaunchKernel(k.fn, grid, block, args, 0, st);
+  // Without row clusters every tile has a workgroup of its own (grouped
+  // order); with them, workgroups loop only when the grid was capped below
+  // one slot per row block of each XCD.
+  const bool persist = p.mode == ROWS_CLUSTER && (int64_t)p.slots * 8 < (int64_t)p.num_rb;
+  return hipLaunchKernel(persist ? k.fn_persist : k.fn, grid, block, args, 0, st);
 }
 
 }  // namespace cf

@@ -304,50 +304,83 @@ __device__ __forceinline__ void wait_vmcnt() {
 // swizzle places on 4 distinct 64-byte bank groups.  Columns past N are
 // clamped to the last 8-column chunk.
 // ---------------------------------------------------------------------------
+// Ring geometry shared by the main loop and the early issue of its first
+// stages: this wave's global source of each of its PW 1 KB loads at stage 0,
+// the bytes between consecutive stages, and the slot rotation.
+template <class S, bool PERM, bool KN>
+struct RingSrc {
+  const char* src[S::V2_PER_WAVE];
+  int64_t w_step;
+  int rot;
+  __device__ __forceinline__ RingSrc(const typename S::T* __restrict__ X, const typename S::T* __restrict__ W,
+                                     const GemmRowsParams& p, int m0, int n0, int lane, int wave) {
+    using T = typename S::T;
+    constexpr int NS = S::STAGES, PW = S::V2_PER_WAVE;
+    static_assert(!KN || (sizeof(T) == 2 && S::TN % 128 == 0 && !PERM), "K x N ring: bf16, TN % 128 == 0");
+    constexpr int KN_RW = S::TN * 2;               // bytes of one k-row of the W part (KN)
+    // Ring slot of stage st: rotated so that the last stage lands in slot
+    // NS-1 and the slots freed during the last iterations are 0, 1, ...
+    rot = (NS - (p.K / S::V2_TK) % NS) % NS;
+#pragma unroll
+    for (int j = 0; j < PW; ++j) {
+      const int row = (wave + j * S::NW) * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ ((row >> 1) & 7);
+      if (row < S::TN) {
+        if constexpr (KN) {
+          const int o = (wave + j * S::NW) * 1024 + lane * 16;   // byte within the W part
+          const int k = o / KN_RW, gc = ((o % KN_RW) >> 4) ^ ((k & 3) << 2);
+          const int n = min(n0 + gc * 8, p.N - 8);
+          src[j] = reinterpret_cast<const char*>(W + (int64_t)k * p.ldw + n);
+        } else {
+          const int n = min(n0 + (PERM ? perm23(row) : row), p.N - 1);
+          src[j] = reinterpret_cast<const char*>(W + (int64_t)n * p.ldw) + c * 16;
+        }
+      } else {
+        const int m = min(m0 + row - S::TN, p.M - 1);
+        src[j] = reinterpret_cast<const char*>(X + (int64_t)m * p.ldx) + c * 16;
+      }
+    }
+    // Bytes between consecutive stages of a load: 128 along k, or (KN W
+    // part) 64 k-rows of W.
+    w_step = KN ? (int64_t)S::V2_TK * p.ldw * (int64_t)sizeof(T) : S::V2_ROWB;
+  }
+  __device__ __forceinline__ char* slot(char* smem, int st) const {
+    return smem + ((st + rot) % S::STAGES) * S::V2_STAGE;
+  }
+  // Load j (of PW) of stage st into its ring slot.
+  __device__ __forceinline__ void issue(char* smem, int wave, int j, int st) const {
+    const bool wpart = (wave + j * S::NW) * 8 < S::TN;
+    dma16(src[j] + (int64_t)st * (wpart ? w_step : (int64_t)S::V2_ROWB), slot(smem, st) + (wave + j * S::NW) * 1024);
+  }
+  // Stages 0 .. NS-2 (the ring's prologue).
+  __device__ __forceinline__ void prologue(char* smem, int wave) const {
+#pragma unroll
+    for (int st = 0; st < S::STAGES - 1; ++st)
+#pragma unroll
+      for (int j = 0; j < S::V2_PER_WAVE; ++j) issue(smem, wave, j, st);
+  }
+};
+
+// pre_issued: the caller has already issued the ring's prologue stages for
+// this tile (RingSrc::prologue with the same arguments), typically at the top
+// of the kernel so that their latency covers the kernel's setup.  Memory
+// operations issued in between only make the vmcnt waits below stricter.
 template <class S, bool STG, bool PERM = false, bool KN = false>
 __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
                                             const typename S::T* __restrict__ X,
                                             const typename S::T* __restrict__ W,
                                             const GemmRowsParams& p, int m0, int n0, int bz,
-                                            char* smem, int lane, int wave, int wm, int wn, bool fold_bias) {
+                                            char* smem, int lane, int wave, int wm, int wn, bool fold_bias,
+                                            bool pre_issued = false) {
   using T = typename S::T;
   acc_init<S, PERM>(acc, p, n0, lane, wn, fold_bias);
 
   constexpr int NS = S::STAGES, PW = S::V2_PER_WAVE;
   const int KT = p.K / S::V2_TK;
-  // Ring slot of stage st: rotated so that the last stage lands in slot NS-1
-  // and the slots freed during the last iterations are 0, 1, ...
-  const int rot = (NS - KT % NS) % NS;
-  static_assert(!KN || (sizeof(T) == 2 && S::TN % 128 == 0 && !PERM), "K x N ring: bf16, TN % 128 == 0");
   constexpr int KN_RW = S::TN * 2;                 // bytes of one k-row of the W part (KN)
-  const char* src[PW];
-#pragma unroll
-  for (int j = 0; j < PW; ++j) {
-    const int row = (wave + j * S::NW) * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ ((row >> 1) & 7);
-    if (row < S::TN) {
-      if constexpr (KN) {
-        const int o = (wave + j * S::NW) * 1024 + lane * 16;   // byte within the W part
-        const int k = o / KN_RW, gc = ((o % KN_RW) >> 4) ^ ((k & 3) << 2);
-        const int n = min(n0 + gc * 8, p.N - 8);
-        src[j] = reinterpret_cast<const char*>(W + (int64_t)k * p.ldw + n);
-      } else {
-        const int n = min(n0 + (PERM ? perm23(row) : row), p.N - 1);
-        src[j] = reinterpret_cast<const char*>(W + (int64_t)n * p.ldw) + c * 16;
-      }
-    } else {
-      const int m = min(m0 + row - S::TN, p.M - 1);
-      src[j] = reinterpret_cast<const char*>(X + (int64_t)m * p.ldx) + c * 16;
-    }
-  }
-  // Bytes between consecutive stages of a load: 128 along k, or (KN W part)
-  // 64 k-rows of W.
-  const int64_t w_step = KN ? (int64_t)S::V2_TK * p.ldw * (int64_t)sizeof(T) : S::V2_ROWB;
-  auto slot = [&](int st) { return smem + ((st + rot) % NS) * S::V2_STAGE; };
-  auto dma = [&](int j, int st) {
-    const bool wpart = (wave + j * S::NW) * 8 < S::TN;
-    dma16(src[j] + (int64_t)st * (wpart ? w_step : (int64_t)S::V2_ROWB), slot(st) + (wave + j * S::NW) * 1024);
-  };
+  const RingSrc<S, PERM, KN> ring(X, W, p, m0, n0, lane, wave);
+  auto slot = [&](int st) { return ring.slot(smem, st); };
+  auto dma = [&](int j, int st) { ring.issue(smem, wave, j, st); };
   // Epilogue staging loads: residual rows (part 0: rows [0, RA) into slot 0,
   // part 1: rows [RA, TM) into slot 1) with the 16-byte chunk of column group
   // c of row r stored at chunk position c ^ (r & 7); and one vector region per
@@ -405,10 +438,7 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
   };
   constexpr int NFR = S::BN + S::BM;               // fragments per step
 
-#pragma unroll
-  for (int st = 0; st < NS - 1; ++st)
-#pragma unroll
-    for (int j = 0; j < PW; ++j) dma(j, st);
+  if (!pre_issued) ring.prologue(smem, wave);
   wait_vmcnt<PW * (NS - 2)>();
   lds_barrier();
 #pragma unroll
@@ -1358,7 +1388,14 @@ __device__ __forceinline__ void epilogue_plain(f32x16_t (&x)[S::BM][S::BN], cons
 //       2 = the same pipeline for bf16 W stored K x N (N a multiple of 8).
 // EPI:  0 = plain epilogue (alpha, bias, store), 1 = row-subgraph epilogue
 //       (whole rows or row clusters), 2 = the split-N GEMM pass.
-template <class S, int LOOP, int EPI>
+// PERSIST: workgroups loop over row-block slots (the row-cluster path when
+//       the co-resident grid is smaller than the tile count).  Otherwise each
+//       workgroup runs one tile and there is no tile loop, so the compiler
+//       has no loop to hoist the epilogue's setup out of: hoisted, that setup
+//       ran before the first operand load and was parked in AGPRs and spilled
+//       SGPR lanes until the epilogue (measured at the BERT-base post-norm
+//       shape: 22.3 us with the loop against 21.0 us without).
+template <class S, int LOOP, int EPI, bool PERSIST = false>
 __global__ __launch_bounds__(S::NT, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_rows_kernel(GemmRowsParams p) {
   using T = typename S::T;
@@ -1378,20 +1415,25 @@ void gemm_rows_kernel(GemmRowsParams p) {
   const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
   const bool grouped = p.mode != ROWS_CLUSTER;
   const int q = local / p.cn;
-  for (int it = 0;; ++it) {
-    int rb, c;
+  // Tile (row block rb, column tile c) of iteration it; false when done.
+  auto tile_at = [&](int it, int& rb, int& c) {
     if (grouped) {
       const int R = (p.num_rb - xcd + 7) / 8;            // row blocks of this XCD
-      if (it > 0 || local >= R * p.cn) break;
+      if (it > 0 || local >= R * p.cn) return false;
       const int span = kTileGroupRows * p.cn;
       const int g0 = local / span * kTileGroupRows, gsz = min(R - g0, kTileGroupRows), w = local % span;
       rb = (g0 + w % gsz) * 8 + xcd;
       c = w / gsz;
     } else {
       rb = (it * p.slots + q) * 8 + xcd;
-      if (rb >= p.num_rb) break;
+      if (rb >= p.num_rb) return false;
       c = local % p.cn;
     }
+    return true;
+  };
+  for (int it = 0; PERSIST || it < 1; ++it) {
+    int rb, c;
+    if (!tile_at(it, rb, c)) break;
     int m0 = rb * S::TM, n0 = c * S::TN;
     // Opaque copies of the tile origin and lane ids for this iteration: the
     // epilogue's addresses and column masks would otherwise be hoisted out of
@@ -1422,11 +1464,21 @@ void gemm_rows_kernel(GemmRowsParams p) {
   }
 }
 
+// The persistent form of an instantiation: only 128-row tiles with the row
+// subgraph run the row-cluster path; every other entry runs one tile per
+// workgroup and names its one-tile kernel again.
+template <class S, int LOOP, int EPI>
+inline const void* gemm_persist_fn() {
+  if constexpr (EPI == 1 && S::TM == 128) return reinterpret_cast<const void*>(&gemm_rows_kernel<S, LOOP, EPI, true>);
+  else return reinterpret_cast<const void*>(&gemm_rows_kernel<S, LOOP, EPI, false>);
+}
+
 // Registry entry of one instantiation: <tile shape S, main loop, epilogue>.
 #define CF_GEMM_ENTRY(S, LOOP, EPI)                                                                  \
   GemmKernel {                                                                                       \
     S::TM, S::TN, std::is_same<typename S::T, float>::value ? 1 : 0, LOOP, EPI, S::NT, S::STAGES,    \
-        reinterpret_cast<const void*>(&gemm_rows_kernel<S, LOOP, EPI>)                               \
+        reinterpret_cast<const void*>(&gemm_rows_kernel<S, LOOP, EPI, false>),                       \
+        gemm_persist_fn<S, LOOP, EPI>()                                                              \
   }
 
 }  // namespace cf

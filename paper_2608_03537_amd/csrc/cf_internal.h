@@ -115,7 +115,8 @@ struct RowKernelParams {
 struct GemmKernel {
   int tm, tn, in_f32, loop, epi, threads;
   int stages;   // direct-to-LDS ring depth (needs K / k_per_stage >= stages - 1); 0 for other loops
-  const void* fn;
+  const void* fn;           // one tile per workgroup
+  const void* fn_persist;   // workgroups loop over row-block slots (row-cluster path with a capped grid)
 };
 const GemmKernel* gemm_kernels_v2(int* n);     // direct-to-LDS pipeline
 const GemmKernel* gemm_kernels_v1(int* n);     // register-staged, any layout
