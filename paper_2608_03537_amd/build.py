@@ -44,6 +44,14 @@ FILE_FLAGS = {f: ["-mllvm", "-amdgpu-mfma-vgpr-form"]
               for f in ("cf_gemm_inst_v2.hip", "cf_gemm_inst_v1.hip", "cf_gemm_inst_wr.hip", "cf_gemm_inst_split.hip",
                         "cf_gemm_inst_kn.hip",
                         "cf_b2b.hip", "cf_mlp.hip")}
+# The GEMM kernels' one atomic (a row-cluster round counter, added by lane 0
+# at the start of a tile) returns a value needed only after the main loop.
+# LLVM's atomic optimizer rewrites it as a wave-wide reduction and broadcasts
+# the result at once, which puts a wait for the atomic's round trip in front
+# of the first operand loads.
+for _f in ("cf_gemm_inst_v2.hip", "cf_gemm_inst_v1.hip", "cf_gemm_inst_wr.hip", "cf_gemm_inst_split.hip",
+           "cf_gemm_inst_kn.hip"):
+    FILE_FLAGS[_f] = FILE_FLAGS[_f] + ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]
 
 
 def _compile(src):
