@@ -67,7 +67,8 @@ struct TileShape {
   static constexpr int B_PT = (B_CHUNKS + NT - 1) / NT;
   static constexpr int LDS_STORE = TM * (TN * 4 + 16);   // staged output tile (fp32 worst case)
   // Row-reduction scratch sits at the end of LDS, past the staged output tile.
-  static constexpr int RED_BYTES = 3 * WN * TM * 4, TAIL_BYTES = RED_BYTES;   // (count, mean, M2) per row and wave column
+  // (count, mean, M2) per row and wave column, then the row-cluster round tag
+  static constexpr int RED_BYTES = 3 * WN * TM * 4, TAIL_BYTES = RED_BYTES + 16;
   static constexpr int SMEM_V1 = LDS_V1 > LDS_STORE + TAIL_BYTES ? LDS_V1 : LDS_STORE + TAIL_BYTES;
   static constexpr int SMEM_V2 = LDS_V2 > LDS_STORE + TAIL_BYTES ? LDS_V2 : LDS_STORE + TAIL_BYTES;
   static_assert(SMEM_V1 <= 160 * 1024 && SMEM_V2 <= 160 * 1024, "LDS budget");
@@ -361,17 +362,12 @@ struct RingSrc {
   }
 };
 
-// pre_issued: the caller has already issued the ring's prologue stages for
-// this tile (RingSrc::prologue with the same arguments), typically at the top
-// of the kernel so that their latency covers the kernel's setup.  Memory
-// operations issued in between only make the vmcnt waits below stricter.
 template <class S, bool STG, bool PERM = false, bool KN = false>
 __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
                                             const typename S::T* __restrict__ X,
                                             const typename S::T* __restrict__ W,
                                             const GemmRowsParams& p, int m0, int n0, int bz,
-                                            char* smem, int lane, int wave, int wm, int wn, bool fold_bias,
-                                            bool pre_issued = false) {
+                                            char* smem, int lane, int wave, int wm, int wn, bool fold_bias) {
   using T = typename S::T;
   acc_init<S, PERM>(acc, p, n0, lane, wn, fold_bias);
 
@@ -438,7 +434,7 @@ __device__ __forceinline__ void mainloop_v2(f32x16_t (&acc)[S::BM][S::BN],
   };
   constexpr int NFR = S::BN + S::BM;               // fragments per step
 
-  if (!pre_issued) ring.prologue(smem, wave);
+  ring.prologue(smem, wave);
   wait_vmcnt<PW * (NS - 2)>();
   lds_barrier();
 #pragma unroll
@@ -617,12 +613,17 @@ __device__ __forceinline__ void wg_stat_reduce(float (&n)[S::BM], float (&mean)[
 // Level 3, ROWS_CLUSTER: the cn workgroups of a row block exchange per-row
 // partials through records in the workspace header.
 //
-// Rounds.  Every wave adds kArriveUnit / (cn * NW) to its peer group's counter
-// when it starts a tile (round_tag), so a round adds exactly kArriveUnit and
-// old / kArriveUnit numbers the round, identically in all its waves.  A wave
-// waits for that add to return before its workgroup's first epilogue barrier,
-// so all adds of a round have landed before any record of the round can be
-// seen, and the next round's adds see the next round number.
+// Rounds.  One wave of every workgroup adds kArriveUnit / cn to its peer
+// group's counter once per tile (round_begin), so a round adds exactly
+// kArriveUnit and old / kArriveUnit numbers the round, identically in every
+// workgroup of the group.  The add goes out after the main loop (the loop's
+// waits count memory operations in issue order); the adding wave waits for
+// its return and leaves the round number in LDS before the workgroup's first
+// epilogue barrier (the other waves read it after that barrier).  So all adds
+// of a round have landed before any record of the round can be seen, and the
+// next round's adds see the next round number.  One add per workgroup rather
+// than per wave: adds to one address are serialised, and sixteen of them per
+// round were measured at about 2 us.
 //
 // Records.  record(stage, parity, slot, peer, row) holds one or two 64-bit
 // words, each a 32-bit value with the round number + 1 in its upper half.  A
@@ -642,19 +643,18 @@ __device__ __forceinline__ void wg_stat_reduce(float (&n)[S::BM], float (&mean)[
 // and moves on; every later wait sees the word and gives up at once, so a
 // broken launch ends quickly.  The host reads and clears the word
 // (cf_workspace_check); results of a call that set it are invalid.
-__device__ __forceinline__ unsigned long long round_begin(const GemmRowsParams& p, int slot, int lane, int nw) {
+// The group's add for this workgroup (lane 0 of wave 0; 0 elsewhere).
+__device__ __forceinline__ unsigned long long round_begin(const GemmRowsParams& p, int slot, int lane, int wave) {
   unsigned long long old = 0;
-  if (lane == 0)
-    old = __hip_atomic_fetch_add(p.ws_arrive + slot, kArriveUnit / (unsigned long long)(p.cn * nw),
-                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (wave == 0 && lane == 0)
+    old = __hip_atomic_fetch_add(p.ws_arrive + slot, kArriveUnit / (unsigned long long)p.cn, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
   return old;
 }
 
-// Tag of the round whose counter value `old` lane 0 of this wave received.
+// Tag of the round whose counter value `old` the adding lane received.
 __device__ __forceinline__ unsigned round_tag(unsigned long long old) {
-  const unsigned lo = __builtin_amdgcn_readfirstlane((unsigned)old);
-  const unsigned hi = __builtin_amdgcn_readfirstlane((unsigned)(old >> 32));
-  return (unsigned)((((unsigned long long)hi << 32) | lo) / kArriveUnit) + 1u;
+  return (unsigned)(old / kArriveUnit) + 1u;
 }
 
 __device__ __forceinline__ unsigned long long rec_word(float v, unsigned tag) {
@@ -932,12 +932,26 @@ __device__ __forceinline__ void epi_prefetch(EpiPrefetch<S>& pf, const GemmRowsP
 // (mean, M2) for the finish pass (nothing else is compiled in).
 template <class S, bool STG, bool SPLIT>
 __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiPrefetch<S>& pf,
-                                         const GemmRowsParams& p, int m0, int n0, int slot, int c, unsigned tag,
-                                         int bz, char* smem, float* red, int tid, int lane, int wm, int wn) {
+                                         const GemmRowsParams& p, int m0, int n0, int slot, int c,
+                                         unsigned long long round_old, int bz, char* smem, float* red, int tid,
+                                         int lane, int wm, int wn) {
   using T = typename S::T;
   const RowEpi& e = p.epi;
   const int M = p.M, N = p.N;
   const int lr = lane & 31, lg = lane >> 5;
+  // The round tag (row clusters): the adding lane leaves it in LDS before the
+  // workgroup's first barrier (the round protocol needs the add returned by
+  // then; the work before that barrier covers its round trip), and every wave
+  // reads it after that barrier.
+  unsigned* tag_lds = reinterpret_cast<unsigned*>(red) + S::RED_BYTES / 4;
+  bool tag_sent = false;
+  auto send_tag = [&] {
+    if (!tag_sent) {
+      if (wm == 0 && wn == 0 && lane == 0) *tag_lds = round_tag(round_old);
+      tag_sent = true;
+    }
+  };
+  auto tag = [&] { return __builtin_amdgcn_readfirstlane(*tag_lds); };
   // Staged vector v (0 bias, 1 gamma, 2 beta) at tile column cl.
   auto vec_lds = [&](int v, int cl) {
     return *reinterpret_cast<const f32x4_t*>(smem + S::STG_RA * S::TN * 2 + v * 1024 + cl * 4);
@@ -1112,6 +1126,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     };
     if (n0 + S::TN <= N) lane_stats(std::false_type{});
     else lane_stats(std::true_type{});
+    send_tag();
     wg_stat_reduce<S>(cnt, mean, m2, red, lane, wm, wn);
 
     if constexpr (SPLIT) {
@@ -1128,7 +1143,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
     }
 
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
-      cluster_exchange<S, MERGE_CHAN>(p, 0, slot, c, tag, mean, m2, lane, wm, wn);
+      cluster_exchange<S, MERGE_CHAN>(p, 0, slot, c, tag(), mean, m2, lane, wm, wn);
       exchanged = true;
     }
 
@@ -1184,13 +1199,14 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
         for (int i = 0; i < 16; ++i) t += x[bm][bn][i] * x[bm][bn][i];
       s[bm] = t;
     }
+    send_tag();
     wg_row_reduce<S, false>(s, red, lane, wm, wn);
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
       // sum of squares: a merge of (mean, M2) pairs (0, s) keeps M2 = sum of s
       float z[S::BM];
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) z[bm] = 0.0f;
-      cluster_exchange<S, MERGE_CHAN>(p, 0, slot, c, tag, z, s, lane, wm, wn);
+      cluster_exchange<S, MERGE_CHAN>(p, 0, slot, c, tag(), z, s, lane, wm, wn);
       exchanged = true;
     }
     const float invN = 1.0f / (float)N;
@@ -1253,6 +1269,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
             for (int q = 0; q < 4; ++q) t = fmaxf(t, x[bm][bn][4 * g + q]);
       mx[bm] = t;
     }
+    send_tag();
     wg_row_reduce<S, true>(mx, red, lane, wm, wn);
 #pragma unroll
     for (int bm = 0; bm < S::BM; ++bm) {
@@ -1278,7 +1295,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
       float mg[S::BM];
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm) mg[bm] = mx[bm];
-      cluster_exchange<S, MERGE_SOFTMAX>(p, 0, slot, c, tag, mg, sm, lane, wm, wn);
+      cluster_exchange<S, MERGE_SOFTMAX>(p, 0, slot, c, tag(), mg, sm, lane, wm, wn);
       exchanged = true;
 #pragma unroll
       for (int bm = 0; bm < S::BM; ++bm)
@@ -1296,6 +1313,7 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
   }
   if (e.Y) {
     char* Yb = reinterpret_cast<char*>(e.Y) + (int64_t)bz * e.sy * (e.y_f32 ? 4 : 2);
+    send_tag();
     if constexpr (STG) __syncthreads();   // staged vectors are no longer read
     store_tile_staged<S>(x, Yb, e.ldy, e.y_f32, M, N, m0, n0, smem, tid, lane, wm, wn);
   }
@@ -1315,9 +1333,10 @@ __device__ __forceinline__ void epilogue(f32x16_t (&x)[S::BM][S::BN], const EpiP
             for (int q = 0; q < 4; ++q) t = fmaxf(t, fabsf(x[bm][bn][4 * g + q]));
       a[bm] = t;
     }
+    send_tag();
     wg_row_reduce<S, true>(a, red, lane, wm, wn);
     if (p.mode == ROWS_CLUSTER && p.cn > 1) {
-      cluster_exchange<S, MERGE_MAX>(p, exchanged ? 1 : 0, slot, c, tag, a, a, lane, wm, wn);
+      cluster_exchange<S, MERGE_MAX>(p, exchanged ? 1 : 0, slot, c, tag(), a, a, lane, wm, wn);
       exchanged = true;
     }
 #pragma unroll
@@ -1445,20 +1464,15 @@ void gemm_rows_kernel(GemmRowsParams p) {
     EpiPrefetch<S> pf;
     const bool cluster = EPI == 1 && p.mode == ROWS_CLUSTER && p.cn > 1;
     unsigned long long round_old = 0;
-    if (cluster) round_old = round_begin(p, q * 8 + xcd, lane, S::NW);
     if constexpr (EPI >= 1 && !STG) epi_prefetch<S>(pf, p, m0, n0, bz, lane, wm, wn);
     // The bias enters the accumulators unless alpha scales the product.
     const bool fold_bias = p.epi.bias != nullptr && p.epi.alpha == 1.0f;
-    if constexpr (LOOP >= 1)
-      mainloop_v2<S, STG, false, LOOP == 2>(acc, X, W, p, m0, n0, bz, smem, lane, wave, wm, wn, fold_bias);
+    if constexpr (LOOP >= 1) mainloop_v2<S, STG, false, LOOP == 2>(acc, X, W, p, m0, n0, bz, smem, lane, wave, wm, wn, fold_bias);
     else mainloop<S>(acc, X, W, p, m0, n0, smem, tid, lane, wm, wn, fold_bias);
-    unsigned tag = 0;
-    if (cluster) {
-      tag = round_tag(round_old);
-      asm volatile("" ::"s"(tag) : "memory");   // this wave's add has returned before any epilogue barrier
-    }
+    // The round counter's add goes out after the main loop (see cluster_exchange).
+    if (cluster) round_old = round_begin(p, q * 8 + xcd, lane, wave);
     if constexpr (EPI >= 1)
-      epilogue<S, STG, EPI == 2>(acc, pf, p, m0, n0, q * 8 + xcd, c, tag, bz, smem, red, tid_t, lane_t, wm, wn);
+      epilogue<S, STG, EPI == 2>(acc, pf, p, m0, n0, q * 8 + xcd, c, round_old, bz, smem, red, tid_t, lane_t, wm, wn);
     else epilogue_plain<S>(acc, p, m0, n0, bz, smem, tid_t, lane_t, wm, wn);
     __syncthreads();
   }
