@@ -164,6 +164,20 @@ def test_chain_full_size_sampled_rows(path):
     assert np.all(np.max(np.abs(O.e4m3_decode(Qg[::97])), axis=1) == 448.0)
 
 
+def test_chain_cluster_capped_grid_uneven_rounds():
+    """Row clusters of 16 peers (N = 4096 in 256-wide tiles) at M = 3072: 24 row
+    blocks, but only 2 slots per XCD fit the device, so the workgroups loop
+    (the persistent kernel form) and the slots of an XCD run different numbers
+    of rounds (row blocks 0..15 in the first, 16..23 in the second).  Every
+    row is compared."""
+    inp = I.postnorm_inputs(3072, 128, 4096, "bf16", seed=21, with_affine=False)
+    Zg, sg, Qg = run_chain(inp, path=2)
+    z, s, q = O.ln_gelu_amax(inp.X, inp.W, inp.bias, inp.R, eps=inp.eps)
+    assert_close_bf16(Zg, z, "cluster 3072x4096 capped grid")
+    np.testing.assert_allclose(sg, s, rtol=1e-3)
+    check_codes(Qg, q)
+
+
 @pytest.mark.parametrize("norm", ["rms", "ln_relu"])
 def test_other_stage_stream_patterns(norm):
     # MatMul-BiasAdd-RMSNorm and MatMul-BiasAdd-LayerNorm-ReLU (Sec. VI).
