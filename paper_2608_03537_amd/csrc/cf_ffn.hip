@@ -174,11 +174,24 @@ void b2b_ffn_kernel(B2BParams p) {
   auto o1 = [&](int u) { return (32 * h + lr) * 128 + ((((u << 1) | lg) ^ sw) << 4); };
   auto o2 = [&](int e, int s2) { return lr * 128 + (((4 * e + 2 * s2 + lg) ^ sw) << 4); };
 
-  // X^T fragments of this pair's 32 rows: xf[ks] = X[m][16 ks + 8 lg .. +8].
-  const bf16_t* xrow = X + (int64_t)min(m, p.M - 1) * p.ldx + 8 * lg;
-  u32x4_t xf[F::KS1];
+  // The X tile goes to LDS first, through the second product's weight ring
+  // (free until round 0's W2^T loads, issued after every wave has read its
+  // fragments): whole rows by wave-wide direct loads, so every 128-byte line
+  // of X is fetched once, in full.  Row r, 16-byte chunk c sits at chunk
+  // position c ^ (r & XSW) of its 2D-byte LDS row; one load fills 1 KB =
+  // 1024 / (2D) rows, lane i the position i % (D / 8) of row i / (D / 8).
+  constexpr int XCPR = D / 8;                       // 16-byte chunks per X row
+  constexpr int XSW = (XCPR < 16 ? XCPR : 16) - 1;  // swizzle mask
+  constexpr int XLOADS = F::TM * XCPR / 64 / F::NW; // wave-wide loads per wave
+  static_assert(F::TM * 2 * D == 2 * F::W2S && (F::TM * XCPR) % (64 * F::NW) == 0, "X staging");
 #pragma unroll
-  for (int ks = 0; ks < F::KS1; ++ks) xf[ks] = gload16(xrow + 16 * ks);
+  for (int j = 0; j < XLOADS; ++j) {
+    const int ld = wave * XLOADS + j;
+    const int r = (ld * 64 + lane) / XCPR, cp = lane % XCPR;
+    const int c = cp ^ (r & XSW);
+    dma16(X + (int64_t)min(m0 + r, p.M - 1) * p.ldx + 8 * c, smem + F::OFF_W2 + ld * 1024);
+  }
+  u32x4_t xf[F::KS1];   // X^T fragments, read from LDS in the prologue below
 
   // O accumulators start at b2 (element i of block b: column 32 b + 8 (i/4) + 4 lg + i%4).
   f32x16_t Oa[F::B2H];
@@ -221,25 +234,6 @@ void b2b_ffn_kernel(B2BParams p) {
   };
 
   issue(0, true, 0, false);
-
-  // Residual R = X: O^T += I X^T, one MFMA per (block, k step) with an
-  // identity fragment as A (exact: the products are x * 1 and x * 0).
-  const bool r_is_x = p.R == p.X && p.ldr == p.ldx && (p.batch == 1 || p.sr == p.sx);
-  if (p.R && r_is_x) {
-    u32x4_t id[2];
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int j = lr - 16 * e - 8 * lg;   // position of the 1 in this lane's 8 k values
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-        id[e][w] = (j == 2 * w ? 0x3F80u : 0u) | (j == 2 * w + 1 ? 0x3F800000u : 0u);
-    }
-#pragma unroll
-    for (int b = 0; b < F::B2H; ++b) {   // block nb0 + b takes X fragments 2 (nb0 + b) and 2 (nb0 + b) + 1
-      Mma<bf16_t>::run(Oa[b], id[0], h ? xf[2 * (F::B2H + b)] : xf[2 * b]);
-      Mma<bf16_t>::run(Oa[b], id[1], h ? xf[2 * (F::B2H + b) + 1] : xf[2 * b + 1]);
-    }
-  }
 
   // One pipeline round t: the first product of this half's chunk of round
   // t+1 (into Pn, if ONE), the second product of both chunks of round t-1
@@ -340,6 +334,32 @@ void b2b_ffn_kernel(B2BParams p) {
   // Prologue: the first product of round 0, then round 0 (no second product yet).
   wait_vmcnt<0>();
   __syncthreads();
+  // X^T fragments of this pair's 32 rows: xf[ks] = X[m][16 ks + 8 lg .. +8].
+  {
+    const int r = pr * 32 + lr;
+    const char* xr = smem + F::OFF_W2 + r * 2 * D;
+#pragma unroll
+    for (int ks = 0; ks < F::KS1; ++ks) xf[ks] = lds_read16(xr + (((2 * ks + lg) ^ (r & XSW)) << 4));
+  }
+  // Residual R = X: O^T += I X^T, one MFMA per (block, k step) with an
+  // identity fragment as A (exact: the products are x * 1 and x * 0).
+  const bool r_is_x = p.R == p.X && p.ldr == p.ldx && (p.batch == 1 || p.sr == p.sx);
+  if (p.R && r_is_x) {
+    u32x4_t id[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int j = lr - 16 * e - 8 * lg;   // position of the 1 in this lane's 8 k values
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        id[e][w] = (j == 2 * w ? 0x3F80u : 0u) | (j == 2 * w + 1 ? 0x3F800000u : 0u);
+    }
+#pragma unroll
+    for (int b = 0; b < F::B2H; ++b) {   // block nb0 + b takes X fragments 2 (nb0 + b) and 2 (nb0 + b) + 1
+      Mma<bf16_t>::run(Oa[b], id[0], h ? xf[2 * (F::B2H + b)] : xf[2 * b]);
+      Mma<bf16_t>::run(Oa[b], id[1], h ? xf[2 * (F::B2H + b) + 1] : xf[2 * b + 1]);
+    }
+  }
+
   if (F::NR > 1) issue(1, true, 0, false);
   iter(-1, T_{}, F_{}, F_{});
   Pc = Pn;
