@@ -190,26 +190,33 @@ void b2b_mlp_kernel(B2BParams p) {
   __syncthreads();
 
   // ---- Epi2 (commit) over the row-major tile: thread t handles the column
-  // pairs (t + 256 j) % 64 of rows (t + 256 j) / 64, so every wave-wide access
-  // covers one whole row: 512 contiguous bytes of partials, 256 of O.
-  constexpr int PAIRS = S::TM * N2 / 2 / S::NT;       // column pairs per thread
-  auto pair_lds = [&](int j) {
-    const int id = tid + j * S::NT, r = id / (N2 / 2), c2 = id % (N2 / 2);
-    return *reinterpret_cast<const float2*>(pt_at(r, c2 / 2) + (c2 & 1) * 8);
-  };
+  // quad (t + 256 j) % QPR of row (t + 256 j) / QPR, so every wave-wide
+  // access covers two whole rows: 1 KB of partials, 512 bytes of O.
+  // The partials go through memory with device-coherent 16-byte accesses
+  // (sc1): the workgroups of a row block need not share an XCD, and the
+  // reader reads only after the writer's stores completed (arrival count).
+  constexpr int QPR = N2 / 4;                          // column quads per row
+  constexpr int QUADS = S::TM * QPR / S::NT;           // quads per thread
+  static_assert(S::NT % QPR == 0, "a thread's column quad is the same in every step");
+  constexpr int kSc1 = 16;                             // cache policy: device-coherent
+  const int q4 = tid % QPR;
+  auto quad_lds = [&](int j) { return *reinterpret_cast<const f32x4_t*>(pt_at((tid + j * S::NT) / QPR, q4)); };
   float* part = p.ws_part + (int64_t)bz * cn * p.M * N2;
+  const int rows = min(S::TM, p.M - m0);
+  // Buffer resource over chunk k's partial rows [m0, m0 + rows): raw 32-bit
+  // data; accesses past its end are dropped (stores) or read as 0 (loads).
+  auto part_rsrc = [&](int k) {
+    return __builtin_amdgcn_make_buffer_rsrc(part + ((int64_t)k * p.M + m0) * N2, 0, rows * N2 * 4, 0x00020000);
+  };
   if (cn > 1) {
-    // publish O_c with agent-scope stores, then count this workgroup's arrival
-    unsigned long long* mine = reinterpret_cast<unsigned long long*>(part + (int64_t)c * p.M * N2);
+    // publish O_c, then count this workgroup's arrival
+    const auto mine = part_rsrc(c);
 #pragma unroll 8
-    for (int j = 0; j < PAIRS; ++j) {
-      const int id = tid + j * S::NT, r = id / (N2 / 2), c2 = id % (N2 / 2);
-      if (m0 + r < p.M) {
-        const float2 v = pair_lds(j);
-        __hip_atomic_store(mine + ((int64_t)(m0 + r) * N2) / 2 + c2,
-                           ((unsigned long long)__float_as_uint(v.y) << 32) | __float_as_uint(v.x),
-                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
+    for (int j = 0; j < QUADS; ++j) {
+      const int r = (tid + j * S::NT) / QPR;
+      if (r < rows)
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, quad_lds(j)), mine, (r * QPR + q4) * 16, 0,
+                                               kSc1);
     }
     wait_vmcnt<0>();          // this wave's partial stores have completed
     __syncthreads();          // ... and every wave's
@@ -226,48 +233,50 @@ void b2b_mlp_kernel(B2BParams p) {
 
   // O = O_0 + O_1 + ... (chunk order, whichever workgroup finished last; its
   // own partial comes from LDS, equal to what it stored) + b2, output ReLU,
-  // bf16 rows.  A thread's column pair is the same in every step (256 threads
-  // cover whole rows), so b2 is read once; the other chunks' partials are
-  // loaded for all steps before any is used, so their latencies overlap.
+  // bf16 rows.  A thread's column quad is the same in every step, so b2 is
+  // read once; the other chunks' partials are loaded for all steps before
+  // any is used, so their latencies overlap.
   uint16_t* O = p.O + (int64_t)bz * p.so;
-  const int c2 = tid % (N2 / 2);
-  float2 bb = make_float2(0.0f, 0.0f);
-  if (p.b2) bb = *reinterpret_cast<const float2*>(p.b2 + 2 * c2);
-  float2 t[PAIRS];
+  f32x4_t bb = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (p.b2) bb = *reinterpret_cast<const f32x4_t*>(p.b2 + 4 * q4);
+  f32x4_t t[QUADS];
 #pragma unroll
-  for (int j = 0; j < PAIRS; ++j) t[j] = pair_lds(j);
+  for (int j = 0; j < QUADS; ++j) t[j] = quad_lds(j);
   if (cn > 1) {
-    float2 acc2[PAIRS];
+    f32x4_t acc2[QUADS];
     for (int k = 0; k < cn; ++k) {
       if (k == c) {
 #pragma unroll
-        for (int j = 0; j < PAIRS; ++j) acc2[j] = k == 0 ? t[j] : make_float2(acc2[j].x + t[j].x, acc2[j].y + t[j].y);
+        for (int j = 0; j < QUADS; ++j) acc2[j] = k == 0 ? t[j] : acc2[j] + t[j];
         continue;
       }
-      unsigned long long w[PAIRS];
-      const unsigned long long* src = reinterpret_cast<const unsigned long long*>(part + (int64_t)k * p.M * N2);
+      const auto src = part_rsrc(k);
+      u32x4_t w[QUADS];
 #pragma unroll
-      for (int j = 0; j < PAIRS; ++j) {
-        const int m = min(m0 + (tid + j * S::NT) / (N2 / 2), p.M - 1);
-        w[j] = __hip_atomic_load(src + ((int64_t)m * N2) / 2 + c2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int j = 0; j < QUADS; ++j) {
+        const int r = min((tid + j * S::NT) / QPR, rows - 1);
+        w[j] = __builtin_amdgcn_raw_buffer_load_b128(src, (r * QPR + q4) * 16, 0, kSc1);
       }
 #pragma unroll
-      for (int j = 0; j < PAIRS; ++j) {
-        const float2 v = make_float2(__uint_as_float((unsigned)w[j]), __uint_as_float((unsigned)(w[j] >> 32)));
-        acc2[j] = k == 0 ? v : make_float2(acc2[j].x + v.x, acc2[j].y + v.y);
+      for (int j = 0; j < QUADS; ++j) {
+        const f32x4_t v = __builtin_bit_cast(f32x4_t, w[j]);
+        acc2[j] = k == 0 ? v : acc2[j] + v;
       }
     }
 #pragma unroll
-    for (int j = 0; j < PAIRS; ++j) t[j] = acc2[j];
+    for (int j = 0; j < QUADS; ++j) t[j] = acc2[j];
   }
 #pragma unroll
-  for (int j = 0; j < PAIRS; ++j) {
-    const int m = m0 + (tid + j * S::NT) / (N2 / 2);
+  for (int j = 0; j < QUADS; ++j) {
+    const int m = m0 + (tid + j * S::NT) / QPR;
     if (m >= p.M) continue;
-    float2 y = t[j];
-    if (p.b2) y = make_float2(y.x + bb.x, y.y + bb.y);
-    if (p.out_relu) y = make_float2(fmaxf(y.x, 0.0f), fmaxf(y.y, 0.0f));
-    __builtin_nontemporal_store(pack_bf16x2(y.x, y.y), reinterpret_cast<uint32_t*>(O + (int64_t)m * p.ldo + 2 * c2));
+    f32x4_t y = t[j];
+    if (p.b2) y += bb;
+    if (p.out_relu)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = fmaxf(y[e], 0.0f);
+    const u32x2_t o2 = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
+    __builtin_nontemporal_store(o2, reinterpret_cast<u32x2_t*>(O + (int64_t)m * p.ldo + 4 * q4));
   }
 }
 
