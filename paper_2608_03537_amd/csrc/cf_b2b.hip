@@ -23,25 +23,49 @@
 
 namespace cf {
 
-// Byte offset of 16-byte chunk c of LDS row `row` (128-byte rows, chunk
-// position XOR-swizzled by (row >> 1) & 7; see mainloop_v2).
-__device__ __forceinline__ int swz_off(int row, int c) { return row * 128 + ((c ^ ((row >> 1) & 7)) << 4); }
-
-__device__ __forceinline__ u32x2_t lds_read8(const char* p) { return *reinterpret_cast<const u32x2_t*>(p); }
-
-// A-operand fragment in the permuted k order of step (bl, s) for LDS row
-// `row` of a 128-byte stage row (64 bf16 of the contraction index).
-__device__ __forceinline__ u32x4_t frag_perm(const char* base, int row, int bl, int s, int lg) {
-  const int c0 = 4 * bl + 2 * s;
-  const u32x2_t lo = lds_read8(base + swz_off(row, c0) + 8 * lg);
-  const u32x2_t hi = lds_read8(base + swz_off(row, c0 + 1) + 8 * lg);
-  return u32x4_t{lo[0], lo[1], hi[0], hi[1]};
-}
-
 // Accumulator elements 8s .. 8s+7 of a block, as 8 packed bf16.
 __device__ __forceinline__ u32x4_t pack_step(const f32x16_t& v, int s) {
   return u32x4_t{pack_bf16x2(v[8 * s + 0], v[8 * s + 1]), pack_bf16x2(v[8 * s + 2], v[8 * s + 3]),
                  pack_bf16x2(v[8 * s + 4], v[8 * s + 5]), pack_bf16x2(v[8 * s + 6], v[8 * s + 7])};
+}
+
+// Transposing 8-byte LDS read (ds_read_b64_tr_b16) at LDS byte address
+// addr + OFF, written as inline assembly.  The compiler builtin carries no
+// memory operand, so the compiler's wait insertion assumes it may read bytes
+// that an outstanding direct-to-LDS load is still writing and puts a wait for
+// every such load (vmcnt(0)) in front of it.  The caller knows the stage it
+// reads is not the one being loaded; it waits for the result itself
+// (lgkm_wait), since the compiler does not know this instruction loads.
+template <int OFF>
+__device__ __forceinline__ u32x2_t ds_read_tr_b64(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
+  u32x2_t v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+// 16-byte LDS read at byte address addr + OFF as inline assembly, for the
+// same reason (K rows sit in a stage that direct loads also write); the
+// caller waits for the result.
+template <int OFF>
+__device__ __forceinline__ u32x4_t ds_read_b128_at(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset field");
+  u32x4_t v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+  return v;
+}
+// Wait until at most N LDS operations of this wave are outstanding; v is tied
+// to the wait so that its uses cannot move above it.
+template <int N>
+__device__ __forceinline__ void lgkm_wait(u32x4_t& v) {
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(v) : "i"(N));
+}
+// Calls f(std::integral_constant<int, I>) for I = B .. E-1 in order.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
 }
 
 __device__ __forceinline__ float lane_pair_sum(float v) { return v + __shfl_xor(v, 32); }
@@ -148,37 +172,58 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   const int row0 = wave * RPI + lane / LPR;     // this lane's row in load 0
   const uint32_t kl_off = (uint32_t)((lane / LPR) * p.ldw1 * 2 + (((lane % LPR) ^ kswz(row0)) << 4));
   const uint32_t vl_off = (uint32_t)((lane / LPR) * p.ldw2 * 2 + (((lane % LPR) ^ vswz(row0)) << 4));
-  auto issue_rows = [&](int j, auto stage_t, auto v_t) {
+  constexpr int NINS = A::TN / RPI / 4;   // direct loads per wave for one K or V block
+  // Load ins of this wave for key block j (K, or V when v_t is true) into a
+  // ring stage; `full` (block j lies inside Lk) selects the wave-uniform form.
+  auto issue_one = [&](int j, auto stage_t, auto v_t, int ins, bool full) {
     constexpr bool VS = decltype(v_t)::value;
     char* dst = smem + decltype(stage_t)::value * A::STAGE + (VS ? A::KB : 0);
     const bf16_t* src = VS ? Vp : Kp;
     const int64_t ld = VS ? p.ldw2 : p.ldw1;
-    if ((j + 1) * A::TN <= Lk) {
-#pragma unroll
-      for (int ins = 0; ins < A::TN / RPI / 4; ++ins) {
-        const int in = wave + 4 * ins;
-        const char* base = reinterpret_cast<const char*>(src + (int64_t)(j * A::TN + in * RPI) * ld);
-        dma16(base + (VS ? vl_off : kl_off), dst + in * 1024);
-      }
+    const int in = wave + 4 * ins;
+    if (full) {
+      const char* base = reinterpret_cast<const char*>(src + (int64_t)(j * A::TN + in * RPI) * ld);
+      dma16(base + (VS ? vl_off : kl_off), dst + in * 1024);
     } else {
-#pragma unroll
-      for (int ins = 0; ins < A::TN / RPI / 4; ++ins) {
-        const int in = wave + 4 * ins;
-        const int row = in * RPI + lane / LPR;
-        const int c = (lane % LPR) ^ (VS ? vswz(row) : kswz(row));
-        const int key = min(j * A::TN + row, Lk - 1);
-        dma16(reinterpret_cast<const char*>(src + (int64_t)key * ld) + c * 16, dst + in * 1024);
-      }
+      const int row = in * RPI + lane / LPR;
+      const int c = (lane % LPR) ^ (VS ? vswz(row) : kswz(row));
+      const int key = min(j * A::TN + row, Lk - 1);
+      dma16(reinterpret_cast<const char*>(src + (int64_t)key * ld) + c * 16, dst + in * 1024);
     }
   };
   auto issue_kv = [&](int j, auto stage_t) {
-    issue_rows(j, stage_t, std::false_type{});
-    issue_rows(j, stage_t, std::true_type{});
+    const bool full = (j + 1) * A::TN <= Lk;
+#pragma unroll
+    for (int ins = 0; ins < NINS; ++ins) issue_one(j, stage_t, std::false_type{}, ins, full);
+#pragma unroll
+    for (int ins = 0; ins < NINS; ++ins) issue_one(j, stage_t, std::true_type{}, ins, full);
   };
   auto lds_sync = [] {   // this wave's LDS accesses are done, then a workgroup barrier
     __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14));
     lds_barrier();
   };
+
+  // LDS byte address of K-fragment reads for d step ks (lane row lr of a
+  // 32-key half; the half and the stage are compile-time offsets).  The
+  // swizzle of row 32 h + lr equals that of row lr.
+  uint32_t kbase[A::DK];
+  // LDS byte address of the V^T fragment reads of output block b, less the
+  // stage and key offsets (compile-time constants at each read).  In a group
+  // of 16 lanes, lane r names 4 consecutive d (offset 4 (r % 4)) of key
+  // k0 + r / 4, where k0 = 32 bl + 16 s + 4 lg is a multiple of 4, so the V
+  // swizzle of that key depends on r only.
+  uint32_t vbase[A::BD];
+  {
+    const int r = lane & 15;
+    const int dcol = (lane & 16) + 4 * (r & 3);
+    const int krow = 4 * lg + (r >> 2);
+    const uint32_t s0 = (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) char*)smem);
+#pragma unroll
+    for (int ks = 0; ks < A::DK; ++ks) kbase[ks] = s0 + koff(lr, 2 * ks + lg);
+#pragma unroll
+    for (int b = 0; b < A::BD; ++b)
+      vbase[b] = s0 + krow * A::KROW + ((((32 * b + dcol) >> 3) ^ vswz(krow)) << 4) + 8 * (r & 1);
+  }
 
   f32x16_t Oa[A::BD];
 #pragma unroll
@@ -186,17 +231,13 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) Oa[b][i] = 0.0f;
   float m_used = -INFINITY;
-  // Row sums l of P, accumulated by MFMAs with an all-ones A operand (every
-  // row of the block holds l of query lr), from the same bf16 P as O.
-  f32x16_t Lacc = {};
+  // This lane's part of the row sum l of P (its 32 of each block's keys),
+  // summed from the same bf16 P as the numerator by dot products with
+  // (1, 1); the lane pair's parts are added at the end.
+  float lsum = 0.0f;
 
-  // MFMA i of an S^T block (half i / DK, d step i % DK); its K fragment is
-  // read two slots ahead.
-  auto kfrag = [&](const char* kb, int i) {
-    return lds_read16(kb + koff((i / A::DK) * 32 + lr, 2 * (i % A::DK) + lg));
-  };
-  auto mma_s = [&](f32x16_t (&S)[2], int i, u32x4_t kf) {
-    const int b = i / A::DK, ks = i % A::DK;
+  // One MFMA of an S^T block: 32-key half b, d step ks.
+  auto mma_s = [&](f32x16_t (&S)[2], int b, int ks, u32x4_t kf) {
     const f32x16_t zero = {};
     S[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kf),
                                                    __builtin_bit_cast(bf16x8_t, qf[ks]), ks == 0 ? zero : S[b],
@@ -244,8 +285,7 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
       for (int b = 0; b < A::BD; ++b)
 #pragma unroll
         for (int i = 0; i < 16; ++i) Oa[b][i] *= st.corr;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) Lacc[i] *= st.corr;
+      lsum *= st.corr;
     }
   };
   // O^T += V^T P^T for block j (V^T fragments two MFMAs ahead).  Fragment
@@ -255,49 +295,67 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   // 16 lanes, lane r names 4 consecutive d of key k0 + r / 4 (d offset
   // 4 (r % 4)), and lane i receives the 4 keys of d offset i.
   auto pv_block = [&](auto stage_t, const SoftmaxStep& st) {
-    const char* vt = smem + decltype(stage_t)::value * A::STAGE + A::KB;
-    const int r = lane & 15;
-    const int dcol = (lane & 16) + 4 * (r & 3);       // d within the 32-block named by this lane
-    const int hb = 8 * (r & 1);
-    auto tr_read = [&](int key, int d) {
-      typedef short v4i16 __attribute__((ext_vector_type(4)));
-      const char* a = vt + key * A::KROW + (((d >> 3) ^ vswz(key)) << 4) + hb;
-      const v4i16 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) v4i16*)(a));
-      return __builtin_bit_cast(u32x2_t, v);
-    };
-    auto vfrag = [&](int i) {   // i = (bl * 2 + s) * BD + b
-      const int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
-      const int k0 = 32 * bl + 16 * s + 4 * lg + (r >> 2);
-      const u32x2_t lo = tr_read(k0, 32 * b + dcol);
-      const u32x2_t hi = tr_read(k0 + 8, 32 * b + dcol);
+    constexpr int VT = decltype(stage_t)::value * A::STAGE + A::KB;   // this stage's V rows
+    auto vfrag = [&](auto i_t) {   // i = (bl * 2 + s) * BD + b
+      constexpr int i = decltype(i_t)::value;
+      constexpr int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
+      constexpr int off = VT + (32 * bl + 16 * s) * A::KROW;
+      const u32x2_t lo = ds_read_tr_b64<off>(vbase[b]);
+      const u32x2_t hi = ds_read_tr_b64<off + 8 * A::KROW>(vbase[b]);
       return u32x4_t{lo[0], lo[1], hi[0], hi[1]};
     };
     u32x4_t vf[3];
-    vf[0] = vfrag(0);
-    vf[1] = vfrag(1);
-#pragma unroll
-    for (int i = 0; i < A::NSB; ++i) {
-      if (i + 2 < A::NSB) vf[(i + 2) % 3] = vfrag(i + 2);
-      const int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
+    vf[0] = vfrag(std::integral_constant<int, 0>{});
+    vf[1] = vfrag(std::integral_constant<int, 1>{});
+    static_for<0, A::NSB>([&](auto i_t) {
+      constexpr int i = decltype(i_t)::value;
+      constexpr int b = i % A::BD, s = (i / A::BD) & 1, bl = i / (2 * A::BD);
+      // Two reads per fragment and no other LDS operation in between, so
+      // fragment i is complete once at most fragment i + 1's two reads are
+      // outstanding.  Fragment i + 2 is read after MFMA i, into the registers
+      // MFMA i - 1 read.
+      lgkm_wait<(i + 1 < A::NSB ? 2 : 0)>(vf[i % 3]);
       Mma<bf16_t>::run(Oa[b], vf[i % 3], st.P[bl][s]);
+      if constexpr (i + 2 < A::NSB) vf[(i + 2) % 3] = vfrag(std::integral_constant<int, i + 2>{});
       __builtin_amdgcn_sched_barrier(0);
-    }
-    const u32x4_t ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};   // bf16 1.0 x 8
+    });
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const bf16x2_t one2 = __builtin_bit_cast(bf16x2_t, 0x3F803F80u);   // bf16 (1.0, 1.0)
+    // Each packed pair goes through a 32-bit value of its own: with the
+    // vector element written inside the call, the compiler passed the
+    // fragment's first register for all four pairs.
 #pragma unroll
-    for (int q = 0; q < 4; ++q) Mma<bf16_t>::run(Lacc, ones, st.P[q >> 1][q & 1]);
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t x = st.P[q >> 1][q & 1][e];
+        lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, x), one2, lsum, false);
+      }
   };
-  // S^T of block j from its K rows in LDS (K fragments two MFMAs ahead).
-  auto s_block = [&](f32x16_t (&S)[2], auto stage_t) {
-    const char* kb = smem + decltype(stage_t)::value * A::STAGE;
-    u32x4_t kf[3];
-    kf[0] = kfrag(kb, 0);
-    kf[1] = kfrag(kb, 1);
-#pragma unroll
-    for (int i = 0; i < A::NSA; ++i) {
-      if (i + 2 < A::NSA) kf[(i + 2) % 3] = kfrag(kb, i + 2);
-      mma_s(S, i, kf[i % 3]);
-    }
+  // S^T of block j from its K rows in LDS: one 16-byte read per MFMA, KLA
+  // reads ahead; MFMA i takes half i % 2 and d step i / 2, so the two
+  // halves' accumulation chains alternate.  No other LDS operation is issued
+  // in between, so read i is complete once at most the KLA - 1 later ones
+  // are outstanding.
+  auto s_block = [&](f32x16_t (&S)[2], auto stage_t, auto&& after_mma) {
+    constexpr int KST = decltype(stage_t)::value * A::STAGE;
+    constexpr int KLA = 4;
+    auto kread = [&](auto i_t) {
+      constexpr int i = decltype(i_t)::value;
+      constexpr int h = i % 2, ks = i / 2;
+      return ds_read_b128_at<KST + h * 32 * A::KROW>(kbase[ks]);
+    };
+    u32x4_t kf[KLA];
+    static_for<0, KLA>([&](auto i_t) { kf[decltype(i_t)::value] = kread(i_t); });
+    static_for<0, A::NSA>([&](auto i_t) {
+      constexpr int i = decltype(i_t)::value;
+      constexpr int rest = A::NSA - 1 - i;
+      lgkm_wait<(rest < KLA - 1 ? rest : KLA - 1)>(kf[i % KLA]);
+      mma_s(S, i % 2, i / 2, kf[i % KLA]);
+      if constexpr (i + KLA < A::NSA) kf[(i + KLA) % KLA] = kread(std::integral_constant<int, i + KLA>{});
+      after_mma(i_t);
+      __builtin_amdgcn_sched_barrier(0);
+    });
   };
   auto softmax_all = [&](f32x16_t (&Sc)[2], int j, SoftmaxStep& st, auto mask_t) {
 #pragma unroll
@@ -313,15 +371,34 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   // Step j: K(j) and V(j) are in stage j & 1 once every wave has passed the
   // barrier, and every wave is then done with block j-1, so stage (j+1) & 1
   // takes K(j+1) and V(j+1) (direct loads).  Then S^T(j), softmax, rescale
-  // and the P V of block j.  Two workgroups share a
-  // CU, so while one wave of a SIMD runs the softmax the other (from the other
-  // workgroup) can issue MFMAs.  The loop runs two blocks per trip so that the
-  // stage, and with it every LDS offset, is a compile-time constant.
+  // and the P V of block j.  Two workgroups share a CU, so while one wave of
+  // a SIMD runs the softmax the other (from the other workgroup) can issue
+  // MFMAs.  The loop runs two blocks per trip so that the stage, and with it
+  // every LDS offset, is a compile-time constant.
+  // The next block's loads go one after every second MFMA of S^T(j): a
+  // wave's load issue waits while the CU's load path takes earlier loads,
+  // and MFMAs already issued keep the matrix core busy meanwhile (eight
+  // loads in a row at the barrier cost a quarter of the step).
+  static_assert(2 * NINS <= A::NSA / 2, "loads per S^T block");
   auto step = [&](int j, auto stage_t, auto next_t) {
     wait_vmcnt<0>();
     lds_sync();
-    if (j + 1 < NB) issue_kv(j + 1, next_t);
-    s_block(S, stage_t);
+    // Load q of the next block (K for q < NINS, then V) after MFMA 2 q + 1.
+    auto loads = [&](auto full_t) {
+      return [&, full_t](auto i_t) {
+        constexpr int i = decltype(i_t)::value;
+        if constexpr (i % 2 == 1 && i / 2 < 2 * NINS) {
+          constexpr bool VS = i / 2 >= NINS;
+          issue_one(j + 1, next_t, std::integral_constant<bool, VS>{}, VS ? i / 2 - NINS : i / 2,
+                    decltype(full_t)::value);
+        }
+      };
+    };
+    // The three cases are separate code paths so that the common one (the
+    // next block lies inside Lk) keeps its wave-uniform addressing.
+    if (j + 2 < NB || (j + 2 == NB && (j + 2) * A::TN <= Lk)) s_block(S, stage_t, loads(std::true_type{}));
+    else if (j + 1 < NB) s_block(S, stage_t, loads(std::false_type{}));
+    else s_block(S, stage_t, [](auto) {});
     if (j + 1 < NB) softmax_all(S, j, st, std::false_type{});
     else softmax_all(S, j, st, std::true_type{});
     rescale(st);
@@ -333,7 +410,7 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
   }
 
   __syncthreads();
-  const float inv = 1.0f / Lacc[0];
+  const float inv = 1.0f / lane_pair_sum(lsum);
 #pragma unroll
   for (int b = 0; b < A::BD; ++b)
 #pragma unroll

@@ -132,8 +132,9 @@ def test_attention_table2_shapes(which):
 
 def test_attention_invariants():
     a = I.attention_inputs(seed=6, B=1, H=2, Lq=128, Lk=200, d=128)
-    # V = 1: the row sums l and the numerator come from the same bf16 P, so
-    # every output is exactly 1
+    # V = 1: the row sums l and the numerator add the same bf16 P (in fp32,
+    # in different orders), so O / l is within a few fp32 ulps of 1 and every
+    # bf16 output is exactly 1
     ones = run_attn(a.Q, a.K, np.ones_like(a.V))
     assert np.array_equal(ones, np.ones_like(ones)), np.max(np.abs(ones - 1.0))
     zq = run_attn(np.zeros_like(a.Q), a.K, a.V)
