@@ -70,7 +70,22 @@ void b2b_mlp_kernel(B2BParams p) {
   const int wm = wave / S::WN, wn = wave % S::WN;
   const int lr = lane & 31, lg = lane >> 5;
   const int cn = p.cn;
-  const int c = blockIdx.x % cn, rb = blockIdx.x / cn;
+  // XCD-aware order: linear id L runs on XCD L % 8.  In full groups of 8 row
+  // blocks, the cn workgroups of row block 8 i + x are L = 8 (cn i + c) + x:
+  // they share XCD x and run at about the same time, so the row block's X
+  // comes from HBM into that XCD's L2 once for all its chunks.  The rows past
+  // the last full group go in plain order.
+  int c, rb;
+  {
+    const int L = blockIdx.x, full = (int)(gridDim.x / cn) / 8 * 8 * cn;
+    if (L < full) {
+      c = (L >> 3) % cn;
+      rb = (L >> 3) / cn * 8 + (L & 7);
+    } else {
+      c = (L - full) % cn;
+      rb = full / cn + (L - full) / cn;
+    }
+  }
   const int m0 = rb * S::TM, h0 = c * kMlpHidden;
   const int bz = blockIdx.y;
   const bf16_t* X = p.X + (int64_t)bz * p.sx;
