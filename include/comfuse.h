@@ -232,19 +232,22 @@ cf_status cf_gemm_subgraph_noalloc(const cf_subgraph_args* a, void* hip_stream);
  * MLP: W1 given as W1^T (N1 x K, CF_LAYOUT_NK), W2 as W2^T (N2 x N1,
  * CF_LAYOUT_NK); N2 = 128, N1 a multiple of 256, K a multiple of 64 and
  * >= 128; b1 [N1] / b2 [N2] fp32 or NULL; out = CF_OUT_STORE or
- * CF_OUT_BIAS_RELU; R, gamma, beta NULL.  N1 is split into chunks of 256
- * hidden units, one workgroup per chunk and 128-row block (the cross-CTA
- * dataflow of Sec. IV-A); their partial second products are summed at
- * commit, in chunk order, by the last workgroup of the row block to finish.
- * Workspace: 0 bytes for the FFN, attention, and MLP with N1 = 256; for MLP
- * with N1 > 256, cf_b2bgemm_workspace() bytes, 16-byte aligned:
+ * CF_OUT_BIAS_RELU; R, gamma, beta NULL.  N1 is cut into chunks of 256
+ * hidden units and the partial second products of the chunks are summed in
+ * chunk order (the partial-sum identity of Sec. IV-A).  With
+ * batch * ceil(M / 128) >= 256 row blocks, one workgroup per 128-row block
+ * runs all chunks and keeps the sum in registers.  With fewer (and
+ * N1 > 256), the chunks are split over workgroups, one per chunk and row
+ * block (the cross-CTA dataflow of Sec. IV-A), and the last workgroup of a
+ * row block to finish sums their partials at commit.
+ * Workspace: 0 bytes for the FFN, attention, and the MLP unless it splits
+ * the chunks; then cf_b2bgemm_workspace() bytes, 16-byte aligned:
  * CF_B2B_WS_HEADER_BYTES of arrival counters (one 32-bit word per batch
- * entry and 128-row block, so batch * ceil(M / 128) <= 262144, else
- * CF_ERR_SHAPE), then the fp32 partial products.  Zero-fill the header once
- * before the first MLP call; every call leaves it all zero again and the
- * partials never reach into it, so later calls of any shape find it valid.
- * Do not share the workspace with calls of another kind, and do not let
- * calls that share it overlap in time.
+ * entry and 128-row block), then the fp32 partial products.  Zero-fill the
+ * header once before the first MLP call; every call leaves it all zero
+ * again and the partials never reach into it, so later calls of any shape
+ * find it valid.  Do not share the workspace with calls of another kind,
+ * and do not let calls that share it overlap in time.
  * ------------------------------------------------------------------------ */
 typedef enum { CF_MID_GELU_BIAS = 0, CF_MID_SOFTMAX = 1, CF_MID_RELU_BIAS = 2 } cf_mid_op;
 typedef enum { CF_OUT_STORE = 0, CF_OUT_BIAS_RESIDUAL_LN = 1, CF_OUT_BIAS_RELU = 2 } cf_out_op;

@@ -708,18 +708,29 @@ cf_status cf_workspace_check(void* workspace, size_t ws_bytes, void* hip_stream)
   }
 }
 
+// MLP form.  With at least kMlpWholeRowBlocks row blocks (one per CU of a
+// 256-CU device) one workgroup per row block runs all chunks and needs no
+// workspace; below that the hidden chunks are split over workgroups, so the
+// grid still fills the device, and their partial products meet in the
+// workspace.  The rule depends on the arguments only.
+static constexpr int64_t kMlpWholeRowBlocks = 256;
+static bool mlp_split(const cf_b2b_args* a) {
+  return a->N1 > kMlpHidden && a->batch * ((a->M + kMlpRows - 1) / kMlpRows) < kMlpWholeRowBlocks;
+}
+
 // Workspace of the split MLP: the fixed counter region (words [batch][row
 // blocks] at its start), then fp32 partials [batch][cn][M][N2].  The counter
 // region does not depend on the shape, so partials of one call never land
 // where a later call of another shape expects zeroed counters.  Other B2B
 // forms need none.
 static size_t mlp_workspace(const cf_b2b_args* a) {
-  if (!a || a->struct_size != sizeof(cf_b2b_args) || a->mid != CF_MID_RELU_BIAS || a->N1 <= kMlpHidden ||
-      a->M <= 0 || a->batch <= 0)
+  if (!a || a->struct_size != sizeof(cf_b2b_args) || a->mid != CF_MID_RELU_BIAS || a->M <= 0 || a->batch <= 0 ||
+      !mlp_split(a))
     return 0;
   const int64_t cn = a->N1 / kMlpHidden;
   return kMlpCounterBytes + (size_t)(a->batch * cn * a->M * a->N2 * 4);
 }
+static_assert(kMlpWholeRowBlocks <= kMlpMaxRowBlocks, "split MLP counters");
 
 size_t cf_b2bgemm_workspace(const cf_b2b_args* a) {
   try {
@@ -756,9 +767,6 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, voi
       if (a->M > 0 && a->batch > 0) {
         const size_t need = mlp_workspace(a);
         if (need > 0) {
-          if (a->batch * ((a->M + kMlpRows - 1) / kMlpRows) > kMlpMaxRowBlocks)
-            return fail(CF_ERR_SHAPE, "split MLP: batch * ceil(M / %d) exceeds %lld counters", kMlpRows,
-                        (long long)kMlpMaxRowBlocks);
           if (!workspace) return fail(CF_ERR_WORKSPACE, "workspace of %zu bytes required (N1 split over workgroups)", need);
           if (ws_bytes < need) return fail(CF_ERR_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
           if (!aligned16(workspace)) return fail(CF_ERR_ALIGN, "workspace is not 16-byte aligned");
@@ -830,7 +838,7 @@ cf_status cf_b2bgemm(const cf_b2b_args* a, void* workspace, size_t ws_bytes, voi
     hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
     if (mlp) {
       p.out_relu = a->out == CF_OUT_BIAS_RELU;
-      p.cn = (int)(a->N1 / kMlpHidden);
+      p.cn = mlp_split(a) ? (int)(a->N1 / kMlpHidden) : 1;
       if (p.cn > 1) {
         char* b = reinterpret_cast<char*>(workspace);
         p.ws_count = reinterpret_cast<unsigned*>(b);

@@ -145,7 +145,7 @@ struct B2BParams {
   // MLP (S = ReLU(P + b1)): output ReLU, and the split of N1 over cn
   // workgroups whose partial second products are summed at commit
   int out_relu;
-  int cn;                                  // workgroups per row block (N1 / 256)
+  int cn;                                  // workgroups per row block: N1 / 256 (split), or 1 (whole)
   unsigned* ws_count;                      // [batch][row blocks] arrival counters (zero between calls)
   float* ws_part;                          // [batch][cn][M][N2] fp32 partial products
 };

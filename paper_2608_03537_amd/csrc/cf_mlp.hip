@@ -295,15 +295,165 @@ void b2b_mlp_kernel(B2BParams p) {
   }
 }
 
+// Whole-row-block form: one workgroup per 128-row block runs the N1 / 256
+// chunks in turn and accumulates the partial second products O_c in
+// registers, in chunk order, so nothing goes through memory.  For the second
+// product a wave takes its 64 rows and half of the N2 output columns over all
+// 256 hidden units of the chunk: its own S half from registers, its wave-
+// column partner's half from LDS.  So each output element has one owner (no
+// reduction across waves), and a wave keeps 64 accumulator registers live
+// across the next chunk's first product.  It needs as many row blocks as
+// the split form has workgroups to fill the chip; the host takes it when the
+// row blocks alone fill every CU.
+template <int N2>
+__global__ __launch_bounds__(MlpS::NT, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void b2b_mlp_whole_kernel(B2BParams p) {
+  using S = MlpS;
+  using L = MlpLayout<N2>;
+  constexpr int NB2 = L::NB2, HB2 = NB2 / 2;        // output blocks: all, per wave column
+  constexpr int OFF_XS = L::W2_BYTES;               // S exchange: [wave 4][bm][bn][s][lane 64][16 B]
+  constexpr int XS_WAVE = S::BM * S::BN * 2 * 1024;
+  static_assert(OFF_XS + 4 * XS_WAVE <= S::SMEM_V2 && S::TM * L::PT_ROWB <= S::SMEM_V2, "LDS budget");
+  __shared__ __attribute__((aligned(16))) char smem[S::SMEM_V2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / S::WN, wn = wave % S::WN;
+  const int lr = lane & 31, lg = lane >> 5;
+  const int rb = blockIdx.x, m0 = rb * S::TM;
+  const int bz = blockIdx.y;
+  const bf16_t* X = p.X + (int64_t)bz * p.sx;
+  const bf16_t* W1 = p.W1 + (int64_t)bz * p.sw1;
+  const bf16_t* W2 = p.W2 + (int64_t)bz * p.sw2;
+  GemmRowsParams g{};
+  g.batch = 1;
+  g.M = p.M;
+  g.N = p.N1;
+  g.K = p.K;
+  g.X = X;
+  g.ldx = p.ldx;
+  g.W = W1;
+  g.ldw = p.ldw1;
+  g.w_nk = 1;
+  g.epi.alpha = 1.0f;
+  g.epi.bias = p.b1;
+
+  // O^T blocks (bm, h): rows wm 64 + bm 32 + lr, output columns (wn HB2 + h) 32 + ...
+  f32x16_t o[S::BM][HB2];
+#pragma unroll
+  for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+    for (int h = 0; h < HB2; ++h)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o[bm][h][i] = 0.0f;
+  char* xs_own = smem + OFF_XS + wave * XS_WAVE + lane * 16;
+  const char* xs_par = smem + OFF_XS + (wm * S::WN + (1 - wn)) * XS_WAVE + lane * 16;
+  const int cn = p.N1 / kMlpHidden;
+  for (int c = 0; c < cn; ++c) {
+    const int h0 = c * kMlpHidden;
+    // ML1 (+ b1) of chunk c; the ring's final barrier also means every wave
+    // finished the previous chunk's second product.  The row offset is opaque
+    // to the compiler here, so the ring's X addresses are formed per chunk
+    // instead of being hoisted and kept live (spilled) across the loop.
+    int m0c = m0;
+    asm volatile("" : "+s"(m0c));
+    f32x16_t acc[S::BM][S::BN];
+    mainloop_v2<S, false, true>(acc, X, W1, g, m0c, h0, 0, smem, lane, wave, wm, wn, p.b1 != nullptr);
+    // W2^T chunk to LDS (layout as in the split form)
+#pragma unroll
+    for (int j = 0; j < L::W2_LOADS / S::NW; ++j) {
+      const int ld = wave + j * S::NW;
+      const int r = 2 * ld + (lane >> 5);
+      const int q = (lane & 31) ^ (r & 15);
+      dma16(W2 + (int64_t)r * p.ldw2 + h0 + q * 8, smem + ld * 1024);
+    }
+    // Epi1: S = ReLU(P + b1), packed bf16 (hidden units wn 128 + bn 32 +
+    // 16 s + 8 lg + 0..7 of the chunk), and to the partner through LDS
+    u32x4_t sf[S::BM][S::BN][2];
+#pragma unroll
+    for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+      for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+#pragma unroll
+          for (int w = 0; w < 4; ++w)
+            sf[bm][bn][s][w] = pack_bf16x2(fmaxf(acc[bm][bn][8 * s + 2 * w], 0.0f),
+                                           fmaxf(acc[bm][bn][8 * s + 2 * w + 1], 0.0f));
+          lds_write16(xs_own + ((bm * S::BN + bn) * 2 + s) * 1024, sf[bm][bn][s]);
+        }
+    wait_vmcnt<0>();
+    __syncthreads();
+    // ML2: O += S_c W2_c over all 256 hidden units of the chunk, half e of
+    // them (e = wn: own registers, else the partner's LDS copy)
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int bn = 0; bn < S::BN; ++bn)
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          const int q = (e * S::WTN + bn * 32 + 16 * s + 8 * lg) / 8;
+          u32x4_t a[HB2], b[S::BM];
+#pragma unroll
+          for (int h = 0; h < HB2; ++h) {
+            const int r = (wn * HB2 + h) * 32 + lr;
+            a[h] = lds_read16(smem + r * L::W2_ROWB + ((q ^ (r & 15)) << 4));
+          }
+#pragma unroll
+          for (int bm = 0; bm < S::BM; ++bm)
+            b[bm] = e == wn ? sf[bm][bn][s] : lds_read16(xs_par + ((bm * S::BN + bn) * 2 + s) * 1024);
+#pragma unroll
+          for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+            for (int h = 0; h < HB2; ++h) Mma<bf16_t>::run(o[bm][h], a[h], b[bm]);
+        }
+  }
+  __syncthreads();   // every wave is done with the W2^T chunk and the S exchange
+
+  // O to LDS, row-major fp32 with 16-byte chunk q of row r at position
+  // q ^ (r & 31); element 4 gq + e of block (bm, h): row wm 64 + bm 32 + lr,
+  // column (wn HB2 + h) 32 + 8 gq + 4 lg + e.
+  auto pt_at = [&](int r, int q) { return smem + r * L::PT_ROWB + ((q ^ (r & 31)) << 4); };
+#pragma unroll
+  for (int bm = 0; bm < S::BM; ++bm)
+#pragma unroll
+    for (int h = 0; h < HB2; ++h)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq)
+        *reinterpret_cast<f32x4_t*>(pt_at(wm * S::WTM + bm * 32 + lr, (wn * HB2 + h) * 8 + 2 * gq + lg)) =
+            f32x4_t{o[bm][h][4 * gq], o[bm][h][4 * gq + 1], o[bm][h][4 * gq + 2], o[bm][h][4 * gq + 3]};
+  __syncthreads();
+  // O + b2 (ReLU) as bf16 rows: thread t takes column quad t % QPR of rows
+  // (t + 256 j) / QPR, so every wave-wide store covers two whole rows.
+  constexpr int QPR = N2 / 4;
+  constexpr int QUADS = S::TM * QPR / S::NT;
+  static_assert(S::NT % QPR == 0, "a thread's column quad is the same in every step");
+  const int q4 = tid % QPR;
+  uint16_t* O = p.O + (int64_t)bz * p.so;
+  f32x4_t bb = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (p.b2) bb = *reinterpret_cast<const f32x4_t*>(p.b2 + 4 * q4);
+#pragma unroll
+  for (int j = 0; j < QUADS; ++j) {
+    const int r = (tid + j * S::NT) / QPR, m = m0 + r;
+    if (m >= p.M) continue;
+    f32x4_t y = *reinterpret_cast<const f32x4_t*>(pt_at(r, q4));
+    if (p.b2) y += bb;
+    if (p.out_relu)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = fmaxf(y[e], 0.0f);
+    const u32x2_t o2 = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
+    __builtin_nontemporal_store(o2, reinterpret_cast<u32x2_t*>(O + (int64_t)m * p.ldo + 4 * q4));
+  }
+}
+
 bool b2b_mlp_supported(int K, int N1, int N2) {
   return N2 == 128 && N1 % kMlpHidden == 0 && N1 > 0 && K % 64 == 0 && K / 64 >= MlpS::STAGES - 1;
 }
 
 hipError_t launch_b2b_mlp(const B2BParams& p, hipStream_t st) {
-  if (!b2b_mlp_supported(p.K, p.N1, p.N2) || p.cn != p.N1 / kMlpHidden) return hipErrorInvalidValue;
+  if (!b2b_mlp_supported(p.K, p.N1, p.N2) || (p.cn != 1 && p.cn != p.N1 / kMlpHidden)) return hipErrorInvalidValue;
   const unsigned rbs = (unsigned)((p.M + kMlpRows - 1) / kMlpRows);
   const dim3 grid(rbs * (unsigned)p.cn, (unsigned)p.batch), block(MlpS::NT);
-  hipLaunchKernelGGL((b2b_mlp_kernel<128>), grid, block, 0, st, p);
+  if (p.cn == 1) hipLaunchKernelGGL((b2b_mlp_whole_kernel<128>), grid, block, 0, st, p);
+  else hipLaunchKernelGGL((b2b_mlp_kernel<128>), grid, block, 0, st, p);
   return hipGetLastError();
 }
 

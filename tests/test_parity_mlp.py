@@ -3,9 +3,12 @@ the DLRM bottom-MLP pattern of Table 2) against the fp64 oracle.
 
 O is bf16: max-abs 2e-2 and rel-RMS 5e-3 (the intermediate S is rounded to
 bf16 as the second product's operand; the oracle keeps it exact).  The hidden
-dimension is split over workgroups in chunks of 256 units; their partial
-second products are summed at commit by the last workgroup of each row block
-to finish, in chunk order, so the result is the same whichever finishes last.
+dimension comes in chunks of 256 units whose partial second products are
+summed in chunk order.  With at least 256 row blocks (batch x 128-row
+blocks) one workgroup per row block runs every chunk; with fewer, the chunks
+are split over workgroups and the last workgroup of each row block to finish
+sums their partials at commit, so the result is the same whichever finishes
+last.
 """
 import numpy as np
 import pytest
@@ -75,6 +78,43 @@ def test_mlp_dlrm_full_size_block_rows():
     ref = O.mlp_b2b(inp.X[rows], inp.W1, inp.b1, inp.W2, inp.b2, out_relu=True)
     assert_close_bf16(Y[rows], ref, "DLRM MLP 65536x1024x512x128")
     assert np.all(Y >= 0.0)
+
+
+def _block_rows(M, seed):
+    # one row in every 128-row block, and every row of the last block
+    nb = (M + 127) // 128
+    rows = np.arange(nb) * 128 + (np.arange(nb) * seed) % 128
+    rows = rows[rows < M]
+    return np.unique(np.concatenate([rows, np.arange((nb - 1) * 128, M)]))
+
+
+def test_mlp_whole_row_block_form():
+    # 257 row blocks (the last one ragged) take the whole-row-block form:
+    # one workgroup runs all 3 chunks of its rows; no workspace is needed
+    inp = I.dlrm_mlp_inputs(seed=8, M=256 * 128 + 77, K=256, N1=768)
+    assert cf.cf_b2bgemm_workspace(cf._b2b_args(batch=1, M=inp.M, K=256, N1=768, N2=128, dtype=cf.CF_BF16,
+                                                mid=cf.CF_MID_RELU_BIAS, out=cf.CF_OUT_STORE)) == 0
+    Y = host(run_mlp(inp, out_relu=True))
+    rows = _block_rows(inp.M, 41)
+    ref = O.mlp_b2b(inp.X[rows], inp.W1, inp.b1, inp.W2, inp.b2, out_relu=True)
+    assert_close_bf16(Y[rows], ref, "MLP whole form 32845x256x768")
+
+
+def test_mlp_whole_row_block_form_batched():
+    # 2 entries x 129 row blocks = 258 >= 256: whole form over a batch, W1
+    # shared, W2 per entry
+    Bn, M, K, N1 = 2, 128 * 128 + 5, 128, 512
+    ins = [I.dlrm_mlp_inputs(seed=30 + b, M=M, K=K, N1=N1) for b in range(Bn)]
+    X = dev(np.stack([t.X for t in ins]))
+    W1t = dev(I.lay_out_weight(ins[0].W1, "nk"))
+    W2t = dev(np.stack([I.lay_out_weight(t.W2, "nk") for t in ins]))
+    Y = cf.b2b_mlp(X, W1t, dev(ins[0].b1, "f32"), W2t, dev(ins[0].b2, "f32"))
+    torch.cuda.synchronize()
+    got = host(Y)
+    rows = _block_rows(M, 23)
+    for b in range(Bn):
+        ref = O.mlp_b2b(ins[b].X[rows], ins[0].W1, ins[0].b1, ins[b].W2, ins[0].b2)
+        assert_close_bf16(got[b][rows], ref, f"MLP whole form batch entry {b}")
 
 
 def test_mlp_shape_change_on_one_workspace():
