@@ -234,12 +234,12 @@ cf_status cf_gemm_subgraph_noalloc(const cf_subgraph_args* a, void* hip_stream);
  * >= 128; b1 [N1] / b2 [N2] fp32 or NULL; out = CF_OUT_STORE or
  * CF_OUT_BIAS_RELU; R, gamma, beta NULL.  N1 is cut into chunks of 256
  * hidden units and the partial second products of the chunks are summed in
- * chunk order (the partial-sum identity of Sec. IV-A).  With
- * batch * ceil(M / 128) >= 256 row blocks, one workgroup per 128-row block
- * runs all chunks and keeps the sum in registers.  With fewer (and
- * N1 > 256), the chunks are split over workgroups, one per chunk and row
- * block (the cross-CTA dataflow of Sec. IV-A), and the last workgroup of a
- * row block to finish sums their partials at commit.
+ * chunk order (the partial-sum identity of Sec. IV-A).  When
+ * batch * ceil(M / 128) * N1 / 256 <= 256 (and N1 > 256), the chunks are
+ * split over workgroups, one per chunk and 128-row block (the cross-CTA
+ * dataflow of Sec. IV-A), and the last workgroup of a row block to finish
+ * sums their partials at commit.  Otherwise one workgroup per row block runs
+ * all chunks and keeps the sum in registers.
  * Workspace: 0 bytes for the FFN, attention, and the MLP unless it splits
  * the chunks; then cf_b2bgemm_workspace() bytes, 16-byte aligned:
  * CF_B2B_WS_HEADER_BYTES of arrival counters (one 32-bit word per batch

@@ -435,9 +435,9 @@ def b2b_ffn(X, W1t, b1, W2t, b2=None, R=None, gamma=None, beta=None, *, eps=1e-5
 def b2b_mlp(X, W1t, b1, W2t, b2=None, *, out_relu=False, out=None, ws=None, stream=None):
     """Fused MLP block O = ReLU(X W1 + b1) W2 + b2 (ReLU(O) with out_relu), the
     DLRM bottom-MLP pattern.  X [M, K] bf16; W1t = W1^T [N1, K]; W2t = W2^T
-    [N2, N1]; hidden units in chunks of 256, all run by one workgroup per
-    128-row block from 256 row blocks up, else split over workgroups and
-    summed through the workspace.  Batched as b2b_ffn: X, out [B, M, .],
+    [N2, N1]; hidden units in chunks of 256, split over workgroups and summed
+    through the workspace while that grid fits 256 workgroups, else all run
+    by one workgroup per 128-row block.  Batched as b2b_ffn: X, out [B, M, .],
     weights 3-D (per entry) or 2-D (shared)."""
     torch = _torch()
     B, M, K, ldx, sx = _stack(X)

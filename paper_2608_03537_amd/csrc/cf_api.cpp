@@ -708,14 +708,17 @@ cf_status cf_workspace_check(void* workspace, size_t ws_bytes, void* hip_stream)
   }
 }
 
-// MLP form.  With at least kMlpWholeRowBlocks row blocks (one per CU of a
-// 256-CU device) one workgroup per row block runs all chunks and needs no
-// workspace; below that the hidden chunks are split over workgroups, so the
-// grid still fills the device, and their partial products meet in the
-// workspace.  The rule depends on the arguments only.
-static constexpr int64_t kMlpWholeRowBlocks = 256;
+// MLP form.  The hidden chunks are split over workgroups (their partial
+// products meeting in the workspace) when the split grid fits one generation
+// of a 256-CU device, one workgroup per CU; otherwise one workgroup per row
+// block runs all chunks and needs no workspace.  Measured at K = 1024,
+// N1 = 512: split 28-32 us against 37-39 us at 96-128 row blocks, whole
+// 42-53 us against 51-62 us at 160-255.  The rule depends on the arguments
+// only.
+static constexpr int64_t kMlpSplitMaxWorkgroups = 256;
 static bool mlp_split(const cf_b2b_args* a) {
-  return a->N1 > kMlpHidden && a->batch * ((a->M + kMlpRows - 1) / kMlpRows) < kMlpWholeRowBlocks;
+  return a->N1 > kMlpHidden &&
+         a->batch * ((a->M + kMlpRows - 1) / kMlpRows) * (a->N1 / kMlpHidden) <= kMlpSplitMaxWorkgroups;
 }
 
 // Workspace of the split MLP: the fixed counter region (words [batch][row
@@ -730,7 +733,7 @@ static size_t mlp_workspace(const cf_b2b_args* a) {
   const int64_t cn = a->N1 / kMlpHidden;
   return kMlpCounterBytes + (size_t)(a->batch * cn * a->M * a->N2 * 4);
 }
-static_assert(kMlpWholeRowBlocks <= kMlpMaxRowBlocks, "split MLP counters");
+static_assert(kMlpSplitMaxWorkgroups <= kMlpMaxRowBlocks, "split MLP counters");
 
 size_t cf_b2bgemm_workspace(const cf_b2b_args* a) {
   try {

@@ -229,16 +229,18 @@ def test_mlp_workspace_and_validation():
     assert B2B_HDR == cf.CF_B2B_WS_HEADER_BYTES
     assert cf.cf_b2bgemm_workspace(_mlp()) == B2B_HDR + 2 * 300 * 128 * 4
     assert cf.cf_b2bgemm_workspace(_mlp(batch=3, M=1000, N1=1024)) == B2B_HDR + 3 * 4 * 1000 * 128 * 4
-    # from 256 row blocks (batch entries x 128-row blocks) one workgroup per
-    # row block runs every chunk: no workspace, so none is checked
-    assert cf.cf_b2bgemm_workspace(_mlp(M=128 * 255)) == B2B_HDR + 2 * 128 * 255 * 128 * 4
-    assert cf.cf_b2bgemm_workspace(_mlp(M=128 * 255 + 1)) == 0
-    assert cf.cf_b2bgemm_workspace(_mlp(batch=2, M=128 * 127 + 1)) == 0
-    assert cf.cf_b2bgemm_workspace(_mlp(batch=2, M=128 * 127)) == B2B_HDR + 2 * 2 * 128 * 127 * 128 * 4
+    # the split grid (batch x 128-row blocks x chunks) fits 256 workgroups;
+    # beyond, one workgroup per row block runs every chunk: no workspace
+    assert cf.cf_b2bgemm_workspace(_mlp(M=128 * 128)) == B2B_HDR + 2 * 128 * 128 * 128 * 4
+    assert cf.cf_b2bgemm_workspace(_mlp(M=128 * 128 + 1)) == 0
+    assert cf.cf_b2bgemm_workspace(_mlp(batch=2, M=128 * 64 + 1)) == 0
+    assert cf.cf_b2bgemm_workspace(_mlp(batch=2, M=128 * 64)) == B2B_HDR + 2 * 2 * 128 * 64 * 128 * 4
+    assert cf.cf_b2bgemm_workspace(_mlp(M=128 * 64, N1=1024)) == B2B_HDR + 4 * 128 * 64 * 128 * 4
+    assert cf.cf_b2bgemm_workspace(_mlp(M=128 * 64 + 1, N1=1024)) == 0
     big = _mlp(batch=3, M=128 * 87382)
     big.sx, big.so = big.M * big.K, big.M * big.N2
     assert cf.cf_b2bgemm_workspace(big) == 0
-    assert cf.STATUS[cf.cf_b2bgemm(_mlp(M=128 * 255), A, 1, None)] == "CF_ERR_WORKSPACE"
+    assert cf.STATUS[cf.cf_b2bgemm(_mlp(M=128 * 128), A, 1, None)] == "CF_ERR_WORKSPACE"
     assert cf.cf_b2bgemm_workspace(_mlp(N1=256)) == 0           # one chunk: nothing to sum
     assert cf.STATUS[cf.cf_b2bgemm(_mlp(), None, 0, None)] == "CF_ERR_WORKSPACE"
     assert cf.STATUS[cf.cf_b2bgemm(_mlp(N2=64), A, 1 << 30, None)] == "CF_ERR_UNSUPPORTED"

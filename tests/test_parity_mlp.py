@@ -4,11 +4,11 @@ the DLRM bottom-MLP pattern of Table 2) against the fp64 oracle.
 O is bf16: max-abs 2e-2 and rel-RMS 5e-3 (the intermediate S is rounded to
 bf16 as the second product's operand; the oracle keeps it exact).  The hidden
 dimension comes in chunks of 256 units whose partial second products are
-summed in chunk order.  With at least 256 row blocks (batch x 128-row
-blocks) one workgroup per row block runs every chunk; with fewer, the chunks
-are split over workgroups and the last workgroup of each row block to finish
-sums their partials at commit, so the result is the same whichever finishes
-last.
+summed in chunk order.  While batch x 128-row blocks x chunks fits 256
+workgroups the chunks are split over workgroups and the last workgroup of
+each row block to finish sums their partials at commit, so the result is
+the same whichever finishes last; beyond that one workgroup per row block
+runs every chunk.
 """
 import numpy as np
 import pytest
@@ -89,8 +89,8 @@ def _block_rows(M, seed):
 
 
 def test_mlp_whole_row_block_form():
-    # 257 row blocks (the last one ragged) take the whole-row-block form:
-    # one workgroup runs all 3 chunks of its rows; no workspace is needed
+    # 257 row blocks (the last one ragged) x 3 chunks: the whole-row-block
+    # form, one workgroup runs all 3 chunks of its rows; no workspace
     inp = I.dlrm_mlp_inputs(seed=8, M=256 * 128 + 77, K=256, N1=768)
     assert cf.cf_b2bgemm_workspace(cf._b2b_args(batch=1, M=inp.M, K=256, N1=768, N2=128, dtype=cf.CF_BF16,
                                                 mid=cf.CF_MID_RELU_BIAS, out=cf.CF_OUT_STORE)) == 0
@@ -101,7 +101,7 @@ def test_mlp_whole_row_block_form():
 
 
 def test_mlp_whole_row_block_form_batched():
-    # 2 entries x 129 row blocks = 258 >= 256: whole form over a batch, W1
+    # 2 entries x 129 row blocks x 2 chunks: the whole form over a batch, W1
     # shared, W2 per entry
     Bn, M, K, N1 = 2, 128 * 128 + 5, 128, 512
     ins = [I.dlrm_mlp_inputs(seed=30 + b, M=M, K=K, N1=N1) for b in range(Bn)]
@@ -118,11 +118,12 @@ def test_mlp_whole_row_block_form_batched():
 
 
 def test_mlp_shape_change_on_one_workspace():
-    """Calls of different shapes share a workspace: the second call has more
-    row blocks (more arrival counters) than the first, and the first call's
-    partials must not be read as the second call's counters."""
+    """Calls of different shapes share a workspace (all three take the split
+    form): the second call has more row blocks (more arrival counters) than
+    the first, and the first call's partials must not be read as the second
+    call's counters."""
     ws = torch.zeros(96 << 20, dtype=torch.uint8, device="cuda")
-    for M, K, N1 in [(16384, 128, 1024), (40000, 128, 512), (300, 256, 768)]:
+    for M, K, N1 in [(8192, 128, 1024), (16000, 128, 512), (300, 256, 768)]:
         inp = I.dlrm_mlp_inputs(seed=6, M=M, K=K, N1=N1)
         got = host(run_mlp(inp, ws=ws))
         assert_close_bf16(got, O.mlp_b2b(inp.X, inp.W1, inp.b1, inp.W2, inp.b2), f"MLP {M}x{K}x{N1} after another shape")
