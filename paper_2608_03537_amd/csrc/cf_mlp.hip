@@ -349,8 +349,9 @@ void b2b_mlp_whole_kernel(B2BParams p) {
   const int cn = p.N1 / kMlpHidden;
   for (int c = 0; c < cn; ++c) {
     const int h0 = c * kMlpHidden;
-    // ML1 (+ b1) of chunk c; the ring's final barrier also means every wave
-    // finished the previous chunk's second product.  The row offset is opaque
+    // ML1 (+ b1) of chunk c.  Its ring prologue writes LDS at once: the
+    // barrier that ends the previous chunk keeps it behind every wave's
+    // reads of that chunk's W2^T and S exchange.  The row offset is opaque
     // to the compiler here, so the ring's X addresses are formed per chunk
     // instead of being hoisted and kept live (spilled) across the loop.
     int m0c = m0;
@@ -405,8 +406,8 @@ void b2b_mlp_whole_kernel(B2BParams p) {
 #pragma unroll
             for (int h = 0; h < HB2; ++h) Mma<bf16_t>::run(o[bm][h], a[h], b[bm]);
         }
+    __syncthreads();   // every wave is done with the W2^T chunk and the S exchange
   }
-  __syncthreads();   // every wave is done with the W2^T chunk and the S exchange
 
   // O to LDS, row-major fp32 with 16-byte chunk q of row r at position
   // q ^ (r & 31); element 4 gq + e of block (bm, h): row wm 64 + bm 32 + lr,
