@@ -385,12 +385,12 @@ __global__ __launch_bounds__(256, 2) void b2b_attention_kernel(B2BParams p) {
     lds_sync();
     // Load q of the next block (K for q < NINS, then V) after MFMA 2 q + 1.
     auto loads = [&](auto full_t) {
-      return [&, full_t](auto i_t) {
+      using FT = decltype(full_t);
+      return [&](auto i_t) {
         constexpr int i = decltype(i_t)::value;
         if constexpr (i % 2 == 1 && i / 2 < 2 * NINS) {
           constexpr bool VS = i / 2 >= NINS;
-          issue_one(j + 1, next_t, std::integral_constant<bool, VS>{}, VS ? i / 2 - NINS : i / 2,
-                    decltype(full_t)::value);
+          issue_one(j + 1, next_t, std::integral_constant<bool, VS>{}, VS ? i / 2 - NINS : i / 2, FT::value);
         }
       };
     };
