@@ -109,8 +109,11 @@ def run_attn(Q, K, V, scale=None):
     return host(o)
 
 
+# Ragged Lk puts the partial last key block in either ring stage: with an odd
+# block count (300, 289 keys) it is loaded from stage 1's step, with an even
+# one (333, 350) from stage 0's, for both head dimensions.
 @pytest.mark.parametrize("B,H,Lq,Lk,d", [(1, 2, 200, 300, 64), (2, 1, 129, 64, 128), (1, 3, 64, 1, 128),
-                                         (1, 1, 256, 333, 128)])
+                                         (1, 1, 256, 333, 128), (1, 2, 130, 289, 128), (1, 1, 100, 350, 64)])
 def test_attention_small(B, H, Lq, Lk, d):
     a = I.attention_inputs(seed=5, B=B, H=H, Lq=Lq, Lk=Lk, d=d)
     got = run_attn(a.Q, a.K, a.V)
