@@ -54,7 +54,10 @@ __device__ __forceinline__ u32x4_t ds_read_b128_at(uint32_t addr) {
   return v;
 }
 // Wait until at most N LDS operations of this wave are outstanding; v is tied
-// to the wait so that its uses cannot move above it.
+// to the wait so that its uses cannot move above it.  The count is exact only
+// while no scalar memory load is in flight (they share the counter and return
+// out of order): the kernel's loop issues none, and each step begins with a
+// full wait (lds_sync).
 template <int N>
 __device__ __forceinline__ void lgkm_wait(u32x4_t& v) {
   asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(v) : "i"(N));
