@@ -100,6 +100,21 @@ def test_mlp_whole_row_block_form():
     assert_close_bf16(Y[rows], ref, "MLP whole form 32845x256x768")
 
 
+def test_mlp_whole_row_block_form_is_deterministic():
+    # the chunks' partial products are summed in registers in chunk order:
+    # repeated calls give the same bits
+    inp = I.dlrm_mlp_inputs(seed=9, M=200 * 128 + 3, K=128, N1=512)
+    X, W1, W2 = dev(inp.X), dev(I.lay_out_weight(inp.W1, "nk")), dev(I.lay_out_weight(inp.W2, "nk"))
+    b1, b2 = dev(inp.b1, "f32"), dev(inp.b2, "f32")
+    outs = [cf.b2b_mlp(X, W1, b1, W2, b2, out_relu=True) for _ in range(3)]
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
+    rows = _block_rows(inp.M, 17)
+    ref = O.mlp_b2b(inp.X[rows], inp.W1, inp.b1, inp.W2, inp.b2, out_relu=True)
+    assert_close_bf16(host(outs[0])[rows], ref, "MLP whole form 25603x128x512")
+
+
 def test_mlp_whole_row_block_form_batched():
     # 2 entries x 129 row blocks x 2 chunks: the whole form over a batch, W1
     # shared, W2 per entry
